@@ -1,0 +1,560 @@
+"""Pins for the CPU oracle: checks against what the paper and the mathematics fix
+(hand-derived worked examples, closed forms, the paper's lemmas and theorem,
+special cases and brute force), never against a retyping of the oracle itself."""
+import ast
+import itertools
+import operator
+import os
+
+import numpy as np
+import pytest
+from scipy.special import logsumexp
+
+import oracle
+from paper_2608_12913_amd import synth
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+# ---------------------------------------------------------------- helpers
+def _num(expr: str) -> float:
+    """Evaluate a closed-form number written with + - * / ** and literals only."""
+    ops = {ast.Add: operator.add, ast.Sub: operator.sub, ast.Mult: operator.mul,
+           ast.Div: operator.truediv, ast.Pow: operator.pow, ast.USub: operator.neg}
+
+    def ev(n):
+        if isinstance(n, ast.Expression):
+            return ev(n.body)
+        if isinstance(n, ast.Constant) and isinstance(n.value, (int, float)):
+            return float(n.value)
+        if isinstance(n, ast.BinOp):
+            return ops[type(n.op)](ev(n.left), ev(n.right))
+        if isinstance(n, ast.UnaryOp):
+            return ops[type(n.op)](ev(n.operand))
+        raise ValueError(expr)
+
+    return ev(ast.parse(expr.strip(), mode="eval"))
+
+
+def _rows(fname):
+    with open(os.path.join(GOLDEN, fname)) as f:
+        for line in f:
+            line = line.strip()
+            if line and not line.startswith("#"):
+                yield [c.strip() for c in line.split(";")]
+
+
+def _bias_only_case(logp, logq):
+    """Inputs whose logits are exactly the given fp32 biases (hidden states zero).
+    The two models get separate bias vectors through separate cases of W = 0."""
+    V = len(logp)
+    d = 8
+    hp = np.zeros((1, d), np.float32)
+    hq = np.zeros((1, d), np.float32)
+    wp = np.zeros((V, d), np.float32)
+    wq = np.zeros((V, d), np.float32)
+    return hp, hq, wp, wq, np.asarray(logp, np.float32), np.asarray(logq, np.float32)
+
+
+def _random_problem(rng, V, dp, dq, R, scale=1.0):
+    hp = rng.standard_normal((R, dp)).astype(np.float32) * np.float32(scale)
+    hq = rng.standard_normal((R, dq)).astype(np.float32) * np.float32(scale)
+    wp = rng.standard_normal((V, dp)).astype(np.float32) / np.float32(np.sqrt(dp))
+    wq = rng.standard_normal((V, dq)).astype(np.float32) / np.float32(np.sqrt(dq))
+    bias = (-np.log(np.arange(V) + 1.0)).astype(np.float32)
+    return hp, hq, wp, wq, bias
+
+
+def _softmax_log(z):
+    return z - logsumexp(z, axis=-1, keepdims=True)
+
+
+# ---------------------------------------------------------------- LM-head logits
+def test_logits_exact_small_integers():
+    """Small-integer weights and hidden states: every product and partial sum is an
+    exact integer, so the oracle's logits must equal exact integer arithmetic."""
+    rng = np.random.default_rng(1)
+    V, dp, dq, R = 37, 24, 16, 5  # non-square so a transposed operand cannot pass
+    hp = rng.integers(-2, 3, (R, dp)).astype(np.float32)
+    hq = rng.integers(-2, 3, (R, dq)).astype(np.float32)
+    wp = rng.integers(-2, 3, (V, dp)).astype(np.float32)
+    wq = rng.integers(-2, 3, (V, dq)).astype(np.float32)
+    bp = rng.integers(-3, 4, V).astype(np.float32)
+    bq = rng.integers(-3, 4, V).astype(np.float32)
+    out = oracle.eval_rows(hp, hq, wp, wq, bp, bq, theta=0.1, s=0.5, want_logits=True)
+    exact_p = hp.astype(np.int64) @ wp.astype(np.int64).T + bp.astype(np.int64)
+    exact_q = hq.astype(np.int64) @ wq.astype(np.int64).T + bq.astype(np.int64)
+    assert np.array_equal(out["zp"], exact_p.astype(np.float64))
+    assert np.array_equal(out["zq"], exact_q.astype(np.float64))
+
+
+def test_logits_one_hot_hidden_state_selects_weight_column():
+    rng = np.random.default_rng(2)
+    V, dp, dq = 29, 12, 8
+    wp = rng.standard_normal((V, dp)).astype(np.float32)
+    wq = rng.standard_normal((V, dq)).astype(np.float32)
+    b = rng.standard_normal(V).astype(np.float32)
+    kp, kq = [3, 0, 11], [7, 2, 5]
+    hp = np.zeros((3, dp), np.float32)
+    hq = np.zeros((3, dq), np.float32)
+    for r in range(3):
+        hp[r, kp[r]] = 1.0
+        hq[r, kq[r]] = 1.0
+    out = oracle.eval_rows(hp, hq, wp, wq, b, b, theta=0.0, s=0.5, want_logits=True)
+    for r in range(3):
+        assert np.array_equal(out["zp"][r], wp[:, kp[r]].astype(np.float64) + b)
+        assert np.array_equal(out["zq"][r], wq[:, kq[r]].astype(np.float64) + b)
+
+
+def test_temperature_divides_logits():
+    rng = np.random.default_rng(3)
+    hp, hq, wp, wq, b = _random_problem(rng, 50, 16, 8, 2)
+    o1 = oracle.eval_rows(hp, hq, wp, wq, b, b, theta=0.0, s=0.5, want_logits=True)
+    o2 = oracle.eval_rows(hp, hq, wp, wq, b, b, theta=0.0, s=0.5, temperature=2.0,
+                          want_logits=True)
+    np.testing.assert_allclose(o2["zp"], o1["zp"] / 2.0, rtol=0, atol=1e-14)
+
+
+# ---------------------------------------------------------------- log-softmax
+def test_lse_matches_library_logsumexp():
+    rng = np.random.default_rng(4)
+    hp, hq, wp, wq, b = _random_problem(rng, 1031, 32, 16, 4, scale=4.0)
+    out = oracle.eval_rows(hp, hq, wp, wq, b, b, theta=0.1, s=0.5, want_logits=True)
+    np.testing.assert_allclose(out["stats"][:, oracle.RS_LSEP], logsumexp(out["zp"], axis=1),
+                               rtol=1e-13, atol=1e-12)
+    np.testing.assert_allclose(out["stats"][:, oracle.RS_LSEQ], logsumexp(out["zq"], axis=1),
+                               rtol=1e-13, atol=1e-12)
+    np.testing.assert_array_equal(out["stats"][:, oracle.RS_MAXP], out["zp"].max(axis=1))
+    total = np.exp(out["zp"] - out["stats"][:, [oracle.RS_LSEP]]).sum(axis=1)
+    np.testing.assert_allclose(total, 1.0, atol=1e-12)
+
+
+# ---------------------------------------------------------------- contrastive target
+@pytest.mark.parametrize("row", list(_rows("cd_worked_examples.txt")), ids=lambda r: r[0])
+def test_cd_worked_examples(row):
+    name, s, theta, pp, pq, pcd, amax, count = row
+    pi_p = np.array([_num(x) for x in pp.split(",")])
+    pi_q = np.array([_num(x) for x in pq.split(",")])
+    expect = np.array([_num(x) for x in pcd.split(",")])
+    hp, hq, wp, wq, bp, bq = _bias_only_case(np.log(pi_p), np.log(pi_q))
+    out = oracle.eval_rows(hp, hq, wp, wq, bp, bq, theta=float(theta), s=float(s),
+                           want_lpcd=True)
+    got = np.exp(out["lpcd"][0])
+    np.testing.assert_allclose(got, expect, atol=2e-7)
+    assert int(out["argmax"][0]) == int(amax)
+    assert int(out["stats"][0, oracle.RS_COUNT]) == int(count)
+    assert np.all(np.isneginf(out["lpcd"][0][expect == 0]))
+
+
+def test_contrast_zero_gives_masked_expert():
+    """s = 0: pi_CD is the expert restricted to the mask and renormalised, and its
+    argmax is the expert argmax (the paper's alpha = 0 reduction)."""
+    rng = np.random.default_rng(5)
+    hp, hq, wp, wq, b = _random_problem(rng, 777, 24, 16, 6, scale=4.0)
+    for theta in (0.0, 0.1, 0.5):
+        out = oracle.eval_rows(hp, hq, wp, wq, b, b, theta=theta, s=0.0, want_logits=True,
+                               want_lpcd=True)
+        lp_p = _softmax_log(out["zp"])
+        pi_p = np.exp(lp_p)
+        mask = pi_p >= theta * pi_p.max(axis=1, keepdims=True)
+        expect = np.where(mask, lp_p - np.log(np.where(mask, pi_p, 0).sum(1, keepdims=True)),
+                          -np.inf)
+        np.testing.assert_allclose(out["lpcd"], expect, atol=1e-10)
+        assert np.array_equal(out["argmax"], out["zp"].argmax(axis=1))
+
+
+def test_identical_amateur_gives_expert_for_every_strength():
+    rng = np.random.default_rng(6)
+    hp, _, wp, _, b = _random_problem(rng, 300, 16, 16, 3, scale=4.0)
+    for s in (0.0, 0.5, 1.0, 3.0):
+        out = oracle.eval_rows(hp, hp, wp, wp, b, b, theta=0.0, s=s, want_logits=True,
+                               want_lpcd=True)
+        np.testing.assert_allclose(out["lpcd"], _softmax_log(out["zp"]), atol=1e-10)
+
+
+def test_kl_decomposition_lemma():
+    """Lemma (KL divergence to target), untruncated target:
+    KL(p||cd) = log Z - s KL(p||q); KL(q||cd) = log Z + (1+s) KL(q||p);
+    KL(e||cd) = log Z + (1+s) KL(e||p) - s KL(e||q), with Z = sum p^(1+s) q^(-s)."""
+    rng = np.random.default_rng(7)
+    hp, hq, wp, wq, b = _random_problem(rng, 500, 24, 16, 4, scale=2.0)
+    for s in (0.25, 0.5, 1.0):
+        out = oracle.eval_rows(hp, hq, wp, wq, b, b, theta=0.0, s=s, want_logits=True,
+                               want_lpcd=True)
+        lp, lq, lc = _softmax_log(out["zp"]), _softmax_log(out["zq"]), out["lpcd"]
+        le = _softmax_log(rng.standard_normal(lp.shape) * 2.0)
+        logZ = out["stats"][:, oracle.RS_LOGZ]
+        kl = lambda la, lb: (np.exp(la) * (la - lb)).sum(axis=1)  # noqa: E731
+        np.testing.assert_allclose(kl(lp, lc), logZ - s * kl(lp, lq), atol=1e-9)
+        np.testing.assert_allclose(kl(lq, lc), logZ + (1 + s) * kl(lq, lp), atol=1e-9)
+        np.testing.assert_allclose(kl(le, lc), logZ + (1 + s) * kl(le, lp) - s * kl(le, lq),
+                                   atol=1e-9)
+        # Z itself: log sum p^(1+s) q^(-s)
+        np.testing.assert_allclose(logZ, logsumexp((1 + s) * lp - s * lq, axis=1), atol=1e-11)
+
+
+def test_reconstruction_error_lemma():
+    """Lemma (reconstruction error decomposition): recombining approximations
+    pi_e ~ pi_p and pi_f ~ pi_q gives an exponential tilt of pi_CD by
+    Delta = (1+s) eps_p - s eps_q, normalised by E_{pi_CD}[exp(Delta)]."""
+    rng = np.random.default_rng(8)
+    V, d = 400, 16
+    hp, hq, wp, wq, b = _random_problem(rng, V, d, d, 2, scale=3.0)
+    # approximating heads: perturbed copies of the true heads
+    we = (wp + 0.3 * rng.standard_normal(wp.shape) / np.sqrt(d)).astype(np.float32)
+    wf = (wq + 0.3 * rng.standard_normal(wq.shape) / np.sqrt(d)).astype(np.float32)
+    s = 0.7
+    true = oracle.eval_rows(hp, hq, wp, wq, b, b, theta=0.0, s=s, want_logits=True,
+                            want_lpcd=True)
+    appr = oracle.eval_rows(hp, hq, we, wf, b, b, theta=0.0, s=s, want_logits=True,
+                            want_lpcd=True)
+    eps_p = _softmax_log(appr["zp"]) - _softmax_log(true["zp"])
+    eps_q = _softmax_log(appr["zq"]) - _softmax_log(true["zq"])
+    delta = (1 + s) * eps_p - s * eps_q
+    pi_cd = np.exp(true["lpcd"])
+    z_delta = (pi_cd * np.exp(delta)).sum(axis=1, keepdims=True)
+    np.testing.assert_allclose(np.exp(appr["lpcd"]), pi_cd * np.exp(delta) / z_delta,
+                               rtol=1e-9, atol=1e-15)
+
+
+def test_full_threshold_is_one_hot_at_expert_argmax():
+    rng = np.random.default_rng(9)
+    hp, hq, wp, wq, b = _random_problem(rng, 333, 16, 16, 5, scale=4.0)
+    for s in (0.0, 0.5, 2.0):
+        out = oracle.eval_rows(hp, hq, wp, wq, b, b, theta=1.0, s=s, want_logits=True,
+                               want_lpcd=True)
+        amax_p = out["zp"].argmax(axis=1)
+        assert np.array_equal(out["argmax"], amax_p)
+        assert np.all(out["stats"][:, oracle.RS_COUNT] == 1)
+        pi = np.exp(out["lpcd"])
+        np.testing.assert_array_equal(pi, np.eye(333)[amax_p])
+        assert np.all(np.isinf(out["stats"][:, oracle.RS_MARGIN]))
+
+
+@pytest.mark.parametrize("theta", [0.0, 0.01, 0.1, 0.5])
+def test_mask_normalisation_and_support(theta):
+    rng = np.random.default_rng(10)
+    hp, hq, wp, wq, b = _random_problem(rng, 1024, 32, 16, 6, scale=4.0)
+    out = oracle.eval_rows(hp, hq, wp, wq, b, b, theta=theta, s=0.5, want_logits=True,
+                           want_lpcd=True)
+    pi_p = np.exp(_softmax_log(out["zp"]))
+    mask = pi_p >= theta * pi_p.max(axis=1, keepdims=True)
+    # membership away from the exact cutoff (within 1e-9 the log/linear forms may differ)
+    clear = np.abs(pi_p - theta * pi_p.max(axis=1, keepdims=True)) > 1e-9 * pi_p.max()
+    assert np.array_equal(np.isfinite(out["lpcd"]) & clear, mask & clear)
+    np.testing.assert_allclose(np.exp(out["lpcd"]).sum(axis=1), 1.0, atol=1e-12)
+    np.testing.assert_array_equal(out["stats"][:, oracle.RS_COUNT], np.isfinite(out["lpcd"]).sum(1))
+
+
+def test_argmax_and_margin_by_full_sort():
+    rng = np.random.default_rng(11)
+    hp, hq, wp, wq, b = _random_problem(rng, 97, 16, 8, 20, scale=4.0)
+    out = oracle.eval_rows(hp, hq, wp, wq, b, b, theta=0.05, s=0.8, want_lpcd=True)
+    for r in range(20):
+        lc = out["lpcd"][r]
+        order = np.argsort(-lc, kind="stable")  # descending, lowest id first on ties
+        assert out["argmax"][r] == order[0]
+        logZ = out["stats"][r, oracle.RS_LOGZ]
+        assert abs(out["stats"][r, oracle.RS_TOP1] - (lc[order[0]] + logZ)) < 1e-12
+        if np.isfinite(lc[order[1]]):
+            np.testing.assert_allclose(out["stats"][r, oracle.RS_MARGIN], lc[order[0]] - lc[order[1]],
+                                       atol=1e-12)
+
+
+def test_flat_logits_tie_breaks_to_lowest_id():
+    V, d = 64, 8
+    z = np.zeros((1, d), np.float32)
+    w = np.zeros((V, d), np.float32)
+    out = oracle.eval_rows(z, z, w, w, None, None, theta=0.1, s=0.5, want_lpcd=True)
+    assert out["argmax"][0] == 0
+    assert out["stats"][0, oracle.RS_COUNT] == V
+    np.testing.assert_allclose(np.exp(out["lpcd"][0]), 1.0 / V, atol=1e-15)
+    assert out["stats"][0, oracle.RS_MARGIN] == 0.0
+
+
+def test_contrastive_signal_statistic():
+    """Row slot 7 is log pi_p(x*) - log pi_q(x*) at the CD argmax x*."""
+    rng = np.random.default_rng(12)
+    hp, hq, wp, wq, b = _random_problem(rng, 200, 16, 8, 4, scale=4.0)
+    out = oracle.eval_rows(hp, hq, wp, wq, b, b, theta=0.1, s=0.5, want_logits=True)
+    lp, lq = _softmax_log(out["zp"]), _softmax_log(out["zq"])
+    a = out["argmax"]
+    np.testing.assert_allclose(out["stats"][:, oracle.RS_SIGNAL],
+                               lp[np.arange(4), a] - lq[np.arange(4), a], atol=1e-12)
+
+
+# ---------------------------------------------------------------- greedy walk
+def _parse_ints(s):
+    return np.array([int(x) for x in s.split(",")], np.int32)
+
+
+@pytest.mark.parametrize("row", list(_rows("greedy_walk_examples.txt")), ids=lambda r: r[0])
+def test_greedy_walk_worked_examples(row):
+    name, par, tok, amax, L, path, nxt = row
+    got_L, got_path, got_next = oracle.greedy_walk(_parse_ints(par), _parse_ints(tok),
+                                                   _parse_ints(amax))
+    assert got_L == int(L)
+    assert np.array_equal(got_path, _parse_ints(path))
+    assert got_next == int(nxt)
+
+
+def _brute_force_walk(parents, tokens, amax):
+    """Enumerate every root-to-node path whose every node carries its parent row's
+    argmax; among the maximal ones take the lexicographically smallest node sequence."""
+    N = len(parents)
+    paths = []
+
+    def ext(p):
+        kids = [c for c in range(N) if parents[c] == p[-1] and tokens[c] == amax[p[-1]]]
+        if not kids:
+            paths.append(tuple(p))
+        for c in kids:
+            ext(p + [c])
+
+    ext([0])
+    best = min(paths)
+    return len(best) - 1, best, int(amax[best[-1]])
+
+
+def test_greedy_walk_matches_brute_force_on_random_trees():
+    rng = np.random.default_rng(13)
+    for trial in range(300):
+        N = int(rng.integers(1, 14))
+        parents = np.array([-1] + [int(rng.integers(0, i)) for i in range(1, N)], np.int32)
+        V = int(rng.integers(2, 5))  # tiny vocabulary: many matches and duplicate siblings
+        tokens = rng.integers(0, V, N).astype(np.int32)
+        amax = rng.integers(0, V, N).astype(np.int32)
+        L, path, nxt = oracle.greedy_walk(parents, tokens, amax)
+        bL, bpath, bnext = _brute_force_walk(parents, tokens, amax)
+        assert (L, nxt) == (bL, bnext), trial
+        assert tuple(path[:L + 1]) == bpath and np.all(path[L + 1:] == -1)
+
+
+def _tiny_greedy_case(seed, **kw):
+    case = synth.make_case("tiny_chain8", seed, **kw)
+    rows = oracle.eval_rows(case.hp, case.hq, case.wp, case.wq, case.bias, case.bias,
+                            theta=case.theta, s=case.s)
+    tokens = synth.greedy_tokens(case, rows["argmax"])
+    return case, tokens
+
+
+@pytest.mark.parametrize("tree", ["chain", "tree"])
+def test_accepted_path_is_prefix_of_cd_greedy_continuation(tree):
+    kw = dict(N=24, tree="tree", depth=5, max_children=4) if tree == "tree" else {}
+    for seed in range(5):
+        case, tokens = _tiny_greedy_case(seed, **kw)
+        o = oracle.verify("greedy", case.B, case.N, case.hp, case.hq, case.wp, case.wq, case.bias,
+                          case.bias, case.parents, tokens, theta=case.theta, s=case.s)
+        assert o["status"][0] == oracle.SEQ_OK
+        L, path = int(o["accept_len"][0]), o["accept_path"][0]
+        amax = o["row_argmax"]
+        for k in range(1, L + 1):  # every accepted token is its parent row's CD argmax
+            node, parent = path[k], path[k - 1]
+            assert case.parents[0, node] == parent
+            assert tokens[0, node] == amax[parent]
+        assert o["next_token"][0] == amax[path[L]]
+        # and the walk stopped: no child of the last node carries the argmax
+        last = path[L]
+        kids = [c for c in range(case.N) if case.parents[0, c] == last]
+        assert all(tokens[0, c] != amax[last] for c in kids)
+
+
+def test_masked_tokens_are_never_accepted():
+    case = synth.make_case("tiny_chain8", 3, N=16)
+    rows = oracle.eval_rows(case.hp, case.hq, case.wp, case.wq, case.bias, case.bias,
+                            theta=case.theta, s=case.s, want_lpcd=True)
+    for trial in range(3):
+        # every draft token is chosen OUTSIDE its parent row's mask
+        tokens = np.zeros((1, case.N), np.int32)
+        for i in range(1, case.N):
+            masked = np.flatnonzero(np.isneginf(rows["lpcd"][i - 1]))
+            tokens[0, i] = masked[(7 * i + trial) % len(masked)]
+        o = oracle.verify("greedy", 1, case.N, case.hp, case.hq, case.wp, case.wq, case.bias,
+                          case.bias, case.parents, tokens, theta=case.theta, s=case.s)
+        assert o["accept_len"][0] == 0
+        assert np.all(o["node_stats"][1:, oracle.NS_INMASK] == 0)
+        assert np.all(np.isneginf(o["node_stats"][1:, oracle.NS_LPCD]))
+
+
+def test_node_statistics_follow_parent_rows():
+    case, tokens = _tiny_greedy_case(4, N=20, tree="tree", depth=4, max_children=5)
+    o = oracle.verify("greedy", 1, case.N, case.hp, case.hq, case.wp, case.wq, case.bias,
+                      case.bias, case.parents, tokens, theta=case.theta, s=case.s)
+    rows = oracle.eval_rows(case.hp, case.hq, case.wp, case.wq, case.bias, case.bias,
+                            theta=case.theta, s=case.s, want_logits=True, want_lpcd=True)
+    lp, lq = _softmax_log(rows["zp"]), _softmax_log(rows["zq"])
+    ns = o["node_stats"]
+    assert np.all(np.isnan(ns[0]))
+    for i in range(1, case.N):
+        j, x = case.parents[0, i], tokens[0, i]
+        np.testing.assert_allclose(ns[i, :3], [lp[j, x], lq[j, x], 1.5 * lp[j, x] - 0.5 * lq[j, x]],
+                                   atol=1e-12)
+        assert ns[i, oracle.NS_LPCD] == rows["lpcd"][j, x]
+
+
+def test_sequence_status_codes():
+    case, tokens = _tiny_greedy_case(0)
+    args = (case.hp, case.hq, case.wp, case.wq, case.bias, case.bias)
+    par = case.parents.copy()
+    par[0, 3] = 5  # parent after child
+    o = oracle.verify("greedy", 1, case.N, *args, par, tokens, theta=0.1, s=0.5)
+    assert o["status"][0] == oracle.SEQ_BAD_TREE and o["accept_len"][0] == 0
+    assert o["next_token"][0] == -1 and np.all(o["accept_path"][0] == -1)
+    bad = tokens.copy()
+    bad[0, 2] = case.V
+    o = oracle.verify("greedy", 1, case.N, *args, case.parents, bad, theta=0.1, s=0.5)
+    assert o["status"][0] == oracle.SEQ_BAD_TOKEN
+    hp = case.hp.copy()
+    hp[4, 0] = np.inf
+    o = oracle.verify("greedy", 1, case.N, hp, *args[1:], case.parents, tokens, theta=0.1, s=0.5)
+    assert o["status"][0] == oracle.SEQ_NONFINITE
+    tree = synth.make_case("tiny_chain8", 0, N=8, tree="tree", depth=3, max_children=3)
+    probs = np.full((8, case.V), 1.0 / case.V, np.float32)
+    o = oracle.verify("sample", 1, 8, *args, tree.parents, tokens, theta=0.1, s=0.5,
+                      draft_probs=probs, u_acc=case.u_acc, u_res=case.u_res)
+    assert o["status"][0] == oracle.SEQ_NOT_CHAIN
+
+
+# ---------------------------------------------------------------- sampled verification
+def _tiny_target(rng, V, theta, s, N):
+    hp, hq, wp, wq, b = _random_problem(rng, V, 8, 8, N, scale=2.0)
+    out = oracle.eval_rows(hp, hq, wp, wq, b, b, theta=theta, s=s, want_lpcd=True)
+    return out["lpcd"]
+
+
+class _ChainCall:
+    """Repeated calls of the oracle's chain sampler on fixed buffers (fast loop)."""
+
+    def __init__(self, lp_cd, q):
+        import ctypes
+        self.lib = oracle._load()
+        self.N, self.V = lp_cd.shape
+        self.lp = np.ascontiguousarray(lp_cd, np.float64)
+        self.q = np.ascontiguousarray(q, np.float32)
+        self.tok = np.zeros(self.N, np.int32)
+        self.ua = np.full(self.N, 0.5, np.float32)
+        self.ur = np.full(self.N, 0.5, np.float32)
+        self.L = np.zeros(1, np.int32)
+        self.path = np.zeros(self.N, np.int32)
+        self.nxt = np.zeros(1, np.int32)
+        p = lambda a: a.ctypes.data_as(ctypes.c_void_p)  # noqa: E731
+        self.args = (self.N, self.V, p(self.tok), p(self.lp), p(self.q), p(self.ua), p(self.ur),
+                     p(self.L), p(self.path), p(self.nxt), None, None)
+
+    def __call__(self):
+        self.lib.dco_sample_chain(*self.args)
+        return int(self.L[0]), int(self.nxt[0])
+
+
+@pytest.mark.parametrize("theta,s", [(0.0, 0.5), (0.1, 0.5), (0.3, 1.0), (0.0, 0.0)])
+def test_lossless_theorem_by_enumeration(theta, s):
+    """Theorem (lossless property) with the plausibility-mask remark: enumerating every
+    draft token x ~ pi_e and a G x G midpoint grid of (u_acc, u_res), the emitted token
+    is distributed exactly as pi_CD up to the grid resolution."""
+    rng = np.random.default_rng(14)
+    V, G = 6, 128
+    lp_cd = _tiny_target(rng, V, theta, s, 2)
+    target = np.exp(lp_cd[0])
+    proposals = [rng.dirichlet(np.ones(V)), np.eye(V)[int(np.argmin(target))],
+                 np.full(V, 1.0 / V), np.r_[0.0, rng.dirichlet(np.ones(V - 1))]]
+    grid = ((np.arange(G) + 0.5) / G).astype(np.float32)
+    for pe in proposals:
+        pe = pe.astype(np.float32)
+        call = _ChainCall(lp_cd, np.stack([np.zeros(V, np.float32), pe]))
+        emitted = np.zeros(V)
+        for x in range(V):
+            if pe[x] == 0:
+                continue
+            call.tok[1] = x
+            for ua in grid:
+                call.ua[1] = ua
+                for ur in grid:
+                    call.ur[0] = ur
+                    L, nxt = call()
+                    emitted[x if L == 1 else nxt] += pe[x] / (G * G)
+        np.testing.assert_allclose(emitted, target, atol=2.0 / G)
+        assert np.all(emitted[target == 0] == 0)
+
+
+def test_proposal_equal_to_target_accepts_everything():
+    rng = np.random.default_rng(15)
+    V, N = 50, 6
+    lp_cd = _tiny_target(rng, V, 0.05, 0.5, N)
+    q = np.zeros((N, V), np.float32)
+    q[1:] = np.exp(lp_cd[:-1])  # node i was drawn from its parent row's target
+    for trial in range(20):
+        tokens = [0] + [int(rng.choice(V, p=np.exp(lp_cd[i - 1]) / np.exp(lp_cd[i - 1]).sum()))
+                        for i in range(1, N)]
+        u = rng.uniform(0.0, 0.999, N).astype(np.float32)
+        o = oracle.sample_chain(tokens, lp_cd, q, u, u)
+        assert o["accept_len"] == N - 1
+        assert np.isfinite(lp_cd[N - 1, o["next_token"]])  # bonus drawn inside the mask
+
+
+def test_masked_one_hot_proposal_rejects_and_resamples_target():
+    """A proposal that is one-hot on a masked token is rejected at node 1 and the
+    residual max(0, pi_CD - pi_e) is pi_CD itself."""
+    rng = np.random.default_rng(16)
+    V, G = 40, 4000
+    lp_cd = _tiny_target(rng, V, 0.2, 0.5, 3)
+    masked = int(np.flatnonzero(np.isneginf(lp_cd[0]))[0])
+    q = np.zeros((3, V), np.float32)
+    q[1, masked] = 1.0
+    q[2] = 1.0 / V
+    counts = np.zeros(V)
+    for ur in (np.arange(G) + 0.5) / G:
+        o = oracle.sample_chain([0, masked, 0], lp_cd, q, [0.5, 1e-7, 0.5], [ur, 0.5, 0.5])
+        assert o["accept_len"] == 0 and o["ratio"][1] == 0.0
+        counts[o["next_token"]] += 1
+    np.testing.assert_allclose(counts / G, np.exp(lp_cd[0]), atol=2.0 / G)
+
+
+def test_sampled_never_accepts_or_emits_masked_tokens():
+    rng = np.random.default_rng(17)
+    V, N = 30, 5
+    for trial in range(200):
+        lp_cd = _tiny_target(rng, V, 0.3, float(rng.uniform(0, 2)), N)
+        q = np.stack([rng.dirichlet(np.ones(V) * 0.3) for _ in range(N)]).astype(np.float32)
+        tokens = [0] + [int(rng.integers(V)) for _ in range(N - 1)]
+        u = rng.uniform(1e-6, 1 - 1e-6, N).astype(np.float32)
+        o = oracle.sample_chain(tokens, lp_cd, q, u, u[::-1].copy())
+        L = o["accept_len"]
+        for i in range(1, L + 1):
+            assert np.isfinite(lp_cd[i - 1, tokens[i]])
+        assert np.isfinite(lp_cd[L, o["next_token"]])
+
+
+def test_zero_proposal_probability_accepts_in_mask():
+    rng = np.random.default_rng(18)
+    V = 20
+    lp_cd = _tiny_target(rng, V, 0.0, 0.5, 2)
+    q = np.zeros((2, V), np.float32)
+    q[1, 3] = 1.0
+    o = oracle.sample_chain([0, 5], lp_cd, q, [0.5, 0.999], [0.5, 0.5])
+    assert o["ratio"][1] == np.inf and o["accept_len"] == 1
+    # a masked token is rejected even when its proposal probability is zero
+    lp_m = _tiny_target(rng, V, 0.5, 0.5, 2)
+    masked = int(np.flatnonzero(np.isneginf(lp_m[0]))[0])
+    o = oracle.sample_chain([0, masked], lp_m, q, [0.5, 1e-7], [0.5, 0.5])
+    assert o["accept_len"] == 0 and np.isfinite(lp_m[0, o["next_token"]])
+
+
+def test_verify_sample_matches_per_row_composition():
+    case = synth.make_case("tiny_chain8", 21, mode="sample", B=3, N=6)
+    rows = oracle.eval_rows(case.hp, case.hq, case.wp, case.wq, case.bias, case.bias,
+                            theta=case.theta, s=case.s, temperature=case.T, want_logits=True,
+                            want_lpcd=True)
+    par_logits = np.zeros_like(rows["zp"])
+    par_logits[1:] = rows["zp"][:-1]
+    probs, tokens = synth.sampled_draft(case, par_logits)
+    o = oracle.verify("sample", case.B, case.N, case.hp, case.hq, case.wp, case.wq, case.bias,
+                      case.bias, case.parents, tokens, theta=case.theta, s=case.s,
+                      temperature=case.T, draft_probs=probs, u_acc=case.u_acc, u_res=case.u_res)
+    for b in range(case.B):
+        sl = slice(b * case.N, (b + 1) * case.N)
+        ref = oracle.sample_chain(tokens[b], rows["lpcd"][sl], probs[sl], case.u_acc[sl],
+                                  case.u_res[sl])
+        assert o["status"][b] == 0
+        assert o["accept_len"][b] == ref["accept_len"]
+        assert o["next_token"][b] == ref["next_token"]
+        np.testing.assert_array_equal(o["node_stats"][sl][1:, oracle.NS_RATIO], ref["ratio"][1:])

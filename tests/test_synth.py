@@ -1,0 +1,69 @@
+"""The seeded input generator: shapes, distributions and tree structure."""
+import numpy as np
+import torch
+
+from paper_2608_12913_amd import synth
+
+
+def test_bf16_rounding_matches_torch():
+    rng = np.random.default_rng(0)
+    x = np.concatenate([rng.standard_normal(100000).astype(np.float32) * 3,
+                        np.array([0.0, -0.0, 1.0, 1.00390625, 1.01171875, 65504.0, 1e-30], np.float32)])
+    ours = synth.bf16_bits(x)
+    ref = torch.from_numpy(x).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    assert np.array_equal(ours, ref)
+    back = synth.bf16_to_f32(ours)
+    assert np.array_equal(back, torch.from_numpy(x).to(torch.bfloat16).float().numpy())
+
+
+def test_uniforms_exact_and_open_interval():
+    u = synth.uniforms(np.random.default_rng(1), 200000)
+    assert u.dtype == np.float32 and u.min() > 0 and u.max() < 1
+    k = u.astype(np.float64) * 2.0 ** 23 - 0.5
+    assert np.array_equal(k, np.round(k))
+
+
+def test_tree_structure():
+    rng = np.random.default_rng(2)
+    for _ in range(50):
+        p = synth.tree_parents(rng, 64, 8, 8)
+        assert p[0] == -1 and np.all(p[1:] < np.arange(1, 64)) and np.all(p[1:] >= 0)
+        depth = np.zeros(64, int)
+        for i in range(1, 64):
+            depth[i] = depth[p[i]] + 1
+        assert depth.max() == 8
+        assert np.bincount(p[1:], minlength=64).max() <= 8
+        # breadth-first labelling: depth is non-decreasing and siblings are contiguous
+        assert np.all(np.diff(depth) >= 0)
+        assert np.all(np.diff(p[1:]) >= 0)
+
+
+def test_chain_and_case_shapes():
+    c = synth.make_case("tiny_chain8", 0)
+    assert c.hp.shape == (8, 256) and c.hq.shape == (8, 128) and c.wp.shape == (1024, 256)
+    assert c.wp.dtype == np.float32 and np.array_equal(c.parents[0], np.arange(-1, 7))
+    assert c.bias[0] == 0.0 and np.isclose(c.bias[9], -np.log(10.0))
+    std = c.wp.std() * np.sqrt(256)
+    assert 0.95 < std < 1.05 and 3.8 < c.hp.std() < 4.2
+
+
+def test_seeding_is_deterministic():
+    a = synth.make_case("tiny_chain8", 5, dtype="bf16")
+    b = synth.make_case("tiny_chain8", 5, dtype="bf16")
+    assert a.wp.dtype == np.uint16 and np.array_equal(a.wp, b.wp) and np.array_equal(a.hq, b.hq)
+    c = synth.make_case("tiny_chain8", 6, dtype="bf16")
+    assert not np.array_equal(a.wp, c.wp)
+
+
+def test_greedy_tokens_siblings_distinct_and_coins():
+    c = synth.make_case("b8_tree64", 0, V=1000, dp=16, dq=8)
+    amax = np.full(c.R, 7, np.int32)
+    tok = synth.greedy_tokens(c, amax)
+    for j in range(c.N):
+        kids = np.flatnonzero(c.parents[0] == j)
+        assert len(set(tok[0, kids])) == len(kids)
+        # at most one child copies the argmax, and it is a heads-coin child
+        for k in kids:
+            if tok[0, k] == 7 and c.coins[0, k]:
+                break
+    assert np.all((tok[0, 1:] >= 0) & (tok[0, 1:] < 1000))
