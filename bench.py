@@ -1,0 +1,177 @@
+"""Benchmark: contrastive-decoding tree verification on one MI355X.
+
+One step = one dcd_verify_greedy call (LM heads of both models, softmax
+partials and candidates, mask + cd score + argmax + log Z per row, draft-token
+statistics, tree walk) over one Llama-3-8B/1B-shaped 64-node draft tree with
+every input resident in HBM.  Prints one JSON line.
+
+  python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload b8_tree64]
+                  [--no-cpu-baseline] [--traffic-kib FETCH WRITE SCALE]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
+MFMA_BF16_PEAK_TFLOPS = 2500.0  # dense bf16 MFMA, TFLOP/s
+
+METRIC = "verified draft nodes/sec (8B/1B-shaped, 64-node tree); % of HBM peak"
+
+
+def algorithmic_bytes(case) -> int:
+    """Bytes the method must move per verification: each LM head once, the hidden
+    states, both bias vectors, the tree inputs and the outputs."""
+    esz = 2 if case.dtype == "bf16" else 4
+    R, V = case.R, case.V
+    weights = V * (case.dp + case.dq) * esz
+    hidden = R * (case.dp + case.dq) * esz
+    bias = 2 * V * 4
+    tree_io = R * 4 * 2 + R * 4 + case.B * 4 * 3   # parents, tokens, path, len/next/status
+    return weights + hidden + bias + tree_io
+
+
+def lmhead_bytes(case) -> int:
+    """Algorithmic bytes of the LM-head kernel alone: weights, hidden states, biases."""
+    esz = 2 if case.dtype == "bf16" else 4
+    return case.V * (case.dp + case.dq) * esz + case.R * (case.dp + case.dq) * esz + 2 * case.V * 4
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="b8_tree64")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--traffic-kib", type=float, nargs=3, default=None,
+                    metavar=("FETCH_KIB", "WRITE_KIB", "SCALE"),
+                    help="rocprofv3 FETCH_SIZE and WRITE_SIZE of the LM-head kernel (KiB per "
+                         "dispatch) and the copy-kernel calibration factor")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
+              "(the verification step runs on a single MI355X)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2608_12913_amd import synth
+    from paper_2608_12913_amd.runner import DeviceProblem
+
+    def log(msg):
+        print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+    case = synth.make_case(args.workload, args.seed)
+    mode = case.mode
+    if mode != "greedy":
+        raise SystemExit("bench.py times the greedy workloads")
+    log(f"{args.workload}: B={case.B} N={case.N} V={case.V} dp={case.dp} dq={case.dq}")
+
+    # draft tokens: half copy the target argmax of the parent row (taken from a first
+    # verification call on the GPU), half are uniform
+    dev = DeviceProblem.from_case(case, np.zeros((case.B, case.N), np.int32))
+    first = dev.run("greedy")
+    tokens = synth.greedy_tokens(case, first["row_argmax"])
+    dev.set_tokens(tokens)
+
+    stream = torch.cuda.current_stream()
+    for _ in range(args.warmup):
+        dev.launch(mode, stream)
+    torch.cuda.synchronize()
+
+    # timed region: K full verification steps
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        dev.launch(mode, stream)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_step = ev0.elapsed_time(ev1) / args.steps
+    out = dev.run("greedy")
+
+    # the dominant kernel alone (LM heads + partials), same stream, HIP events
+    for _ in range(5):
+        dev.launch_lmhead(mode, stream)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(args.steps):
+        dev.launch_lmhead(mode, stream)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms_lmhead = e0.elapsed_time(e1) / args.steps
+    log(f"step {ms_step * 1e3:.1f} us, lm-head kernel {ms_lmhead * 1e3:.1f} us, "
+        f"wall {wall:.3f} s, accept lengths {out['accept_len'].tolist()}")
+
+    R = case.R
+    nodes_per_s = R / (ms_step * 1e-3)
+    kbytes = lmhead_bytes(case)
+    achieved = kbytes / (ms_lmhead * 1e-3) / 1e9
+    traffic = None
+    if args.traffic_kib is not None:
+        fetch, write, scale = args.traffic_kib
+        traffic = (fetch + write) * 1024.0 * scale
+    roofline = dict(bound="hbm", achieved=round(achieved, 1), peak=HBM_PEAK_GBS, unit="GB/s",
+                    frac=round(achieved / HBM_PEAK_GBS, 4), traffic=traffic,
+                    kernel="lmhead_kernel", algorithmic_bytes=kbytes,
+                    avg_us=round(ms_lmhead * 1e3, 2))
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(case, tokens, log)
+
+    step_bytes = algorithmic_bytes(case)
+    line = {
+        "metric": METRIC,
+        "value": round(nodes_per_s, 1),
+        "unit": "nodes/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if case.dtype == "bf16" else "f32",
+        "data": "synthetic",
+        "config": {"workload": args.workload, "batch": case.B, "nodes": case.N, "vocab": case.V,
+                   "d_expert": case.dp, "d_amateur": case.dq, "plaus_thresh": case.theta,
+                   "cd_strength": case.s, "rows": R, "seed": args.seed},
+        "hbm_frac_step": round(step_bytes / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+def cpu_baseline(case, tokens, log):
+    """The oracle, untuned, on the host cores: one complete verification of the same
+    workload (every row's LM heads in fp64, mask, cd target, walk)."""
+    import oracle
+
+    threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or os.cpu_count()
+    hp, hq = oracle.as_f32(case.hp), oracle.as_f32(case.hq)
+    wp, wq = oracle.as_f32(case.wp), oracle.as_f32(case.wq)
+    log(f"cpu baseline: oracle over {case.R} rows on {threads} threads")
+    t0 = time.perf_counter()
+    oracle.verify("greedy", case.B, case.N, hp, hq, wp, wq, case.bias, case.bias, case.parents,
+                  tokens, theta=case.theta, s=case.s, nthreads=threads)
+    dt = time.perf_counter() - t0
+    log(f"cpu baseline: {dt:.2f} s")
+    return {"value": round(case.R / dt, 3), "unit": "nodes/s", "cores": threads, "kind": "oracle",
+            "sample": f"one full {case.name} verification ({case.R} rows, fp64 oracle), "
+                      f"{dt:.2f} s"}
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,198 @@
+/*
+ * dcd.h -- C ABI of libdcd: contrastive-decoding (CD) verification of a drafted
+ * token tree on one AMD Instinct MI355X (gfx950).
+ *
+ * Method: "Decoupled Contrastive Decoding via Expert-Aligned Drafting"
+ * (arXiv 2608.12913).  For every node of a draft tree the library
+ *   1. projects the expert's and the amateur's final hidden states through their
+ *      LM heads (Alg. 1, "parallel model evaluation"): z_m = H_m W_m^T + b_m;
+ *   2. forms the contrastive target of Sec. 2.1, Eq. (1),
+ *        log pi_CD(x) = (1+s) log pi_p(x) - s log pi_q(x) - log Z_CD,
+ *      restricted to the plausibility mask {x : pi_p(x) >= theta * max pi_p}
+ *      and renormalised (Sec. 2.1 and the appendix remark on
+ *      plausibility-constrained CD);
+ *   3. verifies the draft tokens against pi_CD: greedily (T = 0) by walking the
+ *      tree from the root, or by speculative rejection sampling along chains
+ *      (Alg. 1: accept test, residual resampling, bonus token).
+ *
+ * Notation: s = cd_strength (the paper's contrastive strength), theta =
+ * plaus_thresh (the paper's plausibility cutoff).  theta = 0 means no mask (the
+ * untruncated target the paper's experiments use).
+ *
+ * Conventions shared by every entry point
+ *  - Rows: a problem holds B sequences of N nodes each; row r = b*N + i is node i
+ *    of sequence b.  Node 0 is the root (the last committed token).  Row i's
+ *    hidden states produce the distribution that scores node i's CHILDREN.  A chain
+ *    of N nodes therefore verifies N-1 drafted tokens.
+ *  - Pointers named "device" are HIP device pointers (or host-coherent memory the
+ *    GPU can read); the caller owns every buffer.  Matrices are row-major and
+ *    densely packed.  The library allocates no memory and keeps no state between
+ *    calls; calls on distinct streams with distinct workspaces may run concurrently.
+ *  - Asynchrony: work is enqueued on `hip_stream` (a hipStream_t passed as void*,
+ *    NULL = the default stream); calls return without synchronising.  Outputs are
+ *    valid once the stream has reached the call.
+ *  - Errors: problems detectable on the host (NULL pointers, shapes, parameters,
+ *    alignment, workspace size) return a negative DCD_ERR_* code synchronously and
+ *    enqueue nothing.  Data-dependent problems are reported per sequence in
+ *    `status[b]` (DCD_SEQ_*); such a sequence gets accept_len 0, an accept_path of
+ *    -1s and next_token -1 (its row outputs are still written).
+ *  - Alignment: h_* and w_* must be 16-byte aligned and their hidden sizes a
+ *    multiple of 8 (bf16) or 4 (fp32) so rows can be streamed with 128-bit loads;
+ *    every other pointer must be 4-byte aligned.
+ *  - Determinism: two calls with identical inputs produce bit-identical outputs.
+ */
+#ifndef DCD_H
+#define DCD_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* return codes */
+enum {
+    DCD_OK = 0,
+    DCD_ERR_NULL = -1,        /* a required pointer is NULL */
+    DCD_ERR_SHAPE = -2,       /* a size is out of range or inconsistent */
+    DCD_ERR_PARAM = -3,       /* plaus_thresh, cd_strength, temperature or dtype invalid */
+    DCD_ERR_ALIGN = -4,       /* pointer or hidden-size alignment violated */
+    DCD_ERR_WORKSPACE = -5,   /* workspace NULL, not 256-byte aligned, or smaller than dcd_workspace_bytes() */
+    DCD_ERR_UNSUPPORTED = -6, /* valid request this build does not implement */
+    DCD_ERR_HIP = -7          /* the HIP runtime rejected a launch */
+};
+
+/* per-sequence status written to outputs.status[b] */
+enum {
+    DCD_SEQ_OK = 0,
+    DCD_SEQ_BAD_TREE = 1,   /* parents[b,0] != -1 or parents[b,i] outside [0, i) */
+    DCD_SEQ_BAD_TOKEN = 2,  /* a draft token (i >= 1) outside [0, vocab) */
+    DCD_SEQ_NONFINITE = 3,  /* a row of the sequence has a non-finite max, log-normaliser or log Z */
+    DCD_SEQ_NOT_CHAIN = 4   /* sampled verification needs parents[b,i] = i-1 */
+};
+
+/* element type of hidden states and LM-head weights (bias is always fp32) */
+enum { DCD_F32 = 0, DCD_BF16 = 1 };
+
+/* row_stats slots (8 floats per row) */
+enum {
+    DCD_ROW_MAX_P = 0,   /* max_x z_p(x)                                             */
+    DCD_ROW_LSE_P = 1,   /* log sum_x exp z_p(x): log pi_p = z_p - this               */
+    DCD_ROW_LSE_Q = 2,   /* same for the amateur                                      */
+    DCD_ROW_LOGZ = 3,    /* log sum over the mask of exp(cd(x)), cd below             */
+    DCD_ROW_TOP1 = 4,    /* cd score of the argmax                                     */
+    DCD_ROW_MARGIN = 5,  /* top-1 minus top-2 cd score over the mask (+inf: one member) */
+    DCD_ROW_COUNT = 6,   /* number of tokens in the mask                               */
+    DCD_ROW_SIGNAL = 7   /* log pi_p(x*) - log pi_q(x*) at the argmax x*               */
+};
+/* node_stats slots (6 floats per row; row 0 of every sequence is NaN) */
+enum {
+    DCD_NODE_LOGP_P = 0, /* log pi_p(tok_i) under the parent row                      */
+    DCD_NODE_LOGP_Q = 1, /* log pi_q(tok_i)                                           */
+    DCD_NODE_CD = 2,     /* cd score (1+s) log pi_p - s log pi_q                      */
+    DCD_NODE_LOGP_CD = 3,/* log pi_CD(tok_i), -inf outside the mask                    */
+    DCD_NODE_IN_MASK = 4,/* 1 if tok_i is in the parent row's mask, else 0            */
+    DCD_NODE_RATIO = 5   /* sampled: pi_CD(tok_i) / pi_e(tok_i) (+inf if pi_e = 0); greedy: NaN */
+};
+
+typedef struct {
+    int32_t batch;       /* B >= 1 sequences                                            */
+    int32_t nodes;       /* N >= 1 nodes per sequence, root included                    */
+    int32_t vocab;       /* V >= 1                                                      */
+    int32_t d_expert;    /* expert hidden size d_p                                      */
+    int32_t d_amateur;   /* amateur hidden size d_q                                     */
+    int32_t dtype;       /* DCD_BF16 or DCD_F32 for h_* and w_*                         */
+    float plaus_thresh;  /* theta in [0, 1]; 0 = untruncated target                     */
+    float cd_strength;   /* s >= 0 (finite)                                             */
+    float temperature;   /* sampled mode: T > 0 divides both models' logits before
+                            anything else, mask included; ignored by greedy mode         */
+} dcd_problem;
+
+typedef struct {                 /* device pointers, read only                          */
+    const void *h_expert;        /* [B*N, d_p] final expert hidden state of every node   */
+    const void *h_amateur;       /* [B*N, d_q]                                           */
+    const void *w_expert;        /* [V, d_p]  expert LM head (nn.Linear [out, in] layout) */
+    const void *w_amateur;       /* [V, d_q]                                             */
+    const float *bias_expert;    /* [V] fp32 logit bias, or NULL for none                */
+    const float *bias_amateur;   /* [V] fp32, or NULL; may alias bias_expert             */
+    const int32_t *parents;      /* [B, N] parent node of each node; parents[b,0] = -1   */
+    const int32_t *tokens;       /* [B, N] draft token of each node (entry 0 ignored)    */
+} dcd_inputs;
+
+typedef struct {                 /* device pointers, written by the call                 */
+    int32_t *accept_len;         /* [B] number of accepted draft nodes                    */
+    int32_t *accept_path;        /* [B, N] node ids: 0, then accepted nodes, then -1      */
+    int32_t *next_token;         /* [B] greedy: argmax of pi_CD at the last accepted node;
+                                    sampled: the residual or bonus token                  */
+    int32_t *status;             /* [B] DCD_SEQ_*                                         */
+    int32_t *row_argmax;         /* [B*N] optional (NULL skips): argmax of pi_CD per row;
+                                    ties go to the lowest token id                        */
+    float *row_stats;            /* [B*N, 8] optional: DCD_ROW_* slots                    */
+    float *node_stats;           /* [B*N, 6] optional: DCD_NODE_* slots                   */
+} dcd_outputs;
+
+/*
+ * Bytes of device workspace a call with problem `p` needs (0 if `p` is invalid).
+ * The workspace holds per-tile softmax partials, the candidate logits that may
+ * fall inside the plausibility mask, and per-row results; it is
+ * O(B*N*V) bytes (8.1 bytes per row and vocabulary entry).
+ */
+size_t dcd_workspace_bytes(const dcd_problem *p);
+
+/*
+ * Greedy (T = 0) verification of B draft trees.
+ * For every row: logits of both LM heads, max and log-normaliser of each, the
+ * plausibility mask, the cd score, its log normaliser over the mask and its
+ * argmax.  Then, per sequence, starting at the root: accept the lowest-index
+ * child whose draft token equals the current row's argmax, repeat from it, stop
+ * when no child matches; next_token is the argmax of the last accepted node.
+ * A draft token outside the mask is never accepted.
+ * Workspace: device memory of at least dcd_workspace_bytes(p) bytes, 256-byte
+ * aligned, not used by any concurrently running call.
+ */
+int dcd_verify_greedy(const dcd_problem *p, const dcd_inputs *in, const dcd_outputs *out,
+                      void *workspace, size_t workspace_bytes, void *hip_stream);
+
+/*
+ * Sampled verification (Alg. 1) of B chains (parents[b,i] must be i-1, else the
+ * sequence gets DCD_SEQ_NOT_CHAIN).
+ *   draft_probs [B*N, V] fp32 device: row b*N+i is pi_e^(i), the proposal draft
+ *               token i was drawn from (row b*N+0 unused)
+ *   u_accept    [B*N] fp32 device, in (0,1): u_accept[b*N+i] decides node i
+ *   u_resample  [B*N] fp32 device, in (0,1): u_resample[b*N+j] draws the token
+ *               emitted after row j
+ * Node i is accepted iff pi_CD^(i-1)(tok_i) > 0 and
+ * u_accept <= pi_CD^(i-1)(tok_i) / pi_e^(i)(tok_i); verification stops at the first
+ * rejected node k, whose replacement is drawn from the residual
+ * Normalize(max(0, pi_CD^(k-1) - pi_e^(k))) (from pi_CD^(k-1) if that is zero);
+ * if every node is accepted the bonus token is drawn from pi_CD^(N-1).  A draw
+ * is the inverse CDF in token-id order: the smallest token whose cumulative
+ * weight exceeds u_resample times the total.
+ */
+int dcd_verify_sample(const dcd_problem *p, const dcd_inputs *in, const float *draft_probs,
+                      const float *u_accept, const float *u_resample, const dcd_outputs *out,
+                      void *workspace, size_t workspace_bytes, void *hip_stream);
+
+/*
+ * First stage of dcd_verify_greedy / dcd_verify_sample on its own: both LM-head
+ * projections of every row with their per-tile softmax partials and plausibility
+ * candidates, written to `workspace` (one kernel launch, everything else of the
+ * verification left undone).  `sampled` != 0 applies the problem's temperature as
+ * dcd_verify_sample does.  Only h_*, w_* and bias_* of `in` are read.  For callers
+ * that time or schedule the projection separately; the workspace contents are
+ * internal.  Errors as for the verify calls.
+ */
+int dcd_lmhead_partials(const dcd_problem *p, const dcd_inputs *in, int sampled, void *workspace,
+                        size_t workspace_bytes, void *hip_stream);
+
+/* static description of a return code (never NULL) */
+const char *dcd_error_string(int code);
+
+/* ABI version of this header: 1 */
+int dcd_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* DCD_H */

@@ -1,0 +1,177 @@
+// C ABI of libdcd: argument validation, workspace planning and the launch
+// sequence (LM heads + partials -> per-row combine -> per-sequence verification).
+#include <math.h>
+
+#include "../../include/dcd.h"
+#include "dcd_internal.h"
+
+namespace dcd {
+namespace {
+
+constexpr size_t kAlign = 256;
+constexpr long long kMaxRows = 1 << 24;
+constexpr long long kMaxVocab = 1 << 30;
+constexpr int kMaxHidden = 1 << 20;
+
+size_t round_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+bool aligned(const void *p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+int make_plan(const dcd_problem *p, bool sample, Plan &P) {
+    if (!p) return DCD_ERR_NULL;
+    if (p->batch < 1 || p->nodes < 1 || p->vocab < 1 || p->d_expert < 1 || p->d_amateur < 1)
+        return DCD_ERR_SHAPE;
+    const long long R = (long long)p->batch * p->nodes;
+    if (R > kMaxRows || p->vocab > kMaxVocab || p->d_expert > kMaxHidden ||
+        p->d_amateur > kMaxHidden)
+        return DCD_ERR_SHAPE;
+    if (p->dtype != DCD_BF16 && p->dtype != DCD_F32) return DCD_ERR_PARAM;
+    const int mult = p->dtype == DCD_BF16 ? 8 : 4;  // 16-byte rows
+    if (p->d_expert % mult || p->d_amateur % mult) return DCD_ERR_ALIGN;
+    if (!(p->plaus_thresh >= 0.f && p->plaus_thresh <= 1.f)) return DCD_ERR_PARAM;
+    if (!(p->cd_strength >= 0.f) || !isfinite(p->cd_strength)) return DCD_ERR_PARAM;
+    if (sample && (!(p->temperature > 0.f) || !isfinite(p->temperature))) return DCD_ERR_PARAM;
+    P = Plan{};
+    P.B = p->batch;
+    P.N = p->nodes;
+    P.R = (int)R;
+    P.V = p->vocab;
+    P.dp = p->d_expert;
+    P.dq = p->d_amateur;
+    P.dtype = p->dtype == DCD_BF16 ? kBF16 : kF32;
+    P.ntiles = (P.V + kTileTokens - 1) / kTileTokens;
+    P.nrb = (P.R + kTileRows - 1) / kTileRows;
+    P.wstride = P.ntiles * kWordsPerTile;
+    // ln(theta) in double, rounded once; theta = 0 switches the mask off
+    P.log_theta = p->plaus_thresh > 0.f ? (float)log((double)p->plaus_thresh) : -INFINITY;
+    P.s = p->cd_strength;
+    P.inv_T = sample ? (float)(1.0 / (double)p->temperature) : 1.f;
+    const long long groups = (long long)((P.ntiles + 7) / 8) * 8 * P.nrb;
+    if (groups > 0x7fffffffLL) return DCD_ERR_SHAPE;
+    return DCD_OK;
+}
+
+int check_io(const dcd_inputs *in, const dcd_outputs *out) {
+    if (!in || !out) return DCD_ERR_NULL;
+    if (!in->h_expert || !in->h_amateur || !in->w_expert || !in->w_amateur || !in->parents ||
+        !in->tokens)
+        return DCD_ERR_NULL;
+    if (!out->accept_len || !out->accept_path || !out->next_token || !out->status)
+        return DCD_ERR_NULL;
+    if (!aligned(in->h_expert, 16) || !aligned(in->h_amateur, 16) || !aligned(in->w_expert, 16) ||
+        !aligned(in->w_amateur, 16))
+        return DCD_ERR_ALIGN;
+    const void *four[] = {in->bias_expert, in->bias_amateur, in->parents, in->tokens,
+                          out->accept_len, out->accept_path, out->next_token, out->status,
+                          out->row_argmax, out->row_stats, out->node_stats};
+    for (const void *q : four)
+        if (q && !aligned(q, 4)) return DCD_ERR_ALIGN;
+    return DCD_OK;
+}
+
+int run(const dcd_problem *p, const dcd_inputs *in, const SampleInputs *smp,
+        const dcd_outputs *out, void *ws, size_t ws_bytes, void *stream) {
+    Plan P;
+    int rc = make_plan(p, smp != nullptr, P);
+    if (rc) return rc;
+    if ((rc = check_io(in, out))) return rc;
+    if (smp) {
+        if (!smp->draft_probs || !smp->u_acc || !smp->u_res) return DCD_ERR_NULL;
+        if (!aligned(smp->draft_probs, 4) || !aligned(smp->u_acc, 4) || !aligned(smp->u_res, 4))
+            return DCD_ERR_ALIGN;
+    }
+    const size_t need = workspace_layout(P, nullptr);
+    if (!ws || ws_bytes < need) return DCD_ERR_WORKSPACE;
+    if (!aligned(ws, kAlign)) return DCD_ERR_WORKSPACE;
+    workspace_layout(P, (char *)ws);
+
+    const Inputs I{in->h_expert, in->h_amateur, in->w_expert, in->w_amateur,
+                   in->bias_expert, in->bias_amateur, in->parents, in->tokens};
+    const Outputs O{out->accept_len, out->accept_path, out->next_token, out->status,
+                    out->row_argmax, out->row_stats, out->node_stats};
+    hipStream_t st = (hipStream_t)stream;
+    if (launch_lmhead(P, I, st) != hipSuccess) return DCD_ERR_HIP;
+    if (launch_combine(P, O, st) != hipSuccess) return DCD_ERR_HIP;
+    if (launch_sequences(P, I, O, smp, st) != hipSuccess) return DCD_ERR_HIP;
+    return DCD_OK;
+}
+
+int run_lmhead(const dcd_problem *p, const dcd_inputs *in, int sampled, void *ws, size_t ws_bytes,
+               void *stream) {
+    Plan P;
+    int rc = make_plan(p, sampled != 0, P);
+    if (rc) return rc;
+    if (!in) return DCD_ERR_NULL;
+    if (!in->h_expert || !in->h_amateur || !in->w_expert || !in->w_amateur) return DCD_ERR_NULL;
+    if (!aligned(in->h_expert, 16) || !aligned(in->h_amateur, 16) || !aligned(in->w_expert, 16) ||
+        !aligned(in->w_amateur, 16) || !aligned(in->bias_expert, 4) || !aligned(in->bias_amateur, 4))
+        return DCD_ERR_ALIGN;
+    const size_t need = workspace_layout(P, nullptr);
+    if (!ws || ws_bytes < need || !aligned(ws, kAlign)) return DCD_ERR_WORKSPACE;
+    workspace_layout(P, (char *)ws);
+    const Inputs I{in->h_expert, in->h_amateur, in->w_expert, in->w_amateur,
+                   in->bias_expert, in->bias_amateur, in->parents, in->tokens};
+    return launch_lmhead(P, I, (hipStream_t)stream) == hipSuccess ? DCD_OK : DCD_ERR_HIP;
+}
+
+}  // namespace
+
+size_t workspace_layout(Plan &p, char *base) {
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+        char *ptr = base ? base + off : nullptr;
+        off += round_up(bytes);
+        return ptr;
+    };
+    const size_t R = (size_t)p.R;
+    p.partials = (float4 *)take(R * p.ntiles * sizeof(float4));
+    p.cand = (float2 *)take(R * (size_t)p.V * sizeof(float2));
+    p.bits = (uint32_t *)take(R * (size_t)p.wstride * sizeof(uint32_t));
+    p.rowinfo = (float *)take(R * kRowInfo * sizeof(float));
+    return off;
+}
+
+}  // namespace dcd
+
+extern "C" {
+
+size_t dcd_workspace_bytes(const dcd_problem *p) {
+    dcd::Plan P;
+    if (dcd::make_plan(p, false, P) != DCD_OK) return 0;
+    return dcd::workspace_layout(P, nullptr);
+}
+
+int dcd_verify_greedy(const dcd_problem *p, const dcd_inputs *in, const dcd_outputs *out,
+                      void *workspace, size_t workspace_bytes, void *hip_stream) {
+    return dcd::run(p, in, nullptr, out, workspace, workspace_bytes, hip_stream);
+}
+
+int dcd_verify_sample(const dcd_problem *p, const dcd_inputs *in, const float *draft_probs,
+                      const float *u_accept, const float *u_resample, const dcd_outputs *out,
+                      void *workspace, size_t workspace_bytes, void *hip_stream) {
+    const dcd::SampleInputs s{draft_probs, u_accept, u_resample};
+    return dcd::run(p, in, &s, out, workspace, workspace_bytes, hip_stream);
+}
+
+int dcd_lmhead_partials(const dcd_problem *p, const dcd_inputs *in, int sampled, void *workspace,
+                        size_t workspace_bytes, void *hip_stream) {
+    return dcd::run_lmhead(p, in, sampled, workspace, workspace_bytes, hip_stream);
+}
+
+const char *dcd_error_string(int code) {
+    switch (code) {
+        case DCD_OK: return "success";
+        case DCD_ERR_NULL: return "a required pointer is NULL";
+        case DCD_ERR_SHAPE: return "a size is out of range or inconsistent";
+        case DCD_ERR_PARAM: return "invalid plaus_thresh, cd_strength, temperature or dtype";
+        case DCD_ERR_ALIGN: return "pointer or hidden-size alignment violated";
+        case DCD_ERR_WORKSPACE: return "workspace missing, misaligned or too small";
+        case DCD_ERR_UNSUPPORTED: return "request not supported by this build";
+        case DCD_ERR_HIP: return "the HIP runtime rejected a launch";
+        default: return "unknown error code";
+    }
+}
+
+int dcd_abi_version(void) { return 1; }
+
+}  // extern "C"

@@ -1,0 +1,147 @@
+"""ctypes binding of libdcd (include/dcd.h): argument marshalling only.
+
+Every step of the verification runs in the library's HIP kernels.  Buffers are
+passed as device pointers: anything with ``data_ptr()`` (a torch tensor on the
+GPU) or a plain integer address.  A missing or unloadable library raises; there
+is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libdcd.so")
+
+DCD_OK, DCD_ERR_NULL, DCD_ERR_SHAPE, DCD_ERR_PARAM = 0, -1, -2, -3
+DCD_ERR_ALIGN, DCD_ERR_WORKSPACE, DCD_ERR_UNSUPPORTED, DCD_ERR_HIP = -4, -5, -6, -7
+SEQ_OK, SEQ_BAD_TREE, SEQ_BAD_TOKEN, SEQ_NONFINITE, SEQ_NOT_CHAIN = range(5)
+DCD_F32, DCD_BF16 = 0, 1
+ROW_MAX_P, ROW_LSE_P, ROW_LSE_Q, ROW_LOGZ, ROW_TOP1, ROW_MARGIN, ROW_COUNT, ROW_SIGNAL = range(8)
+NODE_LOGP_P, NODE_LOGP_Q, NODE_CD, NODE_LOGP_CD, NODE_IN_MASK, NODE_RATIO = range(6)
+
+EXPORTS = ("dcd_workspace_bytes", "dcd_verify_greedy", "dcd_verify_sample",
+           "dcd_lmhead_partials", "dcd_error_string", "dcd_abi_version")
+
+
+class DcdError(RuntimeError):
+    def __init__(self, code: int):
+        self.code = code
+        super().__init__(f"libdcd error {code}: {error_string(code)}")
+
+
+class Problem(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("nodes", ctypes.c_int32), ("vocab", ctypes.c_int32),
+                ("d_expert", ctypes.c_int32), ("d_amateur", ctypes.c_int32),
+                ("dtype", ctypes.c_int32), ("plaus_thresh", ctypes.c_float),
+                ("cd_strength", ctypes.c_float), ("temperature", ctypes.c_float)]
+
+
+class Inputs(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in ("h_expert", "h_amateur", "w_expert", "w_amateur",
+                                                "bias_expert", "bias_amateur", "parents", "tokens")]
+
+
+class Outputs(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in ("accept_len", "accept_path", "next_token", "status",
+                                                "row_argmax", "row_stats", "node_stats")]
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is not built: run __graft_entry__.build() "
+                               "(or python -m paper_2608_12913_amd.build)")
+        L = ctypes.CDLL(LIB_PATH)
+        P = ctypes.c_void_p
+        L.dcd_workspace_bytes.argtypes = [ctypes.POINTER(Problem)]
+        L.dcd_workspace_bytes.restype = ctypes.c_size_t
+        L.dcd_verify_greedy.argtypes = [ctypes.POINTER(Problem), ctypes.POINTER(Inputs),
+                                        ctypes.POINTER(Outputs), P, ctypes.c_size_t, P]
+        L.dcd_verify_greedy.restype = ctypes.c_int
+        L.dcd_verify_sample.argtypes = [ctypes.POINTER(Problem), ctypes.POINTER(Inputs), P, P, P,
+                                        ctypes.POINTER(Outputs), P, ctypes.c_size_t, P]
+        L.dcd_verify_sample.restype = ctypes.c_int
+        L.dcd_lmhead_partials.argtypes = [ctypes.POINTER(Problem), ctypes.POINTER(Inputs),
+                                          ctypes.c_int, P, ctypes.c_size_t, P]
+        L.dcd_lmhead_partials.restype = ctypes.c_int
+        L.dcd_error_string.argtypes = [ctypes.c_int]
+        L.dcd_error_string.restype = ctypes.c_char_p
+        L.dcd_abi_version.argtypes = []
+        L.dcd_abi_version.restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def error_string(code: int) -> str:
+    return lib().dcd_error_string(int(code)).decode()
+
+
+def ptr(x) -> int | None:
+    """Device address of a buffer (None stays NULL)."""
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    return int(x.data_ptr())
+
+
+def _stream(stream) -> int | None:
+    if stream is None:
+        return None
+    if isinstance(stream, int):
+        return stream
+    return int(stream.cuda_stream)
+
+
+def make_problem(batch, nodes, vocab, d_expert, d_amateur, dtype="bf16", plaus_thresh=0.1,
+                 cd_strength=0.5, temperature=1.0) -> Problem:
+    dt = {"bf16": DCD_BF16, "f32": DCD_F32}.get(dtype, dtype)
+    return Problem(batch, nodes, vocab, d_expert, d_amateur, dt, plaus_thresh, cd_strength,
+                   temperature)
+
+
+def make_inputs(h_expert, h_amateur, w_expert, w_amateur, bias_expert, bias_amateur, parents,
+                tokens) -> Inputs:
+    return Inputs(*(ptr(a) for a in (h_expert, h_amateur, w_expert, w_amateur, bias_expert,
+                                     bias_amateur, parents, tokens)))
+
+
+def make_outputs(accept_len, accept_path, next_token, status, row_argmax=None, row_stats=None,
+                 node_stats=None) -> Outputs:
+    return Outputs(*(ptr(a) for a in (accept_len, accept_path, next_token, status, row_argmax,
+                                      row_stats, node_stats)))
+
+
+def workspace_bytes(problem: Problem) -> int:
+    return int(lib().dcd_workspace_bytes(ctypes.byref(problem)))
+
+
+def verify_greedy(problem: Problem, inputs: Inputs, outputs: Outputs, workspace,
+                  workspace_bytes: int, stream=None) -> None:
+    rc = lib().dcd_verify_greedy(ctypes.byref(problem), ctypes.byref(inputs),
+                                 ctypes.byref(outputs), ptr(workspace), int(workspace_bytes),
+                                 _stream(stream))
+    if rc != DCD_OK:
+        raise DcdError(rc)
+
+
+def verify_sample(problem: Problem, inputs: Inputs, draft_probs, u_accept, u_resample,
+                  outputs: Outputs, workspace, workspace_bytes: int, stream=None) -> None:
+    rc = lib().dcd_verify_sample(ctypes.byref(problem), ctypes.byref(inputs), ptr(draft_probs),
+                                 ptr(u_accept), ptr(u_resample), ctypes.byref(outputs),
+                                 ptr(workspace), int(workspace_bytes), _stream(stream))
+    if rc != DCD_OK:
+        raise DcdError(rc)
+
+
+def lmhead_partials(problem: Problem, inputs: Inputs, sampled: bool, workspace,
+                    workspace_bytes: int, stream=None) -> None:
+    rc = lib().dcd_lmhead_partials(ctypes.byref(problem), ctypes.byref(inputs), int(sampled),
+                                   ptr(workspace), int(workspace_bytes), _stream(stream))
+    if rc != DCD_OK:
+        raise DcdError(rc)

@@ -1,0 +1,115 @@
+"""C-ABI checks that need no GPU: the library loads, exports every function the
+header declares, and rejects invalid requests on the host before any launch."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2608_12913_amd import dcd
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "dcd.h")
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(dcd_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_function():
+    names = _declared_functions()
+    assert set(names) == set(dcd.EXPORTS)
+    L = dcd.lib()
+    for n in names:
+        assert hasattr(L, n), n
+    assert L.dcd_abi_version() == 1
+
+
+def test_error_strings():
+    for code in range(0, -8, -1):
+        assert dcd.error_string(code) and dcd.error_string(code) != "unknown error code"
+    assert dcd.error_string(-99) == "unknown error code"
+
+
+def _problem(**kw):
+    base = dict(batch=1, nodes=64, vocab=128256, d_expert=4096, d_amateur=2048, dtype="bf16",
+                plaus_thresh=0.1, cd_strength=0.5, temperature=1.0)
+    base.update(kw)
+    return dcd.make_problem(**base)
+
+
+def test_workspace_bytes():
+    ws = dcd.workspace_bytes(_problem())
+    R, V = 64, 128256
+    # candidate logits (8 B per row and token) dominate; partials, bitmap, row results on top
+    assert R * V * 8 < ws < R * V * 8 * 1.1
+    assert dcd.workspace_bytes(_problem(batch=32)) > 31 * ws
+    for bad in (dict(batch=0), dict(vocab=0), dict(d_expert=4100), dict(dtype=7),
+                dict(plaus_thresh=1.5), dict(plaus_thresh=-0.1), dict(cd_strength=-1.0),
+                dict(plaus_thresh=float("nan")), dict(cd_strength=float("inf"))):
+        assert dcd.workspace_bytes(_problem(**bad)) == 0, bad
+    # fp32 rows need a multiple of 4 elements, bf16 a multiple of 8
+    assert dcd.workspace_bytes(_problem(dtype="f32", d_expert=4100)) > 0
+
+
+def _fake_ptrs():
+    # host addresses suitably aligned; never dereferenced because validation fails first
+    buf = (ctypes.c_char * 4096)()
+    a = (ctypes.addressof(buf) + 255) // 256 * 256
+    return buf, a
+
+
+def _call_greedy(problem, inputs, outputs, ws, ws_bytes):
+    return dcd.lib().dcd_verify_greedy(ctypes.byref(problem), ctypes.byref(inputs),
+                                       ctypes.byref(outputs), ws, ws_bytes, None)
+
+
+def test_host_validation_errors():
+    buf, a = _fake_ptrs()
+    p = _problem(nodes=8, vocab=1024, d_expert=256, d_amateur=128)
+    good_in = dcd.Inputs(a, a, a, a, a, a, a, a)
+    good_out = dcd.Outputs(a, a, a, a, None, None, None)
+    need = dcd.workspace_bytes(p)
+    # missing required pointers
+    for i in range(8):
+        if i in (4, 5):  # biases are optional
+            continue
+        vals = [a] * 8
+        vals[i] = None
+        assert _call_greedy(p, dcd.Inputs(*vals), good_out, a, need) == dcd.DCD_ERR_NULL
+    for i in range(4):
+        vals = [a] * 4 + [None] * 3
+        vals[i] = None
+        assert _call_greedy(p, good_in, dcd.Outputs(*vals), a, need) == dcd.DCD_ERR_NULL
+    # misaligned matrices (16 bytes) and small buffers (4 bytes)
+    assert _call_greedy(p, dcd.Inputs(a + 8, a, a, a, a, a, a, a), good_out, a, need) == dcd.DCD_ERR_ALIGN
+    assert _call_greedy(p, dcd.Inputs(a, a, a, a, a + 2, a, a, a), good_out, a, need) == dcd.DCD_ERR_ALIGN
+    # workspace too small / missing / misaligned
+    assert _call_greedy(p, good_in, good_out, a, need - 1) == dcd.DCD_ERR_WORKSPACE
+    assert _call_greedy(p, good_in, good_out, None, need) == dcd.DCD_ERR_WORKSPACE
+    assert _call_greedy(p, good_in, good_out, a + 16, need) == dcd.DCD_ERR_WORKSPACE
+    # parameters and shapes
+    assert _call_greedy(_problem(nodes=8, vocab=1024, d_expert=256, d_amateur=128, plaus_thresh=2.0),
+                        good_in, good_out, a, need) == dcd.DCD_ERR_PARAM
+    assert _call_greedy(_problem(nodes=0), good_in, good_out, a, need) == dcd.DCD_ERR_SHAPE
+    assert _call_greedy(_problem(d_amateur=2044), good_in, good_out, a, need) == dcd.DCD_ERR_ALIGN
+    # sampled mode validates temperature and its extra inputs
+    L = dcd.lib()
+    ps = _problem(nodes=8, vocab=1024, d_expert=256, d_amateur=128, temperature=0.0)
+    rc = L.dcd_verify_sample(ctypes.byref(ps), ctypes.byref(good_in), a, a, a,
+                             ctypes.byref(good_out), a, need, None)
+    assert rc == dcd.DCD_ERR_PARAM
+    ps = _problem(nodes=8, vocab=1024, d_expert=256, d_amateur=128)
+    rc = L.dcd_verify_sample(ctypes.byref(ps), ctypes.byref(good_in), None, a, a,
+                             ctypes.byref(good_out), a, need, None)
+    assert rc == dcd.DCD_ERR_NULL
+    del buf
+
+
+def test_binding_raises():
+    p = _problem(batch=0)
+    with pytest.raises(dcd.DcdError) as e:
+        dcd.verify_greedy(p, dcd.Inputs(), dcd.Outputs(), None, 0)
+    assert e.value.code == dcd.DCD_ERR_SHAPE

@@ -1,0 +1,307 @@
+"""GPU parity: libdcd (through the C ABI) against the CPU oracle on seeded inputs."""
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2608_12913_amd import synth
+from tests import parity
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+
+def _say(msg):
+    print(f"[gpu-parity] {msg}", flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2608_12913_amd import dcd
+    dcd.lib()  # loud failure if the library is missing
+
+
+def _runner():
+    from paper_2608_12913_amd.runner import DeviceProblem
+    return DeviceProblem
+
+
+def _oracle_greedy(case, tokens, **kw):
+    args = dict(theta=case.theta, s=case.s)
+    args.update(kw)
+    return oracle.verify("greedy", case.B, case.N, case.hp, case.hq, case.wp, case.wq, case.bias,
+                         case.bias, case.parents, tokens, **args)
+
+
+def _greedy_tokens(case, **kw):
+    rows = oracle.eval_rows(case.hp, case.hq, case.wp, case.wq, case.bias, case.bias,
+                            theta=kw.get("theta", case.theta), s=kw.get("s", case.s))
+    return synth.greedy_tokens(case, rows["argmax"])
+
+
+def _check_greedy(case, tokens, label, **kw):
+    _say(f"{label}: B={case.B} N={case.N} V={case.V} dp={case.dp} dq={case.dq} {case.dtype} {kw}")
+    o = _oracle_greedy(case, tokens, **kw)
+    dp = _runner().from_case(case, tokens, **kw)
+    g = dp.run("greedy")
+    report = {}
+    amb = parity.compare_rows(g, o, np.arange(case.R), report)
+    parity.compare_nodes(g, o, case.parents, amb, report)
+    parity.compare_greedy(g, o, case.parents, amb, report)
+    parity.check_walk_consistent(g, case.parents, tokens)
+    _say(f"{label}: ok {report}")
+    return g, o, dp
+
+
+# ------------------------------------------------------------------ small cases
+@pytest.mark.parametrize("seed", range(5))
+def test_tiny_chain8_fp32(seed):
+    case = synth.make_case("tiny_chain8", seed)
+    _check_greedy(case, _greedy_tokens(case), f"tiny_chain8 seed {seed}")
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_small_tree_bf16_ragged_vocab(seed):
+    # 4099 = 16 full 256-token tiles + 3; 128 rows = 2 row blocks
+    case = synth.make_case("b8_tree64", seed, B=2, V=4099, dp=512, dq=256)
+    _check_greedy(case, _greedy_tokens(case), f"small tree seed {seed}")
+
+
+def test_ragged_hidden_and_rows():
+    # K tails (520 and 136 are not multiples of 64 elements) and 70 rows (64 + 6)
+    case = synth.make_case("b8_tree64", 7, N=70, V=1000, dp=520, dq=136)
+    _check_greedy(case, _greedy_tokens(case), "ragged K and rows")
+
+
+def test_ragged_fp32():
+    case = synth.make_case("tiny_chain8", 8, N=19, V=777, dp=100, dq=36)
+    _check_greedy(case, _greedy_tokens(case), "ragged fp32")
+
+
+@pytest.mark.parametrize("theta,s", [(0.0, 0.5), (1.0, 0.5), (0.1, 0.0), (0.1, 2.0), (0.001, 1.0)])
+def test_mask_and_strength_settings(theta, s):
+    case = synth.make_case("b8_tree64", 11, N=24, depth=5, max_children=4, V=2000, dp=256, dq=128)
+    tokens = _greedy_tokens(case, theta=theta, s=s)
+    _check_greedy(case, tokens, f"theta={theta} s={s}", theta=theta, s=s)
+
+
+def test_flat_logits_every_token_in_mask():
+    case = synth.make_case("tiny_chain8", 12, N=8, V=1500, dp=64, dq=32)
+    case.wp[:] = 0
+    case.wq[:] = 0
+    case.bias[:] = 0
+    tokens = _greedy_tokens(case)
+    g, o, _ = _check_greedy(case, tokens, "flat logits")
+    assert np.all(g["row_argmax"] == 0)
+    assert np.all(g["row_stats"][:, oracle.RS_COUNT] == 1500)
+    np.testing.assert_allclose(g["row_stats"][:, oracle.RS_LOGZ], o["row_stats"][:, oracle.RS_LOGZ],
+                               atol=1e-4)
+
+
+def test_exact_integer_logits_theta_one():
+    """Small-integer bf16 weights and states make every fp32 partial sum exact, so the
+    set of tokens tied at the expert max (the theta = 1 mask) must match exactly."""
+    rng = np.random.default_rng(13)
+    case = synth.make_case("b8_tree64", 13, N=16, depth=4, max_children=4, V=3000, dp=128, dq=64)
+    for name, d in (("hp", 128), ("hq", 64)):
+        setattr(case, name, synth.bf16_bits(rng.integers(-2, 3, (case.R, d)).astype(np.float32)))
+    case.wp = synth.bf16_bits(rng.integers(-1, 2, (3000, 128)).astype(np.float32))
+    case.wq = synth.bf16_bits(rng.integers(-1, 2, (3000, 64)).astype(np.float32))
+    case.bias[:] = 0
+    tokens = _greedy_tokens(case, theta=1.0)
+    _say("exact integer logits")
+    o = _oracle_greedy(case, tokens, theta=1.0)
+    g = _runner().from_case(case, tokens, theta=1.0).run("greedy")
+    assert np.array_equal(g["row_argmax"], o["row_argmax"])
+    assert np.array_equal(g["row_stats"][:, oracle.RS_COUNT], o["row_stats"][:, oracle.RS_COUNT])
+    assert np.array_equal(g["accept_len"], o["accept_len"])
+    assert np.array_equal(g["accept_path"], o["accept_path"])
+    np.testing.assert_allclose(g["row_stats"][:, oracle.RS_MAXP], o["row_stats"][:, oracle.RS_MAXP],
+                               rtol=0, atol=0)
+
+
+def test_duplicate_sibling_tokens():
+    case = synth.make_case("b8_tree64", 14, N=32, depth=4, max_children=6, V=1024, dp=128, dq=64)
+    rows = oracle.eval_rows(case.hp, case.hq, case.wp, case.wq, case.bias, case.bias,
+                            theta=case.theta, s=case.s)
+    tokens = np.zeros((1, case.N), np.int32)
+    for i in range(1, case.N):  # every child carries its parent's argmax
+        tokens[0, i] = rows["argmax"][case.parents[0, i]]
+    _check_greedy(case, tokens, "duplicate siblings")
+
+
+def test_sequence_status_codes():
+    case = synth.make_case("tiny_chain8", 15, B=4, N=8, V=512, dp=64, dq=32)
+    tokens = _greedy_tokens(case)
+    case.parents[1, 3] = 6  # parent after child
+    tokens[2, 4] = 512  # out of the vocabulary
+    case.hp[3 * 8 + 2, 5] = np.inf  # non-finite logits in sequence 3
+    _check_greedy(case, tokens, "status codes")
+
+
+def test_repeated_calls_are_bit_identical():
+    case = synth.make_case("b8_tree64", 16, N=40, V=3001, dp=256, dq=128)
+    tokens = _greedy_tokens(case)
+    dp = _runner().from_case(case, tokens)
+    a = dp.run("greedy")
+    b = dp.run("greedy")
+    for k in a:
+        assert np.array_equal(a[k].view(np.uint8), b[k].view(np.uint8)), k
+
+
+# ------------------------------------------------------------------ sampled
+def _sampled_setup(case):
+    rows = oracle.eval_rows(case.hp, case.hq, case.wp, case.wq, case.bias, case.bias,
+                            theta=case.theta, s=case.s, temperature=case.T, want_logits=True)
+    parent_logits = np.zeros_like(rows["zp"])
+    parent_logits[1:] = rows["zp"][:-1]
+    return synth.sampled_draft(case, parent_logits)
+
+
+def _check_sample(case, probs, tokens, label, seqs=None):
+    _say(f"{label}: B={case.B} N={case.N} V={case.V} {case.dtype} theta={case.theta} s={case.s}")
+    o = oracle.verify("sample", case.B, case.N, case.hp, case.hq, case.wp, case.wq, case.bias,
+                      case.bias, case.parents, tokens, theta=case.theta, s=case.s,
+                      temperature=case.T, draft_probs=probs, u_acc=case.u_acc, u_res=case.u_res)
+    g = _runner().from_case(case, tokens, draft_probs=probs).run("sample")
+    report = {}
+    amb = parity.compare_rows(g, o, np.arange(case.R), report)
+    parity.compare_nodes(g, o, case.parents, amb, report)
+    boundary = o["row_gap"] <= parity.BOUNDARY_GATE
+    parity.compare_sample(g, o, case, tokens, probs, boundary, report, seqs)
+    gr = g["node_stats"][:, oracle.NS_RATIO]
+    orat = o["node_stats"][:, oracle.NS_RATIO]
+    fin = np.isfinite(orat) & (orat > 1e-30)
+    assert np.all(np.abs(gr[fin] / orat[fin] - 1) < 1e-3)
+    _say(f"{label}: ok {report}")
+    return g, o
+
+
+@pytest.mark.parametrize("seed,theta,s", [(0, 0.1, 0.5), (1, 0.0, 0.5), (2, 0.3, 1.0), (3, 0.1, 0.0)])
+def test_sampled_chains_small(seed, theta, s):
+    case = synth.make_case("s8_chain16x8", seed, V=3000, dp=256, dq=128, theta=theta, s=s)
+    probs, tokens = _sampled_setup(case)
+    _check_sample(case, probs, tokens, f"sampled small seed {seed}")
+
+
+def test_sampled_always_accept_and_reject():
+    case = synth.make_case("s8_chain16x8", 5, B=4, N=6, V=700, dp=128, dq=64)
+    rows = oracle.eval_rows(case.hp, case.hq, case.wp, case.wq, case.bias, case.bias,
+                            theta=case.theta, s=case.s, want_lpcd=True)
+    probs = np.zeros((case.R, case.V), np.float32)
+    tokens = np.zeros((case.B, case.N), np.int32)
+    for r in range(case.R):
+        i = r % case.N
+        if i == 0:
+            continue
+        p = np.exp(rows["lpcd"][r - 1])
+        if r // case.N < 2:  # proposal = target: always accepted
+            probs[r] = p
+            tokens[r // case.N, i] = int(np.argmax(p))
+        else:  # one-hot on a masked token: rejected at node 1
+            t = int(np.flatnonzero(p == 0)[r % 5])
+            probs[r, t] = 1.0
+            tokens[r // case.N, i] = t
+    case.u_acc = np.minimum(case.u_acc, np.float32(0.99))
+    g, o = _check_sample(case, probs, tokens, "always accept / reject")
+    assert np.all(g["accept_len"][:2] == case.N - 1) and np.all(g["accept_len"][2:] == 0)
+
+
+def test_sampled_rejects_trees():
+    case = synth.make_case("b8_tree64", 6, N=12, depth=3, max_children=4, V=600, dp=64, dq=32)
+    case.cfg["mode"] = "sample"
+    probs = np.full((case.R, case.V), 1.0 / case.V, np.float32)
+    tokens = np.ones((1, case.N), np.int32)
+    g = _runner().from_case(case, tokens, draft_probs=probs).run("sample")
+    assert g["status"][0] == oracle.SEQ_NOT_CHAIN and g["next_token"][0] == -1
+
+
+# ------------------------------------------------------------------ full-size workloads
+@pytest.mark.slow
+def test_full_b8_tree64():
+    case = synth.make_case("b8_tree64", 0)
+    _say("b8_tree64: oracle over all 64 rows")
+    tokens = _greedy_tokens(case)
+    _check_greedy(case, tokens, "b8_tree64 seed 0")
+
+
+@pytest.mark.slow
+def test_full_b70_tree64():
+    case = synth.make_case("b70_tree64", 0)
+    _say("b70_tree64: oracle over all 64 rows")
+    tokens = _greedy_tokens(case)
+    _check_greedy(case, tokens, "b70_tree64 seed 0")
+
+
+@pytest.mark.slow
+def test_full_s8_chain16x8():
+    case = synth.make_case("s8_chain16x8", 0)
+    # stand-in drafter: expert logits of every parent row from a plain fp32 matmul
+    dev = torch.device("cuda:0")
+    hp = torch.from_numpy(synth.bf16_to_f32(case.hp)).to(dev)
+    wp = torch.from_numpy(synth.bf16_to_f32(case.wp)).to(dev)
+    z = (hp @ wp.T + torch.from_numpy(case.bias).to(dev)).double().cpu().numpy()
+    del hp, wp
+    parent_logits = np.zeros_like(z)
+    parent_logits[1:] = z[:-1]
+    probs, tokens = synth.sampled_draft(case, parent_logits)
+    _say("s8_chain16x8: oracle over sequences 0, 5, 10, 15")
+    seqs = [0, 5, 10, 15]
+    rows = np.concatenate([np.arange(b * 8, b * 8 + 8) for b in seqs])
+    o = oracle.verify("sample", len(seqs), 8, case.hp[rows], case.hq[rows], case.wp, case.wq,
+                      case.bias, case.bias, case.parents[seqs], tokens[seqs], theta=case.theta,
+                      s=case.s, temperature=case.T, draft_probs=probs[rows],
+                      u_acc=case.u_acc[rows], u_res=case.u_res[rows])
+    g = _runner().from_case(case, tokens, draft_probs=probs).run("sample")
+    sel = dict(accept_len=g["accept_len"][seqs], accept_path=g["accept_path"][seqs],
+               next_token=g["next_token"][seqs], status=g["status"][seqs],
+               row_argmax=g["row_argmax"][rows], row_stats=g["row_stats"][rows],
+               node_stats=g["node_stats"][rows])
+    report = {}
+    amb = parity.compare_rows(sel, o, np.arange(len(rows)), report)
+    parity.compare_nodes(sel, o, case.parents[seqs], amb, report)
+
+    class _Sub:
+        B, N = len(seqs), 8
+        u_acc, u_res = case.u_acc[rows], case.u_res[rows]
+
+    parity.compare_sample(sel, o, _Sub, tokens[seqs], probs[rows], o["row_gap"] <= parity.BOUNDARY_GATE,
+                          report)
+    assert np.all(g["status"] == 0)
+    _say(f"s8_chain16x8: ok {report}; accept lengths {g['accept_len'].tolist()}")
+
+
+@pytest.mark.slow
+def test_full_b8_batch32x64():
+    case = synth.make_case("b8_batch32x64", 0)
+    # draft tokens copy the oracle's argmax in sequences 0 and 1; elsewhere they are random
+    seqs = [0, 1]
+    rows = np.concatenate([np.arange(b * 64, b * 64 + 64) for b in seqs])
+    _say("b8_batch32x64: oracle over sequences 0 and 1")
+    o_rows = oracle.eval_rows(case.hp, case.hq, case.wp, case.wq, case.bias, case.bias,
+                              theta=case.theta, s=case.s, rows=rows)
+    amax = np.full(case.R, -1, np.int32)
+    amax[rows] = o_rows["argmax"]
+    tokens = synth.greedy_tokens(case, amax)
+    o = oracle.verify("greedy", 2, 64, case.hp[rows], case.hq[rows], case.wp, case.wq, case.bias,
+                      case.bias, case.parents[seqs], tokens[seqs], theta=case.theta, s=case.s)
+    g = _runner().from_case(case, tokens).run("greedy")
+    sel = dict(accept_len=g["accept_len"][seqs], accept_path=g["accept_path"][seqs],
+               next_token=g["next_token"][seqs], status=g["status"][seqs],
+               row_argmax=g["row_argmax"][rows], row_stats=g["row_stats"][rows],
+               node_stats=g["node_stats"][rows])
+    report = {}
+    amb = parity.compare_rows(sel, o, np.arange(len(rows)), report)
+    parity.compare_nodes(sel, o, case.parents[seqs], amb, report)
+    parity.compare_greedy(sel, o, case.parents[seqs], amb, report)
+    parity.check_walk_consistent(g, case.parents, tokens)
+    # spot rows across the whole batch
+    spot = np.random.default_rng(0).choice(case.R, 12, replace=False)
+    o_spot = oracle.eval_rows(case.hp, case.hq, case.wp, case.wq, case.bias, case.bias,
+                              theta=case.theta, s=case.s, rows=spot)
+    parity.compare_rows(g, o_spot, spot, report)
+    _say(f"b8_batch32x64: ok {report}")
