@@ -91,7 +91,7 @@ int run(const dcd_problem *p, const dcd_inputs *in, const SampleInputs *smp,
                     out->row_argmax, out->row_stats, out->node_stats};
     hipStream_t st = (hipStream_t)stream;
     if (launch_lmhead(P, I, st) != hipSuccess) return DCD_ERR_HIP;
-    if (launch_combine(P, O, st) != hipSuccess) return DCD_ERR_HIP;
+    if (launch_combine(P, I, O, st) != hipSuccess) return DCD_ERR_HIP;
     if (launch_sequences(P, I, O, smp, st) != hipSuccess) return DCD_ERR_HIP;
     return DCD_OK;
 }
@@ -128,6 +128,9 @@ size_t workspace_layout(Plan &p, char *base) {
     p.cand = (float2 *)take(R * (size_t)p.V * sizeof(float2));
     p.bits = (uint32_t *)take(R * (size_t)p.wstride * sizeof(uint32_t));
     p.rowinfo = (float *)take(R * kRowInfo * sizeof(float));
+    p.tcount = (int *)take(R * p.ntiles * sizeof(int));
+    p.bound = (int *)take(R * sizeof(int));
+    p.nodez = (float4 *)take(R * sizeof(float4));
     return off;
 }
 

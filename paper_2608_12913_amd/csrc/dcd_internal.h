@@ -9,9 +9,15 @@ namespace dcd {
 
 // LM-head tile geometry (gfx950: 64-lane waves, 16x16 MFMA blocks).
 constexpr int kWaveSize = 64;
-constexpr int kTileWaves = 4;                        // waves per workgroup
-constexpr int kTileVBlocks = 4;                      // 16-token blocks per wave
-constexpr int kTileTokens = kTileWaves * kTileVBlocks * 16;   // 256 tokens per workgroup
+#ifndef DCD_TILE_WAVES
+#define DCD_TILE_WAVES 4
+#endif
+#ifndef DCD_TILE_VBLOCKS
+#define DCD_TILE_VBLOCKS 4
+#endif
+constexpr int kTileWaves = DCD_TILE_WAVES;           // waves per workgroup
+constexpr int kTileVBlocks = DCD_TILE_VBLOCKS;       // 16-token blocks per wave
+constexpr int kTileTokens = kTileWaves * kTileVBlocks * 16;   // tokens per workgroup
 constexpr int kTileRBlocks = 4;                      // 16-row blocks per workgroup
 constexpr int kTileRows = kTileRBlocks * 16;         // 64 rows per workgroup
 constexpr int kWordsPerTile = kTileTokens / 32;      // candidate bit words per row and tile
@@ -39,6 +45,9 @@ struct Plan {
     float2 *cand;      // [R][V]        (z_p, z_q) of candidate tokens (sparse)
     uint32_t *bits;    // [R][wstride]  candidate bitmap
     float *rowinfo;    // [R][kRowInfo]
+    int *tcount;       // [R][ntiles]   candidates per (row, tile); bitmap words valid where > 0
+    int *bound;        // [R]           running lower bound on max z_p (order-preserving int key)
+    float4 *nodez;     // [R]           (z_p, z_q, candidate?) of node r's token under its parent row
 };
 
 struct Inputs {
@@ -59,7 +68,7 @@ struct SampleInputs {
 size_t workspace_layout(Plan &p, char *base);  // fills the pointers when base != nullptr
 
 hipError_t launch_lmhead(const Plan &p, const Inputs &in, hipStream_t st);
-hipError_t launch_combine(const Plan &p, const Outputs &out, hipStream_t st);
+hipError_t launch_combine(const Plan &p, const Inputs &in, const Outputs &out, hipStream_t st);
 hipError_t launch_sequences(const Plan &p, const Inputs &in, const Outputs &out,
                             const SampleInputs *smp, hipStream_t st);
 

@@ -56,11 +56,41 @@ __device__ T block_reduce(T x, T *sh, F merge) {
     return r;
 }
 
-__global__ __launch_bounds__(NT) void combine_kernel(Plan P, int32_t *row_argmax, float *row_stats) {
+// Dot product h . w over d elements by the whole workgroup (fp32, fixed order).
+template <int DT>
+__device__ float block_dot(const void *h, const void *w, int d, float *sh) {
+    const int tid = threadIdx.x;
+    float acc = 0.f;
+    if constexpr (DT == kBF16) {
+        const uint16_t *hr = (const uint16_t *)h, *wr = (const uint16_t *)w;
+        for (int k = tid * 8; k < d; k += NT * 8) {
+            const uint4 hv = *(const uint4 *)(hr + k), wv = *(const uint4 *)(wr + k);
+            const uint32_t hs[4] = {hv.x, hv.y, hv.z, hv.w}, ws[4] = {wv.x, wv.y, wv.z, wv.w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                acc += __uint_as_float(hs[e] << 16) * __uint_as_float(ws[e] << 16);
+                acc += __uint_as_float(hs[e] & 0xffff0000u) * __uint_as_float(ws[e] & 0xffff0000u);
+            }
+        }
+    } else {
+        const float *hr = (const float *)h, *wr = (const float *)w;
+        for (int k = tid * 4; k < d; k += NT * 4) {
+            const float4 hv = *(const float4 *)(hr + k), wv = *(const float4 *)(wr + k);
+            acc += hv.x * wv.x + hv.y * wv.y + hv.z * wv.z + hv.w * wv.w;
+        }
+    }
+    return block_reduce(acc, sh, [](float a, float b) { return a + b; });
+}
+
+template <int DT>
+__global__ __launch_bounds__(NT) void combine_kernel(Plan P, Inputs in, int32_t *row_argmax,
+                                                     float *row_stats, int want_node_logits) {
     __shared__ Lse sh_lse[NT];
     __shared__ Top2 sh_top[NT];
     __shared__ int sh_cnt[NT];
+    __shared__ float sh_f[NT];
     const int row = blockIdx.x, tid = threadIdx.x;
+    const size_t esz = DT == kBF16 ? 2 : 4;
 
     // 1. merge the per-tile (max, sum exp) pairs of both models
     Lse lp{-INFINITY, 0.f}, lq{-INFINITY, 0.f};
@@ -78,24 +108,28 @@ __global__ __launch_bounds__(NT) void combine_kernel(Plan P, int32_t *row_argmax
     const float thr = max_p + P.log_theta;
     const float s = P.s;
 
-    // 2. mask, cd score, argmax, log Z over the candidate tokens (ascending per thread)
+    // 2. mask, cd score, argmax, log Z over the candidates; a thread takes whole
+    //    tiles (ascending), skipping tiles without candidates
     Lse lc{-INFINITY, 0.f};
     Top2 best{-INFINITY, -1, -INFINITY};
     int count = 0;
+    const int *tc = P.tcount + (size_t)row * P.ntiles;
     const uint32_t *bw = P.bits + (size_t)row * P.wstride;
     const float2 *cz = P.cand + (size_t)row * P.V;
-    const int nwords = (P.V + 31) / 32;
-    for (int w = tid; w < nwords; w += NT) {
-        uint32_t b = bw[w];
-        while (b) {
-            const int t = w * 32 + __ffs(b) - 1;
-            b &= b - 1;
-            const float2 c = cz[t];
-            if (!(c.x >= thr)) continue;
-            ++count;
-            const float cd = (1.f + s) * (c.x - lse_p) - s * (c.y - lse_q);
-            best = top2_merge(best, Top2{cd, t, -INFINITY});
-            lc = lse_merge(lc, Lse{cd, 1.f});
+    for (int tile = tid; tile < P.ntiles; tile += NT) {
+        if (tc[tile] == 0) continue;
+        for (int w = 0; w < kWordsPerTile; ++w) {
+            uint32_t b = bw[tile * kWordsPerTile + w];
+            while (b) {
+                const int t = (tile * kWordsPerTile + w) * 32 + __ffs(b) - 1;
+                b &= b - 1;
+                const float2 c = cz[t];
+                if (!(c.x >= thr)) continue;
+                ++count;
+                const float cd = (1.f + s) * (c.x - lse_p) - s * (c.y - lse_q);
+                best = top2_merge(best, Top2{cd, t, -INFINITY});
+                lc = lse_merge(lc, Lse{cd, 1.f});
+            }
         }
     }
     lc = block_reduce(lc, sh_lse, lse_merge);
@@ -126,36 +160,33 @@ __global__ __launch_bounds__(NT) void combine_kernel(Plan P, int32_t *row_argmax
             for (int k = 0; k < 8; ++k) row_stats[(size_t)row * 8 + k] = ri[k];
         }
     }
-}
 
-// Logit of token x under one model for the hidden state h (fp32 accumulate).
-template <int DT>
-__device__ float wave_dot(const void *h, const void *w, int d, int x) {
-    const int lane = threadIdx.x % kWaveSize;
-    float acc = 0.f;
-    if constexpr (DT == kBF16) {
-        const uint16_t *hr = (const uint16_t *)h;
-        const uint16_t *wr = (const uint16_t *)w + (size_t)x * d;
-        for (int k = lane * 8; k < d; k += kWaveSize * 8) {
-            const uint4 hv = *(const uint4 *)(hr + k), wv = *(const uint4 *)(wr + k);
-            const uint32_t hs[4] = {hv.x, hv.y, hv.z, hv.w}, ws[4] = {wv.x, wv.y, wv.z, wv.w};
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                acc += __uint_as_float(hs[e] << 16) * __uint_as_float(ws[e] << 16);
-                acc += __uint_as_float(hs[e] & 0xffff0000u) * __uint_as_float(ws[e] & 0xffff0000u);
-            }
-        }
-    } else {
-        const float *hr = (const float *)h;
-        const float *wr = (const float *)w + (size_t)x * d;
-        for (int k = lane * 4; k < d; k += kWaveSize * 4) {
-            const float4 hv = *(const float4 *)(hr + k), wv = *(const float4 *)(wr + k);
-            acc += hv.x * wv.x + hv.y * wv.y + hv.z * wv.z + hv.w * wv.w;
-        }
+    // 3. this row as a draft node: its token's logits under its parent row.  A
+    //    candidate reuses the tile's values (the same numbers the mask saw);
+    //    otherwise the token is outside the mask and, when node statistics are
+    //    wanted, its logits are recomputed here.
+    const int i = row % P.N;
+    if (i == 0) return;
+    const int j = in.parents[row], x = in.tokens[row];
+    if (j < 0 || j >= i || x < 0 || x >= P.V) return;  // the sequence is rejected later
+    const size_t rowj = (size_t)(row - i + j);
+    const int xt = x / kTileTokens;
+    const bool cand = P.tcount[rowj * P.ntiles + xt] > 0 &&
+                      (P.bits[rowj * P.wstride + (x >> 5)] >> (x & 31) & 1u);
+    float4 nz{0.f, 0.f, 0.f, 0.f};
+    if (cand) {
+        const float2 c = P.cand[rowj * P.V + x];
+        nz = float4{c.x, c.y, 1.f, 0.f};
+    } else if (want_node_logits) {
+        float zp = block_dot<DT>((const char *)in.hp + rowj * P.dp * esz,
+                                 (const char *)in.wp + (size_t)x * P.dp * esz, P.dp, sh_f);
+        float zq = block_dot<DT>((const char *)in.hq + rowj * P.dq * esz,
+                                 (const char *)in.wq + (size_t)x * P.dq * esz, P.dq, sh_f);
+        zp = (zp + (in.bp ? in.bp[x] : 0.f)) * P.inv_T;
+        zq = (zq + (in.bq ? in.bq[x] : 0.f)) * P.inv_T;
+        nz = float4{zp, zq, 0.f, 0.f};
     }
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) acc += __shfl_xor(acc, o);
-    return acc;
+    if (tid == 0) P.nodez[row] = nz;
 }
 
 template <int DT, bool SAMPLE>
@@ -166,11 +197,9 @@ __global__ __launch_bounds__(NT) void sequence_kernel(Plan P, Inputs in, Outputs
     __shared__ double sh_sum[NT];
     __shared__ double sh_prefix[NT + 1];
     const int b = blockIdx.x, tid = threadIdx.x, N = P.N, V = P.V;
-    const int lane = tid % kWaveSize, wave = tid / kWaveSize;
     const size_t r0 = (size_t)b * N;
     const int32_t *par = in.parents + r0, *tok = in.tokens + r0;
     const float *ri = P.rowinfo + r0 * kRowInfo;
-    const size_t esz = DT == kBF16 ? 2 : 4;
 
     if (tid < 4) sh_flag[tid] = 0;
     if (tid == 0) sh_int[0] = N;  // first rejected node (sampled)
@@ -201,27 +230,14 @@ __global__ __launch_bounds__(NT) void sequence_kernel(Plan P, Inputs in, Outputs
         return;
     }
 
-    // draft-token statistics: one wave per node, scored by the parent row
+    // draft-token statistics under the parent row (logits gathered by the combine)
     if (out.node_stats && tid < 6) out.node_stats[r0 * 6 + tid] = NAN;
-    for (int i = 1 + wave; i < N; i += NWAVES) {
+    for (int i = 1 + tid; i < N; i += NT) {
         const int j = par[i], x = tok[i];
         const float *rj = ri + (size_t)j * kRowInfo;
-        const size_t rowj = r0 + j;
-        const bool cand = P.bits[rowj * P.wstride + (x >> 5)] >> (x & 31) & 1u;
-        float zp = 0.f, zq = 0.f;
-        if (cand) {
-            const float2 c = P.cand[rowj * V + x];
-            zp = c.x;
-            zq = c.y;
-        }
-        const bool in_mask = cand && zp >= rj[RI_THRESH];
-        if (!cand && out.node_stats) {  // not a candidate: never in the mask; logits for stats
-            zp = wave_dot<DT>((const char *)in.hp + rowj * P.dp * esz, in.wp, P.dp, x);
-            zq = wave_dot<DT>((const char *)in.hq + rowj * P.dq * esz, in.wq, P.dq, x);
-            zp = (zp + (in.bp ? in.bp[x] : 0.f)) * P.inv_T;
-            zq = (zq + (in.bq ? in.bq[x] : 0.f)) * P.inv_T;
-        }
-        const float lpp = zp - rj[RI_LSEP], lpq = zq - rj[RI_LSEQ];
+        const float4 nz = P.nodez[r0 + i];
+        const bool in_mask = nz.z != 0.f && nz.x >= rj[RI_THRESH];
+        const float lpp = nz.x - rj[RI_LSEP], lpq = nz.y - rj[RI_LSEQ];
         const float cd = (1.f + P.s) * lpp - P.s * lpq;
         const float lpcd = in_mask ? cd - rj[RI_LOGZ] : -INFINITY;
         float ratio = NAN;
@@ -229,9 +245,9 @@ __global__ __launch_bounds__(NT) void sequence_kernel(Plan P, Inputs in, Outputs
             const float pe = smp.draft_probs[(r0 + i) * V + x];
             ratio = pe > 0.f ? __expf(lpcd) / pe : INFINITY;
             const bool accept = in_mask && smp.u_acc[r0 + i] <= ratio;
-            if (!accept && lane == 0) atomicMin(&sh_int[0], i);
+            if (!accept) atomicMin(&sh_int[0], i);
         }
-        if (out.node_stats && lane == 0) {
+        if (out.node_stats) {
             float *ns = out.node_stats + (r0 + i) * 6;
             ns[0] = lpp;
             ns[1] = lpq;
@@ -288,9 +304,11 @@ __global__ __launch_bounds__(NT) void sequence_kernel(Plan P, Inputs in, Outputs
         const float p = __expf((1.f + P.s) * (c.x - lse_p) - P.s * (c.y - lse_q) - logZ);
         return residual ? (double)fmaxf(0.f, p - qrow[t]) : (double)p;
     };
+    const int *tc = P.tcount + (r0 + jrow) * P.ntiles;
     auto local_sum = [&](bool residual) {
         double acc = 0.0;
         for (int w = w0; w < w1; ++w) {
+            if (tc[w / kWordsPerTile] == 0) continue;
             uint32_t bits = bw[w];
             while (bits) {
                 const int t = w * 32 + __ffs(bits) - 1;
@@ -338,6 +356,7 @@ __global__ __launch_bounds__(NT) void sequence_kernel(Plan P, Inputs in, Outputs
         double run = 0.0;
         int found = -1, last = -1;
         for (int w = w0; w < w1 && found < 0; ++w) {
+            if (tc[w / kWordsPerTile] == 0) continue;
             uint32_t bits = bw[w];
             while (bits) {
                 const int t = w * 32 + __ffs(bits) - 1;
@@ -366,8 +385,14 @@ __global__ __launch_bounds__(NT) void sequence_kernel(Plan P, Inputs in, Outputs
 
 }  // namespace
 
-hipError_t launch_combine(const Plan &p, const Outputs &out, hipStream_t st) {
-    hipLaunchKernelGGL(combine_kernel, dim3(p.R), dim3(NT), 0, st, p, out.row_argmax, out.row_stats);
+hipError_t launch_combine(const Plan &p, const Inputs &in, const Outputs &out, hipStream_t st) {
+    const int want = out.node_stats != nullptr;
+    if (p.dtype == kBF16)
+        hipLaunchKernelGGL(combine_kernel<kBF16>, dim3(p.R), dim3(NT), 0, st, p, in, out.row_argmax,
+                           out.row_stats, want);
+    else
+        hipLaunchKernelGGL(combine_kernel<kF32>, dim3(p.R), dim3(NT), 0, st, p, in, out.row_argmax,
+                           out.row_stats, want);
     return hipGetLastError();
 }
 
