@@ -50,6 +50,9 @@ def main():
     ap.add_argument("--workload", default="b8_tree64")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
+                    help="only run a plain device-to-device copy of BYTES bytes 10 times (for "
+                         "scaling the HBM byte counters of a profiler run) and exit")
     ap.add_argument("--traffic-kib", type=float, nargs=3, default=None,
                     metavar=("FETCH_KIB", "WRITE_KIB", "SCALE"),
                     help="rocprofv3 FETCH_SIZE and WRITE_SIZE of the LM-head kernel (KiB per "
@@ -61,6 +64,15 @@ def main():
         sys.exit(2)
 
     import torch
+
+    if args.calibrate_copy:
+        src = torch.ones(args.calibrate_copy // 4, dtype=torch.int32, device="cuda:0")
+        dst = torch.empty_like(src)
+        for _ in range(10):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"calibrate_copy_bytes": src.numel() * 4, "copies": 10}), flush=True)
+        return
 
     from paper_2608_12913_amd import synth
     from paper_2608_12913_amd.runner import DeviceProblem

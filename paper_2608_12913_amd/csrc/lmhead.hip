@@ -2,30 +2,34 @@
 // candidate epilogue (Alg. 1 "parallel model evaluation" followed by the
 // per-tile pieces of Eq. (1) and the plausibility mask of Sec. 2.1).
 //
-// Tiling.  One workgroup = kTileWaves waves = one tile of 16*kTileWaves
-// vocabulary tokens x 64 rows.  Each wave owns 16 consecutive tokens and
-// accumulates z^T[16 tokens][64 rows] = W * H^T with 4 MFMA blocks per k-step
+// Tiling.  One workgroup = kTileWaves waves = one tile of kTileTokens vocabulary
+// tokens x 64 rows.  Each wave owns 16*kTileVBlocks consecutive tokens and
+// accumulates z^T[tokens][64 rows] = W * H^T in 16x16 MFMA blocks
 // (v_mfma_f32_16x16x32_bf16, or 4 x v_mfma_f32_16x16x4_f32 for fp32).  K is
-// walked in chunks of 256 bytes of every row.
+// walked in chunks of CB bytes of every row; the expert head first, then the
+// amateur head, through the same registers and LDS.
 //
-// Weight stream (HBM-bound part).  A wave reads its 16 rows with non-temporal
-// 128-bit loads, 4 rows x 256 contiguous bytes per instruction, two chunks in
-// flight.  HBM3E delivers the most bandwidth for exactly this shape (long runs
-// per row, few rows open per wave, streaming cache policy); the MFMA A-fragment
-// shape (16 rows x 64 bytes per instruction) reaches noticeably less.  The
-// chunk is therefore transposed through a wave-private LDS buffer into
-// fragment order.  Hidden states (the B operand, shared by all waves) are
-// staged per chunk in a double-buffered LDS tile.  Both LDS tiles use an XOR
-// swizzle (16-byte column c of row m stored at slot c ^ (m mod 16)) so the
-// fragment reads of 16 lanes hit 16 distinct bank groups.
+// Weight stream (the HBM-bound part).  A wave reads its rows with non-temporal
+// 128-bit loads, RPI rows x CB contiguous bytes per instruction.  On MI355X this
+// shape (long runs per row, every tile resident at once) streams HBM3E far
+// faster than the MFMA A-fragment shape (16 rows x 64 bytes per instruction), so
+// each chunk is transposed through a wave-private LDS tile into fragment order.
+// Hidden states (the B operand, shared by all waves) are staged per chunk into
+// one of two LDS tiles.  Both tiles are XOR-swizzled (16-byte column c of row m
+// at slot c ^ (m mod LPR)) so fragment reads of 16 lanes hit distinct bank
+// groups.  One batch of loads is in flight per wave; the amateur head's first
+// batch is issued before the expert epilogue, so the stream does not stop
+// between the two heads.
 //
 // Epilogue.  Per (row, tile): the tile max and sum of exp of both models, and
 // the plausibility candidates: tokens whose expert logit is within ln(theta)
-// of a lower bound on the row max (the larger of the tile max and a running
-// per-row maximum shared through an atomic).  The final mask
-// {z_p >= row max + ln theta} can only contain candidates.  Candidate logits go
-// to a sparse [row][token] array, their positions to a bitmap, their number
-// per (row, tile) to a count array.
+// of the tile max.  A tile whose expert max is itself below a running lower
+// bound on the row max (an atomic maximum over the tiles that have finished
+// their expert pass) + ln(theta) cannot contain mask members and drops its
+// candidates.  Both bounds are <= the row max, so the final mask
+// {z_p >= row max + ln theta} only contains candidates.  Candidate logits go to
+// a sparse [row][token] array, their positions to a bitmap, their number per
+// (row, tile) to a count array.
 #include "dcd_internal.h"
 
 namespace dcd {
@@ -35,27 +39,34 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
+#ifndef DCD_CHUNK_BYTES
+#define DCD_CHUNK_BYTES 128
+#endif
+// minimum waves per SIMD: 2 keeps two 4-wave tiles resident per CU
+#ifndef DCD_LMHEAD_MIN_BLOCKS
+#define DCD_LMHEAD_MIN_BLOCKS 2
+#endif
+
 constexpr int NW = kTileWaves;
 constexpr int VB = kTileVBlocks;          // 16-token blocks per wave
 constexpr int NT = NW * kWaveSize;        // threads per workgroup
 constexpr int TS = kTileTokens;           // tokens per tile
 constexpr int RB = kTileRBlocks;          // 16-row blocks
 constexpr int ROWS = kTileRows;           // 64
-#ifndef DCD_CHUNK_BYTES
-#define DCD_CHUNK_BYTES 128
-#endif
-
 constexpr int CB = DCD_CHUNK_BYTES;       // bytes of every row per K-chunk
 constexpr int LPR = CB / 16;              // lanes per row in a weight load instruction
 constexpr int RPI = kWaveSize / LPR;      // rows per weight load instruction
-constexpr int WLOADS = 16 * kTileVBlocks / RPI;  // weight load instructions per wave and chunk
+constexpr int WLOADS = 16 * VB / RPI;     // weight load instructions per wave and chunk
 constexpr int KS = CB / 64;               // MFMA k-steps per chunk
 constexpr int HLOADS = ROWS * CB / (NT * 16);  // 16-byte hidden-state loads per thread and chunk
-constexpr int WTILE = VB * 16 * CB;       // bytes of one wave's weight chunk (16*VB rows)
+constexpr int WTILE = VB * 16 * CB;       // bytes of one wave's weight chunk
 constexpr int HTILE = ROWS * CB;          // bytes of one hidden-state chunk
+constexpr int QX = LPR / RPI > 0 ? LPR / RPI : 1;  // distinct weight-row swizzles per lane
 static_assert(HLOADS >= 1 && ROWS * CB == HLOADS * NT * 16, "hidden-state staging must tile");
-static_assert(CB % 64 == 0 && WLOADS * RPI == 16 * kTileVBlocks, "weight chunk must tile");
-static_assert(TS == 16 * VB * NW && TS % 32 == 0, "tile = 16*VB tokens per wave, whole bitmap words");
+static_assert(CB % 64 == 0 && WLOADS * RPI == 16 * VB && LPR % RPI == 0 || RPI % LPR == 0,
+              "weight chunk must tile");
+static_assert(TS == 16 * VB * NW && TS % 32 == 0 && TS <= NT, "tile = 16*VB tokens per wave");
+static_assert((NT / LPR) % LPR == 0, "hidden-state rows of one thread share a swizzle");
 
 // One 16-byte A fragment x one 16-byte B fragment, accumulated into c.
 template <int DT>
@@ -85,78 +96,57 @@ __device__ __forceinline__ u32x4 ld_lds(const char *p) { return *reinterpret_cas
 // rows touch distinct bank groups
 __device__ __forceinline__ int swz(int m, int c) { return m * CB + ((c ^ (m % LPR)) << 4); }
 
-struct ModelArgs {
-    const char *h;      // [R][d] elements
-    const char *w;      // [V][d] elements
-    int d;              // hidden size (elements)
-};
-
-// The loads of one K-chunk: this wave's 16 weight rows and this thread's share of
-// the 64 hidden-state rows.
+// The loads of one K-chunk: this wave's weight rows and this thread's share of the
+// 64 hidden-state rows.
 struct Batch {
     u32x4 w[WLOADS];
     u32x4 h[HLOADS];
     bool hok;  // the hidden-state columns are inside the row (false only in the K tail)
 };
 
-// Accumulate one model's logits for this workgroup's tile.
-//   acc[vb][rb]: lane l holds z[token tok0 + 16vb + 4(l/16) + j][row row0 + 16rb + l%16]
-// RAGGED: some of the wave's 16*VB rows lie past the vocabulary (only in the last
-// tile); their loads are clamped to the last row and their results discarded.
-template <int DT, bool RAGGED>
-__device__ __forceinline__ void accumulate(const ModelArgs &m, int R, int V, int row0, int tok0,
-                                           char *hbuf, char *wbuf, f32x4 (&acc)[VB][RB]) {
-    constexpr int ESZ = DT == kBF16 ? 2 : 4;
-    const int tid = threadIdx.x, lane = tid % kWaveSize;
-    const int n = lane % 16, g = lane / 16;
-    const uint32_t rowbytes = (uint32_t)m.d * ESZ;
-    const int nch = (int)((rowbytes + CB - 1) / CB);
-
-    // Weight loads: lane (r, c) = (lane / LPR, lane % LPR) reads 16 bytes at column c
-    // of row RPI*q + r of the wave's 16*VB rows, RPI rows x CB contiguous bytes per
-    // instruction.  Address = wave-uniform row base (scalar registers) + a 32-bit
-    // lane offset, so the loads use the scalar-base form.
-    const int wr = lane / LPR, wc = lane % LPR;
-    const int tbase = min(tok0, V - 1);
-    const char *wbase = m.w + (size_t)tbase * rowbytes;
-    const uint32_t wlane = (uint32_t)wr * rowbytes;
-    uint32_t woff[RAGGED ? WLOADS : 1];  // ragged: per-instruction clamped row offsets
-    if constexpr (RAGGED) {
-#pragma unroll
-        for (int q = 0; q < WLOADS; ++q)
-            woff[q] = (uint32_t)(min(tok0 + RPI * q + wr, V - 1) - tbase) * rowbytes;
-    }
-    // Hidden-state loads: thread -> (row, 16-byte column) of the 64 x CB chunk; rows
-    // past R re-read row R-1 (results discarded).
-    const int hc = tid % LPR, hr0 = tid / LPR;
-    const char *hbase = m.h + (size_t)row0 * rowbytes;
+// Per-thread load addresses of one model's weight and hidden-state streams.
+// RAGGED: the tile reaches past the vocabulary; weight rows are clamped to the
+// last row (their results are discarded).
+template <bool RAGGED>
+struct Stream {
+    const char *wbase, *hbase;
+    uint32_t rowbytes, wlane;
+    uint32_t woff[RAGGED ? WLOADS : 1];
     uint32_t hoff[HLOADS];
-#pragma unroll
-    for (int p = 0; p < HLOADS; ++p)
-        hoff[p] = (uint32_t)(min(row0 + hr0 + p * (NT / LPR), R - 1) - row0) * rowbytes;
+    int nch, wc, hc;
 
-    // LDS addresses (swizzled, see swz): the lane-dependent parts are formed once.
-    // Weight row RPI*q + wr of the wave tile: its swizzle only depends on q % (LPR/RPI).
-    constexpr int QX = LPR / RPI;  // distinct weight-row swizzles per lane
-    int wst[QX];
+    // Weight loads: lane (r, c) = (lane / LPR, lane % LPR) reads 16 bytes at column
+    // c of row RPI*q + r of the wave's rows (RPI rows x CB contiguous bytes per
+    // instruction); address = wave-uniform row base (scalar registers) + a 32-bit
+    // lane offset.  Hidden-state loads: thread -> (row, 16-byte column) of the
+    // 64 x CB chunk; rows past R re-read row R-1 (results discarded).
+    __device__ __forceinline__ void init(const void *h, const void *w, int d, int esz, int R, int V,
+                                         int row0, int tok0) {
+        const int tid = threadIdx.x, lane = tid % kWaveSize;
+        const int wr = lane / LPR;
+        wc = lane % LPR;
+        hc = tid % LPR;
+        rowbytes = (uint32_t)d * esz;
+        nch = (int)((rowbytes + CB - 1) / CB);
+        const int tbase = min(tok0, V - 1);
+        wbase = (const char *)w + (size_t)tbase * rowbytes;
+        wlane = (uint32_t)wr * rowbytes;
+        if constexpr (RAGGED) {
 #pragma unroll
-    for (int k = 0; k < QX; ++k) wst[k] = swz(RPI * k + wr, wc);
-    const int hst = swz(hr0, hc);  // rows hr0 + p*NT/LPR share hr0's swizzle (NT/LPR % LPR == 0)
-    static_assert((NT / LPR) % LPR == 0, "hidden-state rows of one thread share a swizzle");
-    int frag[KS];  // fragment column 4s+g of row n (rows 16vb+n / 16rb+n add constants)
+            for (int q = 0; q < WLOADS; ++q)
+                woff[q] = (uint32_t)(min(tok0 + RPI * q + wr, V - 1) - tbase) * rowbytes;
+        }
+        hbase = (const char *)h + (size_t)row0 * rowbytes;
+        const int hr0 = tid / LPR;
 #pragma unroll
-    for (int s = 0; s < KS; ++s) frag[s] = swz(n, 4 * s + g);
-    static_assert(16 % LPR == 0 || LPR % 16 == 0, "fragment rows 16vb+n share row n's swizzle");
-
-#pragma unroll
-    for (int vb = 0; vb < VB; ++vb)
-#pragma unroll
-        for (int rb = 0; rb < RB; ++rb) acc[vb][rb] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int p = 0; p < HLOADS; ++p)
+            hoff[p] = (uint32_t)(min(row0 + hr0 + p * (NT / LPR), R - 1) - row0) * rowbytes;
+    }
 
     // In the K tail (rowbytes not a multiple of CB) a weight lane past the row end
     // re-reads the row's last 16 bytes (finite values) and the hidden-state
     // columns there are zero, so those products vanish.
-    auto issue = [&](int c, Batch &b) {
+    __device__ __forceinline__ void issue(int c, Batch &b) const {
         const uint32_t col = (uint32_t)c * CB + wc * 16;
         const uint32_t wcol = col < rowbytes ? col : rowbytes - 16;
 #pragma unroll
@@ -170,52 +160,92 @@ __device__ __forceinline__ void accumulate(const ModelArgs &m, int R, int V, int
         b.hok = hcol < rowbytes;
 #pragma unroll
         for (int p = 0; p < HLOADS; ++p) b.h[p] = ld16(hbase + (hoff[p] + (b.hok ? hcol : 0u)));
-    };
-    // arrived batch -> LDS: hidden states into the shared tile (zero in the K tail),
-    // the wave's weights into its private transpose tile.  Nothing inspects loaded
-    // registers before this point, so no wait is forced on loads still in flight.
-    auto stage = [&](const Batch &b) {
-#pragma unroll
-        for (int p = 0; p < HLOADS; ++p)
-            st_lds(hbuf + hst + p * (NT / LPR) * CB, b.hok ? b.h[p] : u32x4{0u, 0u, 0u, 0u});
-#pragma unroll
-        for (int q = 0; q < WLOADS; ++q) st_lds(wbuf + wst[q % QX] + (q / QX) * (QX * RPI) * CB, b.w[q]);
-    };
-    auto compute = [&]() {
-#pragma unroll
-        for (int s = 0; s < KS; ++s) {
-            // one k-step at a time: hoisting every fragment read of the chunk would
-            // cost KS times the fragment registers
-            __builtin_amdgcn_sched_barrier(0);
-            u32x4 bfr[RB];
-#pragma unroll
-            for (int rb = 0; rb < RB; ++rb) bfr[rb] = ld_lds(hbuf + frag[s] + 16 * rb * CB);
-#pragma unroll
-            for (int vb = 0; vb < VB; ++vb) {
-                const u32x4 a = ld_lds(wbuf + frag[s] + 16 * vb * CB);
-#pragma unroll
-                for (int rb = 0; rb < RB; ++rb) acc[vb][rb] = mma<DT>(a, bfr[rb], acc[vb][rb]);
-            }
-        }
-    };
+    }
+};
 
-    // Pipeline: one batch in flight.  Chunk c is staged (its registers are then
-    // free), chunk c+1 is issued, chunk c is computed.  One hidden-state tile: a
-    // barrier before staging (every wave is done reading chunk c-1) and one after
-    // (the tile is complete).  The weight tile is wave-private, so the wave's own
-    // program order protects it.  The scheduling barrier pins the prefetch before
-    // the compute (left free, the scheduler may sink the loads).
-    Batch b0;
-    issue(0, b0);
-    for (int c = 0; c < nch; ++c) {
-        if (c) __syncthreads();
-        stage(b0);
-        if (c + 1 < nch) issue(c + 1, b0);
+// Lane-dependent LDS addresses (the rest are immediates).
+struct LdsAddr {
+    int wst[QX];   // weight row RPI*k + wr, column wc (rows RPI*q + wr repeat every QX)
+    int hst;       // hidden-state row hr0, column hc (rows hr0 + p*NT/LPR share it)
+    int frag[KS];  // fragment column 4s+g of row n (rows 16vb+n and 16rb+n add constants)
+
+    __device__ __forceinline__ void init() {
+        const int tid = threadIdx.x, lane = tid % kWaveSize;
+        const int wr = lane / LPR, wc = lane % LPR;
+#pragma unroll
+        for (int k = 0; k < QX; ++k) wst[k] = swz(RPI * k + wr, wc);
+        hst = swz(tid / LPR, tid % LPR);
+        const int n = lane % 16, g = lane / 16;
+#pragma unroll
+        for (int s = 0; s < KS; ++s) frag[s] = swz(n, 4 * s + g);
+    }
+};
+
+// arrived batch -> LDS: hidden states into the shared tile `hb` (zero in the K
+// tail), the wave's weights into its private transpose tile.  Nothing inspects
+// loaded registers before this point, so no wait is forced on loads in flight.
+__device__ __forceinline__ void stage(const Batch &b, char *hb, char *wbuf, const LdsAddr &a) {
+#pragma unroll
+    for (int p = 0; p < HLOADS; ++p)
+        st_lds(hb + a.hst + p * (NT / LPR) * CB, b.hok ? b.h[p] : u32x4{0u, 0u, 0u, 0u});
+#pragma unroll
+    for (int q = 0; q < WLOADS; ++q) st_lds(wbuf + a.wst[q % QX] + (q / QX) * (QX * RPI) * CB, b.w[q]);
+}
+
+template <int DT>
+__device__ __forceinline__ void compute(const char *hb, const char *wbuf, const LdsAddr &a,
+                                        f32x4 (&acc)[VB][RB]) {
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+        // one k-step at a time: hoisting every fragment read of the chunk would
+        // cost KS times the fragment registers
+        __builtin_amdgcn_sched_barrier(0);
+        u32x4 bfr[RB];
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) bfr[rb] = ld_lds(hb + a.frag[s] + 16 * rb * CB);
+#pragma unroll
+        for (int vb = 0; vb < VB; ++vb) {
+            const u32x4 x = ld_lds(wbuf + a.frag[s] + 16 * vb * CB);
+#pragma unroll
+            for (int rb = 0; rb < RB; ++rb) acc[vb][rb] = mma<DT>(x, bfr[rb], acc[vb][rb]);
+        }
+    }
+}
+
+// One pass over a model's K chunks, one batch in flight.  Chunk c is staged (its
+// registers are then free), chunk c+1 is issued, chunk c is computed.  The two
+// hidden-state tiles alternate, so one barrier per chunk suffices: the tile
+// chunk c+1 goes to was last read by chunk c-1, which every wave finished before
+// passing chunk c's barrier; the weight tile is wave-private and protected by the
+// wave's own program order.  Batch b holds chunk 0 on entry.  If `next` is given,
+// its chunk 0 is issued into b after the last chunk was staged, so that stream
+// starts before this pass's epilogue.  The scheduling barriers pin each prefetch
+// ahead of the compute (left free, the scheduler may sink the loads, and the
+// next stage would then wait for them too).
+template <int DT, bool RAGGED>
+__device__ __forceinline__ void run_pass(const Stream<RAGGED> &st, const Stream<RAGGED> *next,
+                                         Batch &b, char *hbuf, char *wbuf, const LdsAddr &a,
+                                         f32x4 (&acc)[VB][RB]) {
+#pragma unroll
+    for (int vb = 0; vb < VB; ++vb)
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) acc[vb][rb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    int c = 0;
+    for (; c + 1 < st.nch; ++c) {
+        char *hb = hbuf + (c & 1) * HTILE;
+        stage(b, hb, wbuf, a);
+        st.issue(c + 1, b);
         __builtin_amdgcn_sched_barrier(0);
         __syncthreads();
-        compute();
+        compute<DT>(hb, wbuf, a, acc);
     }
-    __syncthreads();  // LDS tiles are reused by the next pass
+    char *hb = hbuf + (c & 1) * HTILE;
+    stage(b, hb, wbuf, a);
+    if (next) next->issue(0, b);
+    __builtin_amdgcn_sched_barrier(0);
+    __syncthreads();
+    compute<DT>(hb, wbuf, a, acc);
+    __syncthreads();  // the LDS tiles are reused next
 }
 
 __device__ __forceinline__ float wave_max16_32(float x) {
@@ -227,11 +257,13 @@ __device__ __forceinline__ float wave_sum16_32(float x) {
     return x + __shfl_xor(x, 32);
 }
 
-// Logits of this lane's 16*VB (token, row) values, tile max and sum of exp per row.
+// Logits of this lane's 16*VB (token, row) values and, per row, the tile's max and
+// sum of exp relative to it.  One LDS exchange of (wave max, wave sum) pairs,
+// merged in wave order.
 //   z[vb][rb][j]    logit (divided by T); -inf for tokens >= V
-//   tmax[rb], tsum[rb]   tile max / sum exp(z - max) of row 16rb + lane%16
-__device__ __forceinline__ void tile_softmax(const f32x4 (&acc)[VB][RB], const float *bias, int V,
-                                             int tok0, float inv_T, float *red,
+//   tmax[rb], tsum[rb]   of row 16rb + lane%16
+__device__ __forceinline__ void tile_softmax(const f32x4 (&acc)[VB][RB], const float *bias_lds,
+                                             int V, int tok0, int wtok0, float inv_T, float2 *pairs,
                                              float (&z)[VB][RB][4], float (&tmax)[RB],
                                              float (&tsum)[RB]) {
     const int lane = threadIdx.x % kWaveSize, wave = threadIdx.x / kWaveSize;
@@ -240,9 +272,9 @@ __device__ __forceinline__ void tile_softmax(const f32x4 (&acc)[VB][RB], const f
     for (int vb = 0; vb < VB; ++vb)
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            const int t = tok0 + 16 * vb + 4 * g + j;
-            const bool ok = t < V;
-            const float b = (ok && bias) ? bias[t] : 0.f;
+            const int o = 16 * vb + 4 * g + j;  // token offset inside the wave
+            const bool ok = tok0 + o < V;
+            const float b = bias_lds[wtok0 + o];
 #pragma unroll
             for (int rb = 0; rb < RB; ++rb)
                 z[vb][rb][j] = ok ? (acc[vb][rb][j] + b) * inv_T : -INFINITY;
@@ -255,37 +287,33 @@ __device__ __forceinline__ void tile_softmax(const f32x4 (&acc)[VB][RB], const f
 #pragma unroll
             for (int j = 0; j < 4; ++j) m = fmaxf(m, z[vb][rb][j]);
         m = wave_max16_32(m);
-        if (g == 0) red[wave * ROWS + rb * 16 + n] = m;
-    }
-    __syncthreads();
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb) {
-        float m = red[rb * 16 + n];
-#pragma unroll
-        for (int w = 1; w < NW; ++w) m = fmaxf(m, red[w * ROWS + rb * 16 + n]);
-        tmax[rb] = m;
-    }
-    __syncthreads();  // red is rewritten below
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb) {
         float s = 0.f;
 #pragma unroll
         for (int vb = 0; vb < VB; ++vb)
 #pragma unroll
-            for (int j = 0; j < 4; ++j) s += __expf(z[vb][rb][j] - tmax[rb]);
-        if (tmax[rb] == -INFINITY) s = 0.f;  // nothing finite in this tile row
+            for (int j = 0; j < 4; ++j) s += __expf(z[vb][rb][j] - m);
+        if (m == -INFINITY) s = 0.f;  // nothing finite in this wave row
         s = wave_sum16_32(s);
-        if (g == 0) red[wave * ROWS + rb * 16 + n] = s;
+        if (g == 0) pairs[wave * ROWS + rb * 16 + n] = float2{m, s};
     }
     __syncthreads();
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
-        float s = 0.f;
+        float m = -INFINITY;
 #pragma unroll
-        for (int w = 0; w < NW; ++w) s += red[w * ROWS + rb * 16 + n];
+        for (int w = 0; w < NW; ++w) m = fmaxf(m, pairs[w * ROWS + rb * 16 + n].x);
+        float s = 0.f;
+        if (m != -INFINITY) {
+#pragma unroll
+            for (int w = 0; w < NW; ++w) {
+                const float2 pw = pairs[w * ROWS + rb * 16 + n];
+                if (pw.x != -INFINITY) s += pw.y * __expf(pw.x - m);
+            }
+        }
+        tmax[rb] = m;
         tsum[rb] = s;
     }
-    __syncthreads();  // red is reused by the next phase
+    __syncthreads();  // the pairs are reused
 }
 
 // float <-> int keys whose signed-integer order is the float order (for atomicMax)
@@ -297,59 +325,59 @@ __device__ __forceinline__ float key_value(int k) {
     return __int_as_float(k >= 0 ? k : k ^ 0x7fffffff);
 }
 
-constexpr int kHTiles = 1;  // hidden-state tiles in LDS
+constexpr int kHTiles = 2;  // hidden-state tiles in LDS
 // epilogue scratch (row reductions, candidate words and counts) reuses the
-// hidden-state tiles, which are idle once a pass has accumulated
-constexpr size_t kEpilogueBytes = NW * ROWS * sizeof(float) + ROWS * kWordsPerTile * sizeof(uint32_t) +
+// hidden-state tiles, which are idle between passes
+constexpr size_t kEpilogueBytes = NW * ROWS * sizeof(float2) + ROWS * kWordsPerTile * sizeof(uint32_t) +
                                   ROWS * sizeof(int);
 static_assert(kEpilogueBytes <= (size_t)kHTiles * HTILE, "epilogue scratch must fit the hidden-state tiles");
-constexpr size_t kLdsBytes = kHTiles * HTILE + NW * WTILE;
+constexpr size_t kLdsBytes = kHTiles * HTILE + NW * WTILE + 2 * TS * sizeof(float);
 
-// minimum waves per SIMD: 2 keeps two 4-wave tiles resident per CU
-#ifndef DCD_LMHEAD_MIN_BLOCKS
-#define DCD_LMHEAD_MIN_BLOCKS 2
-#endif
-
-template <int DT>
-__global__ __launch_bounds__(NT, DCD_LMHEAD_MIN_BLOCKS) void lmhead_kernel(Plan P, Inputs in) {
-    extern __shared__ __align__(16) char lds[];
-    char *hbuf = lds;                                       // [kHTiles][64][CB] hidden states
-    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWaveSize);  // wave-uniform
-    char *wbuf = lds + kHTiles * HTILE + wave * WTILE;      // this wave's [16*VB][CB] weights
-    // epilogue scratch, aliasing the hidden-state tiles (used only between passes)
-    float *red = reinterpret_cast<float *>(lds);                            // [NW][64]
-    uint32_t *twords = reinterpret_cast<uint32_t *>(red + NW * ROWS);      // [64][words]
-    int *tcnt = reinterpret_cast<int *>(twords + ROWS * kWordsPerTile);     // [64]
-
-    // workgroup -> (vocabulary tile, row block); the row blocks of one tile are
-    // dispatched back to back on the same XCD (workgroup id modulo 8) so the
-    // tile's weights are re-read from that XCD's L2
-    const int id = blockIdx.x, xcd = id % 8, local = id / 8;
-    const int rblk = local % P.nrb;
-    const int tile = (local / P.nrb) * 8 + xcd;
-    if (tile >= P.ntiles) return;
-    const int row0 = rblk * ROWS;
-    const int lane = threadIdx.x % kWaveSize;
+template <int DT, bool RAGGED>
+__device__ __forceinline__ void tile_body(const Plan &P, const Inputs &in, int tile, int row0,
+                                          char *lds) {
+    constexpr int ESZ = DT == kBF16 ? 2 : 4;
+    const int tid = threadIdx.x, lane = tid % kWaveSize;
+    const int wave = __builtin_amdgcn_readfirstlane(tid / kWaveSize);  // wave-uniform
     const int n = lane % 16, g = lane / 16;
-    const int tok0 = tile * TS + wave * (16 * VB);
+    const int wtok0 = wave * (16 * VB);  // wave's first token inside the tile
+    const int tok0 = tile * TS + wtok0;
+
+    char *hbuf = lds;                                   // [2][64][CB] hidden states
+    char *wbuf = lds + kHTiles * HTILE + wave * WTILE;  // this wave's [16*VB][CB] weights
+    float *bias_p = reinterpret_cast<float *>(lds + kHTiles * HTILE + NW * WTILE);  // [TS]
+    float *bias_q = bias_p + TS;                                                     // [TS]
+    // epilogue scratch, aliasing the hidden-state tiles (used only between passes)
+    float2 *pairs = reinterpret_cast<float2 *>(lds);                       // [NW][64]
+    uint32_t *twords = reinterpret_cast<uint32_t *>(pairs + NW * ROWS);   // [64][words]
+    int *tcnt = reinterpret_cast<int *>(twords + ROWS * kWordsPerTile);    // [64]
+
+    // both models' bias for the tile (0 past the vocabulary or without a bias);
+    // ordered before their use by the pass barriers
+    if (tid < TS) {
+        const int t = tile * TS + tid;
+        bias_p[tid] = (t < P.V && in.bp) ? in.bp[t] : 0.f;
+        bias_q[tid] = (t < P.V && in.bq) ? in.bq[t] : 0.f;
+    }
+
+    Stream<RAGGED> sp, sq;
+    sp.init(in.hp, in.wp, P.dp, ESZ, P.R, P.V, row0, tok0);
+    sq.init(in.hq, in.wq, P.dq, ESZ, P.R, P.V, row0, tok0);
+    LdsAddr a;
+    a.init();
 
     f32x4 acc[VB][RB];
     float z[VB][RB][4];
     float pmax[RB], psum[RB], qmax[RB], qsum[RB];
     uint32_t flags[RB];  // bit (vb*4 + j): tile-local candidate
+    Batch b;
 
-    // ---- expert head
-    const bool ragged = tok0 + 16 * VB > P.V;  // wave-uniform
-    if (ragged)
-        accumulate<DT, true>(ModelArgs{(const char *)in.hp, (const char *)in.wp, P.dp}, P.R, P.V,
-                             row0, tok0, hbuf, wbuf, acc);
-    else
-        accumulate<DT, false>(ModelArgs{(const char *)in.hp, (const char *)in.wp, P.dp}, P.R, P.V,
-                              row0, tok0, hbuf, wbuf, acc);
-    tile_softmax(acc, in.bp, P.V, tok0, P.inv_T, red, z, pmax, psum);
-    // Tile-local candidates: z_p within ln(theta) of the tile max.  Their expert
-    // logits are parked in the sparse candidate array; the final decision waits
-    // for the amateur pass, when the running row bound is (nearly) the row max.
+    // ---- expert head (the amateur stream starts before its epilogue)
+    sp.issue(0, b);
+    run_pass<DT, RAGGED>(sp, &sq, b, hbuf, wbuf, a, acc);
+    tile_softmax(acc, bias_p, P.V, tok0, wtok0, P.inv_T, pairs, z, pmax, psum);
+    // tile-local candidates: z_p within ln(theta) of the tile max; their expert
+    // logits are parked in the sparse candidate array
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
         const int row = row0 + rb * 16 + n;
@@ -371,27 +399,25 @@ __global__ __launch_bounds__(NT, DCD_LMHEAD_MIN_BLOCKS) void lmhead_kernel(Plan 
     }
 
     // ---- amateur head
-    if (ragged)
-        accumulate<DT, true>(ModelArgs{(const char *)in.hq, (const char *)in.wq, P.dq}, P.R, P.V,
-                             row0, tok0, hbuf, wbuf, acc);
-    else
-        accumulate<DT, false>(ModelArgs{(const char *)in.hq, (const char *)in.wq, P.dq}, P.R, P.V,
-                              row0, tok0, hbuf, wbuf, acc);
-    // the hidden-state tiles are idle now: clear the candidate words and counts
-    // (ordered before their use by the barriers inside tile_softmax)
-    for (int i = threadIdx.x; i < ROWS * kWordsPerTile; i += NT) twords[i] = 0;
-    if (threadIdx.x < ROWS) tcnt[threadIdx.x] = 0;
-    tile_softmax(acc, in.bq, P.V, tok0, P.inv_T, red, z, qmax, qsum);
-    // Final candidates: z_p >= max(tile max, running row bound) + ln(theta).  Both
-    // bounds are <= the row max, so the plausibility mask (z_p >= row max +
-    // ln theta) never loses a member.
+    run_pass<DT, RAGGED>(sq, nullptr, b, hbuf, wbuf, a, acc);
+    // the running bound of the lane's rows (read before the softmax, so the load
+    // latency overlaps it); the hidden-state tiles are idle: clear the candidate
+    // words and counts (ordered before their use by the barriers in tile_softmax)
+    float bnd[RB];
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+        const int row = min(row0 + rb * 16 + n, P.R - 1);
+        bnd[rb] = flags[rb] ? key_value(__atomic_load_n(&P.bound[row], __ATOMIC_RELAXED)) : 0.f;
+    }
+    for (int i = tid; i < ROWS * kWordsPerTile; i += NT) twords[i] = 0;
+    if (tid < ROWS) tcnt[tid] = 0;
+    tile_softmax(acc, bias_q, P.V, tok0, wtok0, P.inv_T, pairs, z, qmax, qsum);
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
         const int row = row0 + rb * 16 + n;
-        const uint32_t f = flags[rb];
+        // a tile whose expert max is below the row bound + ln(theta) holds no mask member
+        const uint32_t f = pmax[rb] >= bnd[rb] + P.log_theta ? flags[rb] : 0u;
         if (f == 0) continue;
-        const float b = fmaxf(pmax[rb], key_value(__atomic_load_n(&P.bound[row], __ATOMIC_RELAXED)));
-        const float thr = b + P.log_theta;
 #pragma unroll
         for (int vb = 0; vb < VB; ++vb) {
             uint32_t bits = 0;
@@ -399,14 +425,11 @@ __global__ __launch_bounds__(NT, DCD_LMHEAD_MIN_BLOCKS) void lmhead_kernel(Plan 
             for (int j = 0; j < 4; ++j)
                 if (f >> (vb * 4 + j) & 1u) {
                     const int t = tok0 + 16 * vb + 4 * g + j;
-                    float2 *c = P.cand + (size_t)row * P.V + t;
-                    if (c->x >= thr) {
-                        c->y = z[vb][rb][j];
-                        bits |= 1u << (t % 32);
-                    }
+                    P.cand[(size_t)row * P.V + t].y = z[vb][rb][j];
+                    bits |= 1u << (t % 32);
                 }
             if (bits) {
-                const int word = (16 * VB * wave + 16 * vb) / 32;
+                const int word = (wtok0 + 16 * vb) / 32;
                 atomicOr(&twords[(rb * 16 + n) * kWordsPerTile + word], bits);
                 atomicAdd(&tcnt[rb * 16 + n], __popc(bits));
             }
@@ -415,7 +438,7 @@ __global__ __launch_bounds__(NT, DCD_LMHEAD_MIN_BLOCKS) void lmhead_kernel(Plan 
     __syncthreads();
     // per (row, tile): the candidate count, the bitmap words where it is nonzero,
     // and the softmax partials of both models
-    for (int i = threadIdx.x; i < ROWS * kWordsPerTile; i += NT) {
+    for (int i = tid; i < ROWS * kWordsPerTile; i += NT) {
         const int r = i / kWordsPerTile, row = row0 + r;
         if (row < P.R && tcnt[r] > 0)
             P.bits[(size_t)row * P.wstride + tile * kWordsPerTile + i % kWordsPerTile] = twords[i];
@@ -431,6 +454,23 @@ __global__ __launch_bounds__(NT, DCD_LMHEAD_MIN_BLOCKS) void lmhead_kernel(Plan 
     }
 }
 
+template <int DT>
+__global__ __launch_bounds__(NT, DCD_LMHEAD_MIN_BLOCKS) void lmhead_kernel(Plan P, Inputs in) {
+    extern __shared__ __align__(16) char lds[];
+    // workgroup -> (vocabulary tile, row block); the row blocks of one tile are
+    // dispatched back to back on the same XCD (workgroup id modulo 8) so the
+    // tile's weights are re-read from that XCD's L2
+    const int id = blockIdx.x, xcd = id % 8, local = id / 8;
+    const int rblk = local % P.nrb;
+    const int tile = (local / P.nrb) * 8 + xcd;
+    if (tile >= P.ntiles) return;
+    const int row0 = rblk * ROWS;
+    if ((tile + 1) * TS > P.V)  // workgroup-uniform: only the last tile is ragged
+        tile_body<DT, true>(P, in, tile, row0, lds);
+    else
+        tile_body<DT, false>(P, in, tile, row0, lds);
+}
+
 // Row bounds start at -inf for every call.
 __global__ void init_bound_kernel(int *bound, int R) {
     const int r = blockIdx.x * blockDim.x + threadIdx.x;
@@ -440,7 +480,7 @@ __global__ void init_bound_kernel(int *bound, int R) {
 }  // namespace
 
 hipError_t launch_lmhead(const Plan &p, const Inputs &in, hipStream_t st) {
-    // the tile needs more than 64 KB of LDS (gfx950 has 160 KB per CU)
+    // the tile may need more than 64 KB of LDS (gfx950 has 160 KB per CU)
     static const hipError_t attr = [] {
         hipError_t e = hipFuncSetAttribute((const void *)lmhead_kernel<kBF16>,
                                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsBytes);
