@@ -6,7 +6,7 @@ statistics, tree walk) over one Llama-3-8B/1B-shaped 64-node draft tree with
 every input resident in HBM.  Prints one JSON line.
 
   python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload b8_tree64]
-                  [--no-cpu-baseline] [--traffic-kib FETCH WRITE SCALE]
+                  [--no-cpu-baseline] [--calibrate-copy BYTES]
 """
 from __future__ import annotations
 
@@ -53,10 +53,6 @@ def main():
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
                     help="only run a plain device-to-device copy of BYTES bytes 10 times (for "
                          "scaling the HBM byte counters of a profiler run) and exit")
-    ap.add_argument("--traffic-kib", type=float, nargs=3, default=None,
-                    metavar=("FETCH_KIB", "WRITE_KIB", "SCALE"),
-                    help="rocprofv3 FETCH_SIZE and WRITE_SIZE of the LM-head kernel (KiB per "
-                         "dispatch) and the copy-kernel calibration factor")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
@@ -129,14 +125,11 @@ def main():
     nodes_per_s = R / (ms_step * 1e-3)
     kbytes = lmhead_bytes(case)
     achieved = kbytes / (ms_lmhead * 1e-3) / 1e9
-    traffic = None
-    if args.traffic_kib is not None:
-        fetch, write, scale = args.traffic_kib
-        traffic = (fetch + write) * 1024.0 * scale
+    traffic, traffic_src = counted_traffic()
     roofline = dict(bound="hbm", achieved=round(achieved, 1), peak=HBM_PEAK_GBS, unit="GB/s",
                     frac=round(achieved / HBM_PEAK_GBS, 4), traffic=traffic,
                     kernel="lmhead_kernel", algorithmic_bytes=kbytes,
-                    avg_us=round(ms_lmhead * 1e3, 2))
+                    avg_us=round(ms_lmhead * 1e3, 2), traffic_source=traffic_src)
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -166,23 +159,53 @@ def main():
     print(json.dumps(line), flush=True)
 
 
-def cpu_baseline(case, tokens, log):
-    """The oracle, untuned, on the host cores: one complete verification of the same
-    workload (every row's LM heads in fp64, mask, cd target, walk)."""
+def counted_traffic():
+    """HBM bytes per LM-head launch from the committed profiler counter summary, or
+    None when the kernel sources have changed since the counters were taken."""
+    import hashlib
+
+    root = os.path.dirname(os.path.abspath(__file__))
+    path = os.path.join(root, "profiles", "lmhead_kernel_b8_tree64_hbm_counters.txt")
+    if not os.path.exists(path):
+        return None, None
+    fields = {}
+    for line in open(path):
+        if ":" in line and not line.startswith(" "):
+            k, v = line.split(":", 1)
+            fields[k.strip()] = v.strip()
+    h = hashlib.sha256()
+    for rel in fields.get("sources", "").split():
+        h.update(open(os.path.join(root, rel), "rb").read())
+    if not fields.get("sources") or h.hexdigest() != fields.get("sources_sha256"):
+        return None, "stale counters (kernel changed since they were taken)"
+    fetch = float(fields["fetch_kib_per_dispatch"]) * float(fields["fetch_scale"])
+    write = float(fields["write_kib_per_dispatch"]) * float(fields["write_scale"])
+    return round((fetch + write) * 1024.0), os.path.relpath(path, root)
+
+
+def cpu_baseline(case, tokens, log, min_seconds=10.0):
+    """The oracle, untuned, on the host cores: complete verifications of the same
+    workload (every row's LM heads in fp64, mask, cd target, walk), repeated until
+    min_seconds have passed; the rate is the mean over the repetitions."""
     import oracle
 
     threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or os.cpu_count()
     hp, hq = oracle.as_f32(case.hp), oracle.as_f32(case.hq)
     wp, wq = oracle.as_f32(case.wp), oracle.as_f32(case.wq)
     log(f"cpu baseline: oracle over {case.R} rows on {threads} threads")
-    t0 = time.perf_counter()
-    oracle.verify("greedy", case.B, case.N, hp, hq, wp, wq, case.bias, case.bias, case.parents,
-                  tokens, theta=case.theta, s=case.s, nthreads=threads)
-    dt = time.perf_counter() - t0
-    log(f"cpu baseline: {dt:.2f} s")
-    return {"value": round(case.R / dt, 3), "unit": "nodes/s", "cores": threads, "kind": "oracle",
-            "sample": f"one full {case.name} verification ({case.R} rows, fp64 oracle), "
-                      f"{dt:.2f} s"}
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        oracle.verify("greedy", case.B, case.N, hp, hq, wp, wq, case.bias, case.bias,
+                      case.parents, tokens, theta=case.theta, s=case.s, nthreads=threads)
+        reps += 1
+        dt = time.perf_counter() - t0
+        if dt >= min_seconds:
+            break
+    log(f"cpu baseline: {reps} verifications in {dt:.2f} s")
+    return {"value": round(reps * case.R / dt, 3), "unit": "nodes/s", "cores": threads,
+            "kind": "oracle",
+            "sample": f"{reps} full {case.name} verifications ({case.R} rows each, fp64 "
+                      f"oracle) in {dt:.2f} s"}
 
 
 if __name__ == "__main__":
