@@ -98,7 +98,7 @@ enum {
 
 typedef struct {
     int32_t batch;       /* B >= 1 sequences                                            */
-    int32_t nodes;       /* N >= 1 nodes per sequence, root included                    */
+    int32_t nodes;       /* 1 <= N <= 4096 nodes per sequence, root included            */
     int32_t vocab;       /* V >= 1                                                      */
     int32_t d_expert;    /* expert hidden size d_p                                      */
     int32_t d_amateur;   /* amateur hidden size d_q                                     */

@@ -22,6 +22,7 @@ int make_plan(const dcd_problem *p, bool sample, Plan &P) {
     if (p->batch < 1 || p->nodes < 1 || p->vocab < 1 || p->d_expert < 1 || p->d_amateur < 1)
         return DCD_ERR_SHAPE;
     const long long R = (long long)p->batch * p->nodes;
+    if (p->nodes > kMaxNodes) return DCD_ERR_SHAPE;
     if (R > kMaxRows || p->vocab > kMaxVocab || p->d_expert > kMaxHidden ||
         p->d_amateur > kMaxHidden)
         return DCD_ERR_SHAPE;
@@ -91,8 +92,7 @@ int run(const dcd_problem *p, const dcd_inputs *in, const SampleInputs *smp,
                     out->row_argmax, out->row_stats, out->node_stats};
     hipStream_t st = (hipStream_t)stream;
     if (launch_lmhead(P, I, st) != hipSuccess) return DCD_ERR_HIP;
-    if (launch_combine(P, I, O, st) != hipSuccess) return DCD_ERR_HIP;
-    if (launch_sequences(P, I, O, smp, st) != hipSuccess) return DCD_ERR_HIP;
+    if (launch_finish(P, I, O, smp, st) != hipSuccess) return DCD_ERR_HIP;
     return DCD_OK;
 }
 
@@ -131,6 +131,7 @@ size_t workspace_layout(Plan &p, char *base) {
     p.tcount = (int *)take(R * p.ntiles * sizeof(int));
     p.bound = (int *)take(R * sizeof(int));
     p.nodez = (float4 *)take(R * sizeof(float4));
+    p.seqdone = (int *)take((size_t)p.B * sizeof(int));
     return off;
 }
 

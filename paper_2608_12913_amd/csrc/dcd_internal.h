@@ -22,6 +22,7 @@ constexpr int kTileRBlocks = 4;                      // 16-row blocks per workgr
 constexpr int kTileRows = kTileRBlocks * 16;         // 64 rows per workgroup
 constexpr int kWordsPerTile = kTileTokens / 32;      // candidate bit words per row and tile
 constexpr int kRowInfo = 16;                         // floats of per-row results
+constexpr int kMaxNodes = 4096;                      // nodes per sequence (staged in LDS)
 
 // rowinfo slots (floats; the argmax is stored as an int bit pattern)
 enum {
@@ -48,6 +49,7 @@ struct Plan {
     int *tcount;       // [R][ntiles]   candidates per (row, tile); bitmap words valid where > 0
     int *bound;        // [R]           running lower bound on max z_p (order-preserving int key)
     float4 *nodez;     // [R]           (z_p, z_q, candidate?) of node r's token under its parent row
+    int *seqdone;      // [B]           rows of each sequence finished by the combine step
 };
 
 struct Inputs {
@@ -65,11 +67,21 @@ struct SampleInputs {
     const float *draft_probs, *u_acc, *u_res;
 };
 
+// float <-> int keys whose signed-integer order is the float order (for atomicMax)
+__device__ __forceinline__ int ordered_key(float f) {
+    const int i = __float_as_int(f);
+    return i >= 0 ? i : i ^ 0x7fffffff;
+}
+__device__ __forceinline__ float key_value(int k) {
+    return __int_as_float(k >= 0 ? k : k ^ 0x7fffffff);
+}
+
 size_t workspace_layout(Plan &p, char *base);  // fills the pointers when base != nullptr
 
+// LM heads with softmax partials and candidates (clears bound and seqdone first)
 hipError_t launch_lmhead(const Plan &p, const Inputs &in, hipStream_t st);
-hipError_t launch_combine(const Plan &p, const Inputs &in, const Outputs &out, hipStream_t st);
-hipError_t launch_sequences(const Plan &p, const Inputs &in, const Outputs &out,
-                            const SampleInputs *smp, hipStream_t st);
+// per-row combination and per-sequence verification (greedy when smp is null)
+hipError_t launch_finish(const Plan &p, const Inputs &in, const Outputs &out,
+                         const SampleInputs *smp, hipStream_t st);
 
 }  // namespace dcd

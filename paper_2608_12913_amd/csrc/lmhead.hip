@@ -316,15 +316,6 @@ __device__ __forceinline__ void tile_softmax(const f32x4 (&acc)[VB][RB], const f
     __syncthreads();  // the pairs are reused
 }
 
-// float <-> int keys whose signed-integer order is the float order (for atomicMax)
-__device__ __forceinline__ int ordered_key(float f) {
-    const int i = __float_as_int(f);
-    return i >= 0 ? i : i ^ 0x7fffffff;
-}
-__device__ __forceinline__ float key_value(int k) {
-    return __int_as_float(k >= 0 ? k : k ^ 0x7fffffff);
-}
-
 constexpr int kHTiles = 2;  // hidden-state tiles in LDS
 // epilogue scratch (row reductions, candidate words and counts) reuses the
 // hidden-state tiles, which are idle between passes
@@ -471,10 +462,12 @@ __global__ __launch_bounds__(NT, DCD_LMHEAD_MIN_BLOCKS) void lmhead_kernel(Plan 
         tile_body<DT, false>(P, in, tile, row0, lds);
 }
 
-// Row bounds start at -inf for every call.
-__global__ void init_bound_kernel(int *bound, int R) {
+// Row bounds start at -inf and the per-sequence row counters of the finishing
+// step at 0, for every call.
+__global__ void init_kernel(int *bound, int R, int *seqdone, int B) {
     const int r = blockIdx.x * blockDim.x + threadIdx.x;
     if (r < R) bound[r] = ordered_key(-INFINITY);
+    if (r < B) seqdone[r] = 0;
 }
 
 }  // namespace
@@ -491,7 +484,9 @@ hipError_t launch_lmhead(const Plan &p, const Inputs &in, hipStream_t st) {
     }();
     if (attr != hipSuccess) return attr;
     const int groups = ((p.ntiles + 7) / 8) * 8 * p.nrb;
-    hipLaunchKernelGGL(init_bound_kernel, dim3((p.R + 255) / 256), dim3(256), 0, st, p.bound, p.R);
+    const int ninit = p.R > p.B ? p.R : p.B;
+    hipLaunchKernelGGL(init_kernel, dim3((ninit + 255) / 256), dim3(256), 0, st, p.bound, p.R, p.seqdone,
+                       p.B);
     if (p.dtype == kBF16)
         hipLaunchKernelGGL(lmhead_kernel<kBF16>, dim3(groups), dim3(NT), kLdsBytes, st, p, in);
     else

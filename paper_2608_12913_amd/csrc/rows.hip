@@ -1,22 +1,27 @@
-// Per-row combination of the LM-head partials and per-sequence verification.
+// Per-row combination of the LM-head partials and per-sequence verification, in
+// one launch.
 //
-// combine_kernel (one workgroup per row):
-//   max_p, log-normalisers of both models from the per-tile (max, sum exp) pairs;
-//   the plausibility mask z_p >= max_p + ln theta (Sec. 2.1) over the candidate
-//   tokens; the cd score (1+s)(z_p - lse_p) - s(z_q - lse_q) of Eq. (1); its log
-//   normaliser over the mask, argmax (lowest id on ties) and top-2 margin.
-// sequence_kernel (one workgroup per sequence):
+// Row phase (one workgroup per row):
+//   max_p and the log-normalisers of both models from the per-tile
+//   (max, sum exp) pairs; the plausibility mask z_p >= max_p + ln theta
+//   (Sec. 2.1) over the candidate tokens; the cd score
+//   (1+s)(z_p - lse_p) - s(z_q - lse_q) of Eq. (1); its log normaliser over the
+//   mask, argmax (lowest id on ties) and top-2 margin; and the row's own draft
+//   token's logits under its parent row.
+// Sequence phase (the workgroup that completes a sequence's last row):
 //   tree / token checks, draft-token statistics under the parent row, then either
-//   the greedy walk from the root or Alg. 1's accept test with residual / bonus
-//   resampling along a chain.
+//   the greedy walk from the root or Alg. 1's accept test with the residual /
+//   bonus draw along a chain.
 // All reductions run in a fixed order, so repeated calls are bit-identical.
 #include "dcd_internal.h"
 
 namespace dcd {
 namespace {
 
-constexpr int NT = 256;
-constexpr int NWAVES = NT / kWaveSize;
+constexpr int NT = 256;                  // threads of the finish kernel (4 waves)
+constexpr int kTilesPerLane = 8;         // vocabulary tiles a lane takes per pass
+constexpr int kPass = kWaveSize * kTilesPerLane;
+constexpr int kList = 1024;              // candidate ids gathered per round
 
 struct Lse {  // running log-sum-exp: value = m + log(s)
     float m, s;
@@ -41,29 +46,59 @@ __device__ __forceinline__ Top2 top2_merge(Top2 a, Top2 b) {
     return Top2{w.v, w.id, fmaxf(w.v2, l.id >= 0 ? l.v : -INFINITY)};
 }
 
-// Fixed-order block reductions through shared memory (tree over thread ids).
-template <typename T, typename F>
-__device__ T block_reduce(T x, T *sh, F merge) {
-    const int tid = threadIdx.x;
-    sh[tid] = x;
-    __syncthreads();
-    for (int w = NT / 2; w > 0; w >>= 1) {
-        if (tid < w) sh[tid] = merge(sh[tid], sh[tid + w]);
-        __syncthreads();
-    }
-    T r = sh[0];
-    __syncthreads();
-    return r;
+// ---------------------------------------------------------------------------
+// Wave-level reductions (64 lanes).  Each is a fixed tree towards lane 0, so the
+// result does not depend on timing; only lane 0's value is meaningful.
+__device__ __forceinline__ Lse wave_lse(Lse x) {
+#pragma unroll
+    for (int d = kWaveSize / 2; d > 0; d >>= 1)
+        x = lse_merge(x, Lse{__shfl_down(x.m, d, kWaveSize), __shfl_down(x.s, d, kWaveSize)});
+    return x;
 }
 
-// Dot product h . w over d elements by the whole workgroup (fp32, fixed order).
+__device__ __forceinline__ Top2 wave_top2(Top2 x) {
+#pragma unroll
+    for (int d = kWaveSize / 2; d > 0; d >>= 1)
+        x = top2_merge(x, Top2{__shfl_down(x.v, d, kWaveSize), __shfl_down(x.id, d, kWaveSize),
+                               __shfl_down(x.v2, d, kWaveSize)});
+    return x;
+}
+
+template <typename T>
+__device__ __forceinline__ T wave_sum(T x) {
+#pragma unroll
+    for (int d = kWaveSize / 2; d > 0; d >>= 1) x += __shfl_down(x, d, kWaveSize);
+    return x;
+}
+
+// Orders one wave's LDS writes before its later LDS reads of other lanes' data
+// (a wave's LDS operations complete in issue order; this stops the compiler
+// from moving memory operations across the point).
+__device__ __forceinline__ void wave_lds_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+}
+
+// exclusive prefix sum over the wave; *total receives the sum of all lanes
+__device__ __forceinline__ int wave_exclusive_scan(int x, int lane, int *total) {
+    int incl = x;
+#pragma unroll
+    for (int d = 1; d < kWaveSize; d <<= 1) {
+        const int y = __shfl_up(incl, d, kWaveSize);
+        if (lane >= d) incl += y;
+    }
+    *total = __shfl(incl, kWaveSize - 1, kWaveSize);
+    return incl - x;
+}
+
+// Dot product h . w over d elements by one wave (fp32, fixed order); lane 0 holds it.
 template <int DT>
-__device__ float block_dot(const void *h, const void *w, int d, float *sh) {
-    const int tid = threadIdx.x;
+__device__ float wave_dot(const void *h, const void *w, int d, int lane) {
     float acc = 0.f;
     if constexpr (DT == kBF16) {
         const uint16_t *hr = (const uint16_t *)h, *wr = (const uint16_t *)w;
-        for (int k = tid * 8; k < d; k += NT * 8) {
+#pragma unroll 4
+        for (int k = lane * 8; k < d; k += kWaveSize * 8) {
             const uint4 hv = *(const uint4 *)(hr + k), wv = *(const uint4 *)(wr + k);
             const uint32_t hs[4] = {hv.x, hv.y, hv.z, hv.w}, ws[4] = {wv.x, wv.y, wv.z, wv.w};
 #pragma unroll
@@ -74,55 +109,180 @@ __device__ float block_dot(const void *h, const void *w, int d, float *sh) {
         }
     } else {
         const float *hr = (const float *)h, *wr = (const float *)w;
-        for (int k = tid * 4; k < d; k += NT * 4) {
+#pragma unroll 4
+        for (int k = lane * 4; k < d; k += kWaveSize * 4) {
             const float4 hv = *(const float4 *)(hr + k), wv = *(const float4 *)(wr + k);
             acc += hv.x * wv.x + hv.y * wv.y + hv.z * wv.z + hv.w * wv.w;
         }
     }
-    return block_reduce(acc, sh, [](float a, float b) { return a + b; });
+    return wave_sum(acc);
 }
 
-template <int DT>
-__global__ __launch_bounds__(NT) void combine_kernel(Plan P, Inputs in, int32_t *row_argmax,
-                                                     float *row_stats, int want_node_logits) {
-    __shared__ Lse sh_lse[NT];
-    __shared__ Top2 sh_top[NT];
-    __shared__ int sh_cnt[NT];
-    __shared__ float sh_f[NT];
-    const int row = blockIdx.x, tid = threadIdx.x;
-    const size_t esz = DT == kBF16 ? 2 : 4;
+__device__ __forceinline__ uint4 mask4(uint4 v, uint32_t m) {
+    return uint4{v.x & m, v.y & m, v.z & m, v.w & m};
+}
 
-    // 1. merge the per-tile (max, sum exp) pairs of both models
-    Lse lp{-INFINITY, 0.f}, lq{-INFINITY, 0.f};
-    const float4 *pr = P.partials + (size_t)row * P.ntiles;
-    for (int t = tid; t < P.ntiles; t += NT) {
-        const float4 v = pr[t];
-        lp = lse_merge(lp, Lse{v.x, v.y});
-        lq = lse_merge(lq, Lse{v.z, v.w});
+__device__ __forceinline__ int popc8(const uint4 (&w)[2]) {
+    return __popc(w[0].x) + __popc(w[0].y) + __popc(w[0].z) + __popc(w[0].w) + __popc(w[1].x) +
+           __popc(w[1].y) + __popc(w[1].z) + __popc(w[1].w);
+}
+
+// Writes the ids of the set bits of one tile's 8 bitmap words whose running
+// index (*idx, advanced over every set bit) falls in [lo, lo + kList) to list[].
+__device__ __forceinline__ void emit_ids(const uint4 (&w)[2], int tile, int lo, int *idx, int *list) {
+    const uint32_t ws[8] = {w[0].x, w[0].y, w[0].z, w[0].w, w[1].x, w[1].y, w[1].z, w[1].w};
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+        uint32_t b = ws[e];
+        while (b) {
+            if (*idx >= lo && *idx < lo + kList)
+                list[*idx - lo] = (tile * kWordsPerTile + e) * 32 + __ffs(b) - 1;
+            ++*idx;
+            b &= b - 1;
+        }
     }
-    lp = block_reduce(lp, sh_lse, lse_merge);
-    lq = block_reduce(lq, sh_lse, lse_merge);
-    const float max_p = lp.m;
-    const float lse_p = lp.m + __logf(lp.s);
-    const float lse_q = lq.m + __logf(lq.s);
+}
+
+// Shared memory of the finish kernel (the dynamic part holds the sequence's
+// parents, tokens and row argmax: 12 bytes per node).
+struct Smem {
+    int list[kList];    // candidate ids (row phase: wave 0; draw: whole group)
+    double wts[kList];  // draw weights
+    int wave_tot[NT / kWaveSize];
+    int flag[4];
+    int ints[4];
+};
+
+// ---------------------------------------------------------------------------
+// Row phase.  wave 0: the row's statistics; wave 1: the row as a draft node.
+template <int DT>
+__device__ void combine_row(const Plan &P, const Inputs &in, int row, int lane, int wave,
+                            int32_t *row_argmax, float *row_stats, bool want_node_logits, int *list) {
+    if (wave == 1) {
+        // this row's draft token under the parent row: from the parent's
+        // candidates when the token is one (the numbers the mask saw), otherwise
+        // (node statistics wanted) a dot product
+        const int i = row % P.N;
+        if (i == 0) return;
+        const int j = in.parents[row], x = in.tokens[row];
+        if (j < 0 || j >= i || x < 0 || x >= P.V) return;  // the sequence is rejected later
+        const size_t rowj = (size_t)(row - i + j);
+        // count, bitmap word and candidate slot are fetched together
+        const int tcnt = P.tcount[rowj * P.ntiles + x / kTileTokens];
+        const uint32_t word = P.bits[rowj * P.wstride + (x >> 5)];
+        const float2 c = P.cand[rowj * P.V + x];
+        const bool cand = tcnt > 0 && (word >> (x & 31) & 1u);
+        float4 nz{0.f, 0.f, 0.f, 0.f};
+        if (cand) {
+            nz = float4{c.x, c.y, 1.f, 0.f};
+        } else if (want_node_logits) {
+            const size_t esz = DT == kBF16 ? 2 : 4;
+            float zp = wave_dot<DT>((const char *)in.hp + rowj * P.dp * esz,
+                                    (const char *)in.wp + (size_t)x * P.dp * esz, P.dp, lane);
+            float zq = wave_dot<DT>((const char *)in.hq + rowj * P.dq * esz,
+                                    (const char *)in.wq + (size_t)x * P.dq * esz, P.dq, lane);
+            zp = (zp + (in.bp ? in.bp[x] : 0.f)) * P.inv_T;
+            zq = (zq + (in.bq ? in.bq[x] : 0.f)) * P.inv_T;
+            nz = float4{zp, zq, 0.f, 0.f};
+        }
+        if (lane == 0) P.nodez[row] = nz;
+        // publish nodez at device scope before the row is counted (wave 0's
+        // results are published by the counting atomic itself)
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+        return;
+    }
+    if (wave != 0) return;
+
+    const float4 *pr = P.partials + (size_t)row * P.ntiles;
+    const int *tc = P.tcount + (size_t)row * P.ntiles;
+    const uint4 *bw = reinterpret_cast<const uint4 *>(P.bits + (size_t)row * P.wstride);
+    const float2 *cz = P.cand + (size_t)row * P.V;
+
+    // the first pass's partials, counts and bitmap words are fetched together
+    float4 v[kTilesPerLane];
+    uint4 w[kTilesPerLane][2];
+    // Loads are issued unconditionally from clamped indices and masked
+    // afterwards (with selects), so that all of them are in flight together.
+    int c[kTilesPerLane];
+    auto issue_partials = [&](int base) {
+#pragma unroll
+        for (int k = 0; k < kTilesPerLane; ++k) v[k] = pr[min(base + lane + k * kWaveSize, P.ntiles - 1)];
+    };
+    auto issue_cands = [&](int base) {
+#pragma unroll
+        for (int k = 0; k < kTilesPerLane; ++k) {
+            const int t = min(base + lane + k * kWaveSize, P.ntiles - 1);
+            c[k] = tc[t];
+            w[k][0] = bw[2 * t];
+            w[k][1] = bw[2 * t + 1];
+        }
+    };
+    auto mask_partials = [&](int base) {
+#pragma unroll
+        for (int k = 0; k < kTilesPerLane; ++k) {
+            const bool ok = base + lane + k * kWaveSize < P.ntiles;
+            v[k] = ok ? v[k] : float4{-INFINITY, 0.f, -INFINITY, 0.f};
+        }
+    };
+    auto mask_cands = [&](int base) {
+#pragma unroll
+        for (int k = 0; k < kTilesPerLane; ++k) {
+            // words of tiles without candidates are stale
+            const uint32_t keep = (base + lane + k * kWaveSize < P.ntiles && c[k] > 0) ? ~0u : 0u;
+            w[k][0] = mask4(w[k][0], keep);
+            w[k][1] = mask4(w[k][1], keep);
+        }
+    };
+    issue_partials(0);
+    issue_cands(0);
+    __builtin_amdgcn_sched_barrier(0);
+    mask_partials(0);
+
+    // 1. per-tile (max, sum exp) pairs of both models -> max_p, lse_p, lse_q
+    Lse lp{-INFINITY, 0.f}, lq{-INFINITY, 0.f};
+    for (int base = 0;;) {
+#pragma unroll
+        for (int k = 0; k < kTilesPerLane; ++k) {
+            lp = lse_merge(lp, Lse{v[k].x, v[k].y});
+            lq = lse_merge(lq, Lse{v[k].z, v[k].w});
+        }
+        base += kPass;
+        if (base >= P.ntiles) break;
+        issue_partials(base);
+        mask_partials(base);
+    }
+    lp = wave_lse(lp);
+    lq = wave_lse(lq);
+    const float max_p = __shfl(lp.m, 0, kWaveSize);
+    const float lse_p = __shfl(lp.m + __logf(lp.s), 0, kWaveSize);
+    const float lse_q = __shfl(lq.m + __logf(lq.s), 0, kWaveSize);
     const float thr = max_p + P.log_theta;
     const float s = P.s;
 
-    // 2. mask, cd score, argmax, log Z over the candidates; a thread takes whole
-    //    tiles (ascending), skipping tiles without candidates
+    // 2. candidates of the tiles that kept any, compacted into LDS so that their
+    //    logits are fetched in one round
     Lse lc{-INFINITY, 0.f};
     Top2 best{-INFINITY, -1, -INFINITY};
     int count = 0;
-    const int *tc = P.tcount + (size_t)row * P.ntiles;
-    const uint32_t *bw = P.bits + (size_t)row * P.wstride;
-    const float2 *cz = P.cand + (size_t)row * P.V;
-    for (int tile = tid; tile < P.ntiles; tile += NT) {
-        if (tc[tile] == 0) continue;
-        for (int w = 0; w < kWordsPerTile; ++w) {
-            uint32_t b = bw[tile * kWordsPerTile + w];
-            while (b) {
-                const int t = (tile * kWordsPerTile + w) * 32 + __ffs(b) - 1;
-                b &= b - 1;
+    for (int base = 0; base < P.ntiles; base += kPass) {
+        if (base > 0) issue_cands(base);
+        mask_cands(base);
+        int nset = 0;
+#pragma unroll
+        for (int k = 0; k < kTilesPerLane; ++k) nset += popc8(w[k]);
+        int total;
+        const int first = wave_exclusive_scan(nset, lane, &total);
+        for (int lo = 0; lo < total; lo += kList) {
+            if (nset > 0 && first < lo + kList && first + nset > lo) {
+                int idx = first;
+#pragma unroll
+                for (int k = 0; k < kTilesPerLane; ++k)
+                    emit_ids(w[k], base + lane + k * kWaveSize, lo, &idx, list);
+            }
+            wave_lds_sync();
+            const int n = min(kList, total - lo);
+            for (int m = lane; m < n; m += kWaveSize) {
+                const int t = list[m];
                 const float2 c = cz[t];
                 if (!(c.x >= thr)) continue;
                 ++count;
@@ -130,20 +290,21 @@ __global__ __launch_bounds__(NT) void combine_kernel(Plan P, Inputs in, int32_t 
                 best = top2_merge(best, Top2{cd, t, -INFINITY});
                 lc = lse_merge(lc, Lse{cd, 1.f});
             }
+            wave_lds_sync();
         }
     }
-    lc = block_reduce(lc, sh_lse, lse_merge);
-    best = block_reduce(best, sh_top, top2_merge);
-    count = block_reduce(count, sh_cnt, [](int a, int b) { return a + b; });
+    lc = wave_lse(lc);
+    best = wave_top2(best);
+    count = wave_sum(count);
 
-    if (tid == 0) {
+    if (lane == 0) {
         const float logZ = lc.m + __logf(lc.s);
         float signal = NAN;
         if (best.id >= 0) {
             const float2 c = cz[best.id];
             signal = (c.x - lse_p) - (c.y - lse_q);
         }
-        float *ri = P.rowinfo + (size_t)row * kRowInfo;
+        float ri[kRowInfo] = {};
         ri[RI_MAXP] = max_p;
         ri[RI_LSEP] = lse_p;
         ri[RI_LSEQ] = lse_q;
@@ -154,68 +315,214 @@ __global__ __launch_bounds__(NT) void combine_kernel(Plan P, Inputs in, int32_t 
         ri[RI_SIGNAL] = signal;
         ri[RI_THRESH] = thr;
         ri[RI_ARGMAX] = __int_as_float(best.id);
+        float4 *dst = reinterpret_cast<float4 *>(P.rowinfo + (size_t)row * kRowInfo);
+#pragma unroll
+        for (int k = 0; k < kRowInfo / 4; ++k)
+            dst[k] = float4{ri[4 * k], ri[4 * k + 1], ri[4 * k + 2], ri[4 * k + 3]};
         if (row_argmax) row_argmax[row] = best.id;
         if (row_stats) {
 #pragma unroll
             for (int k = 0; k < 8; ++k) row_stats[(size_t)row * 8 + k] = ri[k];
         }
     }
+}
 
-    // 3. this row as a draft node: its token's logits under its parent row.  A
-    //    candidate reuses the tile's values (the same numbers the mask saw);
-    //    otherwise the token is outside the mask and, when node statistics are
-    //    wanted, its logits are recomputed here.
-    const int i = row % P.N;
-    if (i == 0) return;
-    const int j = in.parents[row], x = in.tokens[row];
-    if (j < 0 || j >= i || x < 0 || x >= P.V) return;  // the sequence is rejected later
-    const size_t rowj = (size_t)(row - i + j);
-    const int xt = x / kTileTokens;
-    const bool cand = P.tcount[rowj * P.ntiles + xt] > 0 &&
-                      (P.bits[rowj * P.wstride + (x >> 5)] >> (x & 31) & 1u);
-    float4 nz{0.f, 0.f, 0.f, 0.f};
-    if (cand) {
-        const float2 c = P.cand[rowj * P.V + x];
-        nz = float4{c.x, c.y, 1.f, 0.f};
-    } else if (want_node_logits) {
-        float zp = block_dot<DT>((const char *)in.hp + rowj * P.dp * esz,
-                                 (const char *)in.wp + (size_t)x * P.dp * esz, P.dp, sh_f);
-        float zq = block_dot<DT>((const char *)in.hq + rowj * P.dq * esz,
-                                 (const char *)in.wq + (size_t)x * P.dq * esz, P.dq, sh_f);
-        zp = (zp + (in.bp ? in.bp[x] : 0.f)) * P.inv_T;
-        zq = (zq + (in.bq ? in.bq[x] : 0.f)) * P.inv_T;
-        nz = float4{zp, zq, 0.f, 0.f};
+// ---------------------------------------------------------------------------
+// Sequence phase.
+
+// (max_p, lse_p, lse_q, log Z) and (threshold, argmax bits, -, -) of one row
+struct RowInfo {
+    float4 a, b;
+};
+
+__device__ __forceinline__ RowInfo load_rowinfo(const float *ri, size_t r) {
+    const float4 *p = reinterpret_cast<const float4 *>(ri + r * kRowInfo);
+    return RowInfo{p[0], p[2]};
+}
+
+// Statistics of a draft node under its parent row from the raw logits gathered
+// in the row phase: log pi_p, log pi_q, cd score, log pi_CD (-inf outside the mask).
+struct NodeStat {
+    float lpp, lpq, cd, lpcd;
+    bool in_mask;
+};
+
+__device__ __forceinline__ NodeStat node_stat(float4 nz, RowInfo rj, float s) {
+    NodeStat n;
+    n.in_mask = nz.z != 0.f && nz.x >= rj.b.x;
+    n.lpp = nz.x - rj.a.y;
+    n.lpq = nz.y - rj.a.z;
+    n.cd = (1.f + s) * n.lpp - s * n.lpq;
+    n.lpcd = n.in_mask ? n.cd - rj.a.w : -INFINITY;
+    return n;
+}
+
+__device__ __forceinline__ void write_node_stats(float *ns, const NodeStat &n, float ratio) {
+    ns[0] = n.lpp;
+    ns[1] = n.lpq;
+    ns[2] = n.cd;
+    ns[3] = n.lpcd;
+    ns[4] = n.in_mask ? 1.f : 0.f;
+    ns[5] = ratio;
+}
+
+// exclusive prefix sum over the whole group (fixed order); *total = the sum
+__device__ int group_exclusive_scan(int x, int tid, int *total, Smem &sm) {
+    const int lane = tid % kWaveSize, wave = tid / kWaveSize;
+    int wt;
+    const int in_wave = wave_exclusive_scan(x, lane, &wt);
+    if (lane == 0) sm.wave_tot[wave] = wt;
+    __syncthreads();
+    int before = 0, all = 0;
+#pragma unroll
+    for (int q = 0; q < NT / kWaveSize; ++q) {
+        before += q < wave ? sm.wave_tot[q] : 0;
+        all += sm.wave_tot[q];
     }
-    if (tid == 0) P.nodez[row] = nz;
+    __syncthreads();
+    *total = all;
+    return before + in_wave;
+}
+
+// Draws one token from the mask members of row jrow (the support of pi_CD): with
+// weights max(0, pi_CD - pi_e) when qrow is given (Alg. 1's residual), else
+// pi_CD itself (the bonus draw, or a residual that sums to zero); inverse CDF in
+// token-id order with uniform u: the smallest token whose cumulative weight
+// exceeds u times the total.  Called by the whole group; returns the token.
+__device__ int draw_token(const Plan &P, size_t jrow, const float *qrow, float u, int tid,
+                          Smem &sm) {
+    const float *rj = P.rowinfo + jrow * kRowInfo;
+    const float thr = rj[RI_THRESH], lse_p = rj[RI_LSEP], lse_q = rj[RI_LSEQ], logZ = rj[RI_LOGZ];
+    const int *tc = P.tcount + jrow * P.ntiles;
+    const uint4 *bw = reinterpret_cast<const uint4 *>(P.bits + jrow * P.wstride);
+    const float2 *cz = P.cand + jrow * P.V;
+    // each thread takes a contiguous range of tiles, so the gathered ids are in
+    // token order
+    const int t0 = (int)((long long)tid * P.ntiles / NT);
+    const int t1 = (int)((long long)(tid + 1) * P.ntiles / NT);
+    auto tile_words = [&](int t, uint4 (&w)[2]) {
+        const int c = tc[t];
+        w[0] = bw[2 * t];
+        w[1] = bw[2 * t + 1];
+        const uint32_t keep = c > 0 ? ~0u : 0u;  // words are stale without candidates
+        w[0] = mask4(w[0], keep);
+        w[1] = mask4(w[1], keep);
+    };
+    int mine = 0;
+    for (int t = t0; t < t1; ++t) {
+        uint4 w[2];
+        tile_words(t, w);
+        mine += popc8(w);
+    }
+    int L;
+    const int first = group_exclusive_scan(mine, tid, &L, sm);
+    auto weight = [&](int t, bool residual) -> double {
+        const float2 c = cz[t];
+        if (!(c.x >= thr)) return 0.0;
+        const float p = __expf((1.f + P.s) * (c.x - lse_p) - P.s * (c.y - lse_q) - logZ);
+        return residual ? (double)fmaxf(0.f, p - qrow[t]) : (double)p;
+    };
+    // ids of list positions [lo, lo + kList) into sm.list
+    auto fill = [&](int lo) {
+        if (mine > 0 && first < lo + kList && first + mine > lo) {
+            int idx = first;
+            for (int t = t0; t < t1; ++t) {
+                uint4 w[2];
+                tile_words(t, w);
+                emit_ids(w, t, lo, &idx, sm.list);
+            }
+        }
+        __syncthreads();
+    };
+    auto weigh = [&](int lo, bool residual) {
+        const int n = min(kList, L - lo);
+        for (int m = tid; m < n; m += NT) sm.wts[m] = weight(sm.list[m], residual);
+        __syncthreads();
+        return n;
+    };
+    const bool one_round = L <= kList;
+    // pass 1: the total, summed sequentially in token order by thread 0
+    auto total_of = [&](bool residual) {
+        double run = 0.0;
+        for (int lo = 0; lo < L; lo += kList) {
+            fill(lo);
+            const int n = weigh(lo, residual);
+            if (tid == 0)
+                for (int m = 0; m < n; ++m) run += sm.wts[m];
+            __syncthreads();
+        }
+        return run;
+    };
+    bool residual = qrow != nullptr;
+    double total = total_of(residual);
+    if (tid == 0) sm.ints[0] = residual && !(total > 0.0);
+    __syncthreads();
+    if (sm.ints[0]) {  // degenerate residual: fall back to pi_CD
+        __syncthreads();
+        residual = false;
+        total = total_of(false);
+    }
+    // pass 2: the first token whose cumulative weight exceeds u * total (the last
+    // token of positive weight if rounding leaves none); with one round the ids
+    // and weights of pass 1 are still in place
+    const double target = (double)u * total;
+    double run = 0.0;
+    int last = -1;
+    if (tid == 0) sm.ints[1] = -1;
+    __syncthreads();
+    for (int lo = 0; lo < L; lo += kList) {
+        int n = min(kList, L - lo);
+        if (!one_round) {
+            fill(lo);
+            n = weigh(lo, residual);
+        }
+        if (tid == 0) {
+            int found = -1;
+            for (int m = 0; m < n; ++m) {
+                const double wt = sm.wts[m];
+                run += wt;
+                if (wt > 0.0) {
+                    last = sm.list[m];
+                    if (run > target) {
+                        found = last;
+                        break;
+                    }
+                }
+            }
+            sm.ints[1] = found >= 0 ? found : (lo + kList >= L ? last : -1);
+        }
+        __syncthreads();
+        const int got = sm.ints[1];
+        __syncthreads();
+        if (got >= 0) return got;
+    }
+    return -1;  // empty support (a row without mask members)
 }
 
 template <int DT, bool SAMPLE>
-__global__ __launch_bounds__(NT) void sequence_kernel(Plan P, Inputs in, Outputs out,
-                                                      SampleInputs smp) {
-    __shared__ int sh_flag[4];
-    __shared__ int sh_int[2];
-    __shared__ double sh_sum[NT];
-    __shared__ double sh_prefix[NT + 1];
-    const int b = blockIdx.x, tid = threadIdx.x, N = P.N, V = P.V;
+__device__ void verify_sequence(const Plan &P, const Inputs &in, const Outputs &out,
+                                const SampleInputs &smp, int b, int tid, Smem &sm, int *dyn) {
+    const int N = P.N, V = P.V;
     const size_t r0 = (size_t)b * N;
-    const int32_t *par = in.parents + r0, *tok = in.tokens + r0;
-    const float *ri = P.rowinfo + r0 * kRowInfo;
+    int *s_par = dyn, *s_tok = dyn + N, *s_amax = dyn + 2 * N;
 
-    if (tid < 4) sh_flag[tid] = 0;
-    if (tid == 0) sh_int[0] = N;  // first rejected node (sampled)
+    if (tid < 4) sm.flag[tid] = 0;
+    if (tid == 0) sm.ints[2] = N;  // first rejected node (sampled)
     __syncthreads();
     for (int i = tid; i < N; i += NT) {
-        const int p = par[i];
-        if (i == 0 ? p != -1 : (p < 0 || p >= i)) atomicOr(&sh_flag[0], 1);
-        if (i > 0 && (tok[i] < 0 || tok[i] >= V)) atomicOr(&sh_flag[1], 1);
-        if (SAMPLE && i > 0 && p != i - 1) atomicOr(&sh_flag[2], 1);
-        const float *r = ri + (size_t)i * kRowInfo;
-        if (!isfinite(r[RI_MAXP]) || !isfinite(r[RI_LSEP]) || !isfinite(r[RI_LSEQ]) ||
-            !isfinite(r[RI_LOGZ]))
-            atomicOr(&sh_flag[3], 1);
+        const int p = in.parents[r0 + i], x = in.tokens[r0 + i];
+        const RowInfo r = load_rowinfo(P.rowinfo, r0 + i);
+        s_par[i] = p;
+        s_tok[i] = x;
+        s_amax[i] = __float_as_int(r.b.y);
+        if (i == 0 ? p != -1 : (p < 0 || p >= i)) atomicOr(&sm.flag[0], 1);
+        if (i > 0 && (x < 0 || x >= V)) atomicOr(&sm.flag[1], 1);
+        if (SAMPLE && i > 0 && p != i - 1) atomicOr(&sm.flag[2], 1);
+        if (!isfinite(r.a.x) || !isfinite(r.a.y) || !isfinite(r.a.z) || !isfinite(r.a.w))
+            atomicOr(&sm.flag[3], 1);
     }
     __syncthreads();
-    const int status = sh_flag[0] ? 1 : sh_flag[1] ? 2 : sh_flag[2] ? 4 : sh_flag[3] ? 3 : 0;
+    const int status = sm.flag[0] ? 1 : sm.flag[1] ? 2 : sm.flag[2] ? 4 : sm.flag[3] ? 3 : 0;
     if (status != 0) {
         for (int i = tid; i < N; i += NT) {
             out.accept_path[r0 + i] = -1;
@@ -230,185 +537,116 @@ __global__ __launch_bounds__(NT) void sequence_kernel(Plan P, Inputs in, Outputs
         return;
     }
 
-    // draft-token statistics under the parent row (logits gathered by the combine)
-    if (out.node_stats && tid < 6) out.node_stats[r0 * 6 + tid] = NAN;
-    for (int i = 1 + tid; i < N; i += NT) {
-        const int j = par[i], x = tok[i];
-        const float *rj = ri + (size_t)j * kRowInfo;
-        const float4 nz = P.nodez[r0 + i];
-        const bool in_mask = nz.z != 0.f && nz.x >= rj[RI_THRESH];
-        const float lpp = nz.x - rj[RI_LSEP], lpq = nz.y - rj[RI_LSEQ];
-        const float cd = (1.f + P.s) * lpp - P.s * lpq;
-        const float lpcd = in_mask ? cd - rj[RI_LOGZ] : -INFINITY;
-        float ratio = NAN;
-        if (SAMPLE) {
-            const float pe = smp.draft_probs[(r0 + i) * V + x];
-            ratio = pe > 0.f ? __expf(lpcd) / pe : INFINITY;
-            const bool accept = in_mask && smp.u_acc[r0 + i] <= ratio;
-            if (!accept) atomicMin(&sh_int[0], i);
-        }
-        if (out.node_stats) {
-            float *ns = out.node_stats + (r0 + i) * 6;
-            ns[0] = lpp;
-            ns[1] = lpq;
-            ns[2] = cd;
-            ns[3] = lpcd;
-            ns[4] = in_mask ? 1.f : 0.f;
-            ns[5] = ratio;
-        }
-    }
-    __syncthreads();
-
     if (!SAMPLE) {
-        // greedy walk: lowest-index child carrying the current row's argmax
+        if (tid >= kWaveSize) {
+            // node statistics (waves 1..)
+            if (!out.node_stats) return;
+            const int t1 = tid - kWaveSize;
+            if (t1 < 6) out.node_stats[r0 * 6 + t1] = NAN;
+            for (int i = 1 + t1; i < N; i += NT - kWaveSize)
+                write_node_stats(out.node_stats + (r0 + i) * 6,
+                                 node_stat(P.nodez[r0 + i], load_rowinfo(P.rowinfo, r0 + s_par[i]), P.s),
+                                 NAN);
+            return;
+        }
+        // greedy walk (wave 0): the lowest-index child carrying the current row's
+        // argmax; children have larger indices than their parent
+        const int lane = tid;
         int cur = 0, len = 0;
-        if (tid == 0) out.accept_path[r0] = 0;
         for (;;) {
-            const int target = __float_as_int(ri[(size_t)cur * kRowInfo + RI_ARGMAX]);
-            if (tid == 0) sh_int[1] = N;
-            __syncthreads();
-            for (int c = cur + 1 + tid; c < N; c += NT)
-                if (par[c] == cur && tok[c] == target) atomicMin(&sh_int[1], c);
-            __syncthreads();
-            const int chosen = sh_int[1];
-            __syncthreads();
+            const int target = s_amax[cur];
+            int chosen = N;
+            for (int c0 = cur + 1; c0 < N; c0 += kWaveSize) {
+                const int c = c0 + lane;
+                const unsigned long long hit =
+                    __ballot(c < N && s_par[c] == cur && s_tok[c] == target);
+                if (hit) {
+                    chosen = c0 + __builtin_ctzll(hit);
+                    break;
+                }
+            }
             if (chosen >= N) break;
             ++len;
             cur = chosen;
-            if (tid == 0) out.accept_path[r0 + len] = cur;
+            if (lane == 0) out.accept_path[r0 + len] = cur;
         }
-        // every path entry is written by exactly one thread
-        for (int i = len + 1 + tid; i < N; i += NT) out.accept_path[r0 + i] = -1;
-        if (tid == 0) {
+        // every path entry is written once
+        for (int i = len + 1 + lane; i < N; i += kWaveSize) out.accept_path[r0 + i] = -1;
+        if (lane == 0) {
+            out.accept_path[r0] = 0;
             out.status[b] = 0;
             out.accept_len[b] = len;
-            out.next_token[b] = __float_as_int(ri[(size_t)cur * kRowInfo + RI_ARGMAX]);
+            out.next_token[b] = s_amax[cur];
         }
         return;
     }
 
-    // sampled: accept nodes 1..k-1; draw from the residual at k or the bonus row
-    const int k = sh_int[0];
+    // sampled: node statistics and the first rejection
+    if (out.node_stats && tid < 6) out.node_stats[r0 * 6 + tid] = NAN;
+    for (int i = 1 + tid; i < N; i += NT) {
+        const int x = s_tok[i];
+        const NodeStat n = node_stat(P.nodez[r0 + i], load_rowinfo(P.rowinfo, r0 + s_par[i]), P.s);
+        const float pe = smp.draft_probs[(r0 + i) * V + x];
+        const float ratio = pe > 0.f ? __expf(n.lpcd) / pe : INFINITY;
+        const bool accept = n.in_mask && smp.u_acc[r0 + i] <= ratio;
+        if (!accept) atomicMin(&sm.ints[2], i);
+        if (out.node_stats) write_node_stats(out.node_stats + (r0 + i) * 6, n, ratio);
+    }
+    __syncthreads();
+    // accept nodes 1..k-1; draw from the residual at k or from the bonus row
+    const int k = sm.ints[2];
     const int jrow = k < N ? k - 1 : N - 1;
-    const float *rj = ri + (size_t)jrow * kRowInfo;
-    const float thr = rj[RI_THRESH], lse_p = rj[RI_LSEP], lse_q = rj[RI_LSEQ], logZ = rj[RI_LOGZ];
     const float *qrow = k < N ? smp.draft_probs + (r0 + k) * V : nullptr;
-    const uint32_t *bw = P.bits + (r0 + jrow) * P.wstride;
-    const float2 *cz = P.cand + (r0 + jrow) * V;
-    const int nwords = (V + 31) / 32;
-    const int w0 = (int)((long long)tid * nwords / NT), w1 = (int)((long long)(tid + 1) * nwords / NT);
-    // weight of token t under the chosen distribution (0 outside the mask)
-    auto weight = [&](int t, bool residual) -> double {
-        const float2 c = cz[t];
-        if (!(c.x >= thr)) return 0.0;
-        const float p = __expf((1.f + P.s) * (c.x - lse_p) - P.s * (c.y - lse_q) - logZ);
-        return residual ? (double)fmaxf(0.f, p - qrow[t]) : (double)p;
-    };
-    const int *tc = P.tcount + (r0 + jrow) * P.ntiles;
-    auto local_sum = [&](bool residual) {
-        double acc = 0.0;
-        for (int w = w0; w < w1; ++w) {
-            if (tc[w / kWordsPerTile] == 0) continue;
-            uint32_t bits = bw[w];
-            while (bits) {
-                const int t = w * 32 + __ffs(bits) - 1;
-                bits &= bits - 1;
-                acc += weight(t, residual);
-            }
-        }
-        return acc;
-    };
-    bool residual = qrow != nullptr;
-    double local = local_sum(residual);
-    sh_sum[tid] = local;
-    __syncthreads();
-    if (tid == 0) {  // sequential exclusive scan: the partial sums tile [0, total) exactly
-        double run = 0.0;
-        for (int i = 0; i < NT; ++i) {
-            sh_prefix[i] = run;
-            run += sh_sum[i];
-        }
-        sh_prefix[NT] = run;
-    }
-    __syncthreads();
-    if (residual && !(sh_prefix[NT] > 0.0)) {  // degenerate residual: fall back to pi_CD
-        __syncthreads();
-        residual = false;
-        local = local_sum(false);
-        sh_sum[tid] = local;
-        __syncthreads();
-        if (tid == 0) {
-            double run = 0.0;
-            for (int i = 0; i < NT; ++i) {
-                sh_prefix[i] = run;
-                run += sh_sum[i];
-            }
-            sh_prefix[NT] = run;
-        }
-        __syncthreads();
-    }
-    const double total = sh_prefix[NT];
-    const double target = (double)smp.u_res[r0 + jrow] * total;
-    if (tid == 0) sh_int[1] = -1;
-    __syncthreads();
-    const double prefix = sh_prefix[tid];
-    if (local > 0.0 && prefix <= target && target < prefix + local) {
-        double run = 0.0;
-        int found = -1, last = -1;
-        for (int w = w0; w < w1 && found < 0; ++w) {
-            if (tc[w / kWordsPerTile] == 0) continue;
-            uint32_t bits = bw[w];
-            while (bits) {
-                const int t = w * 32 + __ffs(bits) - 1;
-                bits &= bits - 1;
-                const double wt = weight(t, residual);
-                run += wt;
-                if (wt > 0.0) {
-                    last = t;
-                    if (prefix + run > target) {
-                        found = t;
-                        break;
-                    }
-                }
-            }
-        }
-        sh_int[1] = found >= 0 ? found : last;
-    }
-    __syncthreads();
+    const int next = draw_token(P, r0 + jrow, qrow, smp.u_res[r0 + jrow], tid, sm);
     for (int i = tid; i < N; i += NT) out.accept_path[r0 + i] = i < k ? i : -1;
     if (tid == 0) {
         out.status[b] = 0;
         out.accept_len[b] = k - 1;
-        out.next_token[b] = sh_int[1];
+        out.next_token[b] = next;
     }
+}
+
+// One workgroup per row; the workgroup that finishes a sequence's last row
+// (counted in seqdone, cleared before the LM-head launch) runs the sequence phase.
+template <int DT, bool SAMPLE>
+__global__ __launch_bounds__(NT) void finish_kernel(Plan P, Inputs in, Outputs out,
+                                                    SampleInputs smp) {
+    __shared__ Smem sm;
+    __shared__ int last;
+    extern __shared__ int dyn[];
+    const int row = blockIdx.x, tid = threadIdx.x;
+    combine_row<DT>(P, in, row, tid % kWaveSize, tid / kWaveSize, out.row_argmax, out.row_stats,
+                    out.node_stats != nullptr, sm.list);
+    // count the row once both of its waves are done; the release half of the
+    // atomic publishes wave 0's results, wave 1 released its own
+    __syncthreads();
+    const int b = row / P.N;
+    if (tid == 0)
+        last = __hip_atomic_fetch_add(&P.seqdone[b], 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT) ==
+               P.N - 1;
+    __syncthreads();
+    if (!last) return;
+    // acquire: the other rows of the sequence are visible from here on
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    verify_sequence<DT, SAMPLE>(P, in, out, smp, b, tid, sm, dyn);
 }
 
 }  // namespace
 
-hipError_t launch_combine(const Plan &p, const Inputs &in, const Outputs &out, hipStream_t st) {
-    const int want = out.node_stats != nullptr;
-    if (p.dtype == kBF16)
-        hipLaunchKernelGGL(combine_kernel<kBF16>, dim3(p.R), dim3(NT), 0, st, p, in, out.row_argmax,
-                           out.row_stats, want);
-    else
-        hipLaunchKernelGGL(combine_kernel<kF32>, dim3(p.R), dim3(NT), 0, st, p, in, out.row_argmax,
-                           out.row_stats, want);
-    return hipGetLastError();
-}
-
-hipError_t launch_sequences(const Plan &p, const Inputs &in, const Outputs &out,
-                            const SampleInputs *smp, hipStream_t st) {
+hipError_t launch_finish(const Plan &p, const Inputs &in, const Outputs &out,
+                         const SampleInputs *smp, hipStream_t st) {
     const SampleInputs s = smp ? *smp : SampleInputs{nullptr, nullptr, nullptr};
+    const size_t lds = (size_t)3 * p.N * sizeof(int);  // parents, tokens, argmax
     if (p.dtype == kBF16) {
         if (smp)
-            hipLaunchKernelGGL((sequence_kernel<kBF16, true>), dim3(p.B), dim3(NT), 0, st, p, in, out, s);
+            hipLaunchKernelGGL((finish_kernel<kBF16, true>), dim3(p.R), dim3(NT), lds, st, p, in, out, s);
         else
-            hipLaunchKernelGGL((sequence_kernel<kBF16, false>), dim3(p.B), dim3(NT), 0, st, p, in, out, s);
+            hipLaunchKernelGGL((finish_kernel<kBF16, false>), dim3(p.R), dim3(NT), lds, st, p, in, out, s);
     } else {
         if (smp)
-            hipLaunchKernelGGL((sequence_kernel<kF32, true>), dim3(p.B), dim3(NT), 0, st, p, in, out, s);
+            hipLaunchKernelGGL((finish_kernel<kF32, true>), dim3(p.R), dim3(NT), lds, st, p, in, out, s);
         else
-            hipLaunchKernelGGL((sequence_kernel<kF32, false>), dim3(p.B), dim3(NT), 0, st, p, in, out, s);
+            hipLaunchKernelGGL((finish_kernel<kF32, false>), dim3(p.R), dim3(NT), lds, st, p, in, out, s);
     }
     return hipGetLastError();
 }

@@ -94,6 +94,7 @@ def test_host_validation_errors():
     assert _call_greedy(_problem(nodes=8, vocab=1024, d_expert=256, d_amateur=128, plaus_thresh=2.0),
                         good_in, good_out, a, need) == dcd.DCD_ERR_PARAM
     assert _call_greedy(_problem(nodes=0), good_in, good_out, a, need) == dcd.DCD_ERR_SHAPE
+    assert _call_greedy(_problem(nodes=4097), good_in, good_out, a, need) == dcd.DCD_ERR_SHAPE
     assert _call_greedy(_problem(d_amateur=2044), good_in, good_out, a, need) == dcd.DCD_ERR_ALIGN
     # sampled mode validates temperature and its extra inputs
     L = dcd.lib()
