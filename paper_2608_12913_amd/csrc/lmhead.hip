@@ -322,7 +322,11 @@ constexpr int kHTiles = 2;  // hidden-state tiles in LDS
 constexpr size_t kEpilogueBytes = NW * ROWS * sizeof(float2) + ROWS * kWordsPerTile * sizeof(uint32_t) +
                                   ROWS * sizeof(int);
 static_assert(kEpilogueBytes <= (size_t)kHTiles * HTILE, "epilogue scratch must fit the hidden-state tiles");
-constexpr size_t kLdsBytes = kHTiles * HTILE + NW * WTILE + 2 * TS * sizeof(float);
+// expert logits of tile-local candidates, parked per lane until the amateur
+// epilogue decides which survive ([slot][lane] per wave)
+constexpr int kStash = 4;
+constexpr size_t kLdsBytes = kHTiles * HTILE + NW * WTILE + 2 * TS * sizeof(float) +
+                             NW * kStash * kWaveSize * sizeof(float);
 
 template <int DT, bool RAGGED>
 __device__ __forceinline__ void tile_body(const Plan &P, const Inputs &in, int tile, int row0,
@@ -338,6 +342,7 @@ __device__ __forceinline__ void tile_body(const Plan &P, const Inputs &in, int t
     char *wbuf = lds + kHTiles * HTILE + wave * WTILE;  // this wave's [16*VB][CB] weights
     float *bias_p = reinterpret_cast<float *>(lds + kHTiles * HTILE + NW * WTILE);  // [TS]
     float *bias_q = bias_p + TS;                                                     // [TS]
+    float *stash = bias_q + TS + wave * kStash * kWaveSize;                          // [kStash][64]
     // epilogue scratch, aliasing the hidden-state tiles (used only between passes)
     float2 *pairs = reinterpret_cast<float2 *>(lds);                       // [NW][64]
     uint32_t *twords = reinterpret_cast<uint32_t *>(pairs + NW * ROWS);   // [64][words]
@@ -367,8 +372,12 @@ __device__ __forceinline__ void tile_body(const Plan &P, const Inputs &in, int t
     sp.issue(0, b);
     run_pass<DT, RAGGED>(sp, &sq, b, hbuf, wbuf, a, acc);
     tile_softmax(acc, bias_p, P.V, tok0, wtok0, P.inv_T, pairs, z, pmax, psum);
-    // tile-local candidates: z_p within ln(theta) of the tile max; their expert
-    // logits are parked in the sparse candidate array
+    // tile-local candidates: z_p within ln(theta) of the tile max.  Their expert
+    // logits wait in the lane's LDS slots (the lane's k-th candidate in slot k;
+    // beyond kStash they go to the candidate array now): most are pruned at the
+    // end, and global stores issued here would delay the amateur stream's first
+    // loads behind them
+    int k = 0;
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
         const int row = row0 + rb * 16 + n;
@@ -381,7 +390,11 @@ __device__ __forceinline__ void tile_body(const Plan &P, const Inputs &in, int t
                 const int t = tok0 + 16 * vb + 4 * g + j;
                 if (t < P.V && z[vb][rb][j] >= thr && row < P.R) {
                     f |= 1u << (vb * 4 + j);
-                    P.cand[(size_t)row * P.V + t].x = z[vb][rb][j];
+                    if (k < kStash)
+                        stash[k * kWaveSize + lane] = z[vb][rb][j];
+                    else
+                        P.cand[(size_t)row * P.V + t].x = z[vb][rb][j];
+                    ++k;
                 }
             }
         flags[rb] = f;
@@ -403,11 +416,13 @@ __device__ __forceinline__ void tile_body(const Plan &P, const Inputs &in, int t
     for (int i = tid; i < ROWS * kWordsPerTile; i += NT) twords[i] = 0;
     if (tid < ROWS) tcnt[tid] = 0;
     tile_softmax(acc, bias_q, P.V, tok0, wtok0, P.inv_T, pairs, z, qmax, qsum);
+    k = 0;  // walks the lane's candidates in the order they were parked
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
         const int row = row0 + rb * 16 + n;
         // a tile whose expert max is below the row bound + ln(theta) holds no mask member
-        const uint32_t f = pmax[rb] >= bnd[rb] + P.log_theta ? flags[rb] : 0u;
+        const bool keep = pmax[rb] >= bnd[rb] + P.log_theta;
+        const uint32_t f = flags[rb];
         if (f == 0) continue;
 #pragma unroll
         for (int vb = 0; vb < VB; ++vb) {
@@ -416,8 +431,15 @@ __device__ __forceinline__ void tile_body(const Plan &P, const Inputs &in, int t
             for (int j = 0; j < 4; ++j)
                 if (f >> (vb * 4 + j) & 1u) {
                     const int t = tok0 + 16 * vb + 4 * g + j;
-                    P.cand[(size_t)row * P.V + t].y = z[vb][rb][j];
-                    bits |= 1u << (t % 32);
+                    if (keep) {
+                        float2 *c = &P.cand[(size_t)row * P.V + t];
+                        if (k < kStash)
+                            *c = float2{stash[k * kWaveSize + lane], z[vb][rb][j]};
+                        else
+                            c->y = z[vb][rb][j];
+                        bits |= 1u << (t % 32);
+                    }
+                    ++k;
                 }
             if (bits) {
                 const int word = (wtok0 + 16 * vb) / 32;
