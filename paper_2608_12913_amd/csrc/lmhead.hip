@@ -260,12 +260,15 @@ __device__ __forceinline__ float wave_sum16_32(float x) {
 // Logits of this lane's 16*VB (token, row) values and, per row, the tile's max and
 // sum of exp relative to it.  One LDS exchange of (wave max, wave sum) pairs,
 // merged in wave order.
-//   z[vb][rb][j]    logit (divided by T); -inf for tokens >= V
+//   bias_lds        the tile's bias already divided by T (0 without a bias)
+//   z[vb][rb][j]    logit (divided by T); -inf for tokens >= V (ragged tile only)
 //   tmax[rb], tsum[rb]   of row 16rb + lane%16
+template <bool RAGGED>
 __device__ __forceinline__ void tile_softmax(const f32x4 (&acc)[VB][RB], const float *bias_lds,
                                              int V, int tok0, int wtok0, float inv_T, float2 *pairs,
                                              float (&z)[VB][RB][4], float (&tmax)[RB],
                                              float (&tsum)[RB]) {
+    constexpr float kLog2e = 1.4426950408889634f;
     const int lane = threadIdx.x % kWaveSize, wave = threadIdx.x / kWaveSize;
     const int n = lane % 16, g = lane / 16;
 #pragma unroll
@@ -273,11 +276,12 @@ __device__ __forceinline__ void tile_softmax(const f32x4 (&acc)[VB][RB], const f
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             const int o = 16 * vb + 4 * g + j;  // token offset inside the wave
-            const bool ok = tok0 + o < V;
             const float b = bias_lds[wtok0 + o];
 #pragma unroll
-            for (int rb = 0; rb < RB; ++rb)
-                z[vb][rb][j] = ok ? (acc[vb][rb][j] + b) * inv_T : -INFINITY;
+            for (int rb = 0; rb < RB; ++rb) {
+                z[vb][rb][j] = fmaf(acc[vb][rb][j], inv_T, b);
+                if (RAGGED && tok0 + o >= V) z[vb][rb][j] = -INFINITY;
+            }
         }
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
@@ -287,11 +291,12 @@ __device__ __forceinline__ void tile_softmax(const f32x4 (&acc)[VB][RB], const f
 #pragma unroll
             for (int j = 0; j < 4; ++j) m = fmaxf(m, z[vb][rb][j]);
         m = wave_max16_32(m);
+        const float ml = m * kLog2e;
         float s = 0.f;
 #pragma unroll
         for (int vb = 0; vb < VB; ++vb)
 #pragma unroll
-            for (int j = 0; j < 4; ++j) s += __expf(z[vb][rb][j] - m);
+            for (int j = 0; j < 4; ++j) s += __builtin_amdgcn_exp2f(fmaf(z[vb][rb][j], kLog2e, -ml));
         if (m == -INFINITY) s = 0.f;  // nothing finite in this wave row
         s = wave_sum16_32(s);
         if (g == 0) pairs[wave * ROWS + rb * 16 + n] = float2{m, s};
@@ -322,9 +327,9 @@ constexpr int kHTiles = 2;  // hidden-state tiles in LDS
 constexpr size_t kEpilogueBytes = NW * ROWS * sizeof(float2) + ROWS * kWordsPerTile * sizeof(uint32_t) +
                                   ROWS * sizeof(int);
 static_assert(kEpilogueBytes <= (size_t)kHTiles * HTILE, "epilogue scratch must fit the hidden-state tiles");
-// expert logits of tile-local candidates, parked per lane until the amateur
-// epilogue decides which survive ([slot][lane] per wave)
-constexpr int kStash = 4;
+// expert logit of a lane's first tile-local candidate of each row block, parked
+// until the amateur epilogue decides whether the tile survives ([rb][lane] per wave)
+constexpr int kStash = RB;
 constexpr size_t kLdsBytes = kHTiles * HTILE + NW * WTILE + 2 * TS * sizeof(float) +
                              NW * kStash * kWaveSize * sizeof(float);
 
@@ -342,18 +347,18 @@ __device__ __forceinline__ void tile_body(const Plan &P, const Inputs &in, int t
     char *wbuf = lds + kHTiles * HTILE + wave * WTILE;  // this wave's [16*VB][CB] weights
     float *bias_p = reinterpret_cast<float *>(lds + kHTiles * HTILE + NW * WTILE);  // [TS]
     float *bias_q = bias_p + TS;                                                     // [TS]
-    float *stash = bias_q + TS + wave * kStash * kWaveSize;                          // [kStash][64]
+    float *stash = bias_q + TS + wave * kStash * kWaveSize;                          // [RB][64]
     // epilogue scratch, aliasing the hidden-state tiles (used only between passes)
     float2 *pairs = reinterpret_cast<float2 *>(lds);                       // [NW][64]
     uint32_t *twords = reinterpret_cast<uint32_t *>(pairs + NW * ROWS);   // [64][words]
     int *tcnt = reinterpret_cast<int *>(twords + ROWS * kWordsPerTile);    // [64]
 
-    // both models' bias for the tile (0 past the vocabulary or without a bias);
+    // both models' bias for the tile divided by T (0 past the vocabulary or without a bias);
     // ordered before their use by the pass barriers
     if (tid < TS) {
         const int t = tile * TS + tid;
-        bias_p[tid] = (t < P.V && in.bp) ? in.bp[t] : 0.f;
-        bias_q[tid] = (t < P.V && in.bq) ? in.bq[t] : 0.f;
+        bias_p[tid] = (t < P.V && in.bp) ? in.bp[t] * P.inv_T : 0.f;
+        bias_q[tid] = (t < P.V && in.bq) ? in.bq[t] * P.inv_T : 0.f;
     }
 
     Stream<RAGGED> sp, sq;
@@ -371,35 +376,49 @@ __device__ __forceinline__ void tile_body(const Plan &P, const Inputs &in, int t
     // ---- expert head (the amateur stream starts before its epilogue)
     sp.issue(0, b);
     run_pass<DT, RAGGED>(sp, &sq, b, hbuf, wbuf, a, acc);
-    tile_softmax(acc, bias_p, P.V, tok0, wtok0, P.inv_T, pairs, z, pmax, psum);
-    // tile-local candidates: z_p within ln(theta) of the tile max.  Their expert
-    // logits wait in the lane's LDS slots (the lane's k-th candidate in slot k;
-    // beyond kStash they go to the candidate array now): most are pruned at the
-    // end, and global stores issued here would delay the amateur stream's first
-    // loads behind them
-    int k = 0;
+    tile_softmax<RAGGED>(acc, bias_p, P.V, tok0, wtok0, P.inv_T, pairs, z, pmax, psum);
+    // tile-local candidates: z_p within ln(theta) of the tile max (bit vb*4+j of
+    // flags[rb]), found without branches.  The lane's first candidate of each row
+    // block waits in its LDS slot; most tiles are pruned at the end, and global
+    // stores issued here would delay the amateur stream's first loads behind
+    // them.  Further candidates of a row block (rare) are stored at once.
+    bool over = false;
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
         const int row = row0 + rb * 16 + n;
         const float thr = pmax[rb] + P.log_theta;
         uint32_t f = 0;
+        float first = 0.f;
 #pragma unroll
         for (int vb = 0; vb < VB; ++vb)
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 const int t = tok0 + 16 * vb + 4 * g + j;
-                if (t < P.V && z[vb][rb][j] >= thr && row < P.R) {
-                    f |= 1u << (vb * 4 + j);
-                    if (k < kStash)
-                        stash[k * kWaveSize + lane] = z[vb][rb][j];
-                    else
-                        P.cand[(size_t)row * P.V + t].x = z[vb][rb][j];
-                    ++k;
-                }
+                const bool c = (!RAGGED || t < P.V) && z[vb][rb][j] >= thr;
+                first = (c && f == 0) ? z[vb][rb][j] : first;
+                f |= c ? 1u << (vb * 4 + j) : 0u;
             }
+        f = row < P.R ? f : 0u;
         flags[rb] = f;
+        stash[rb * kWaveSize + lane] = first;
+        over |= (f & (f - 1)) != 0;
         // running lower bound on the row's expert max: one update per (row, tile)
         if (wave == 0 && g == 0 && row < P.R) atomicMax(&P.bound[row], ordered_key(pmax[rb]));
+    }
+    if (__builtin_amdgcn_ballot_w64(over)) {  // wave-uniform: some lane has more than one
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) {
+            const int row = row0 + rb * 16 + n;
+            uint32_t rest = flags[rb] & (flags[rb] - 1);  // all but the first
+            while (rest) {
+                const int bit = __builtin_ctz(rest);
+                rest &= rest - 1;
+                float v = z[0][rb][0];
+#pragma unroll
+                for (int i = 1; i < 4 * VB; ++i) v = bit == i ? z[i / 4][rb][i % 4] : v;
+                P.cand[(size_t)row * P.V + tok0 + 16 * (bit / 4) + 4 * g + bit % 4].x = v;
+            }
+        }
     }
 
     // ---- amateur head
@@ -415,32 +434,30 @@ __device__ __forceinline__ void tile_body(const Plan &P, const Inputs &in, int t
     }
     for (int i = tid; i < ROWS * kWordsPerTile; i += NT) twords[i] = 0;
     if (tid < ROWS) tcnt[tid] = 0;
-    tile_softmax(acc, bias_q, P.V, tok0, wtok0, P.inv_T, pairs, z, qmax, qsum);
-    k = 0;  // walks the lane's candidates in the order they were parked
+    tile_softmax<RAGGED>(acc, bias_q, P.V, tok0, wtok0, P.inv_T, pairs, z, qmax, qsum);
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
         const int row = row0 + rb * 16 + n;
         // a tile whose expert max is below the row bound + ln(theta) holds no mask member
-        const bool keep = pmax[rb] >= bnd[rb] + P.log_theta;
-        const uint32_t f = flags[rb];
-        if (f == 0) continue;
+        const uint32_t f = pmax[rb] >= bnd[rb] + P.log_theta ? flags[rb] : 0u;
+        if (!__builtin_amdgcn_ballot_w64(f != 0)) continue;  // wave-uniform skip
+        const uint32_t lowest = f & (0u - f);  // the candidate parked in LDS
 #pragma unroll
         for (int vb = 0; vb < VB; ++vb) {
             uint32_t bits = 0;
 #pragma unroll
-            for (int j = 0; j < 4; ++j)
-                if (f >> (vb * 4 + j) & 1u) {
+            for (int j = 0; j < 4; ++j) {
+                const uint32_t bit = 1u << (vb * 4 + j);
+                if (f & bit) {
                     const int t = tok0 + 16 * vb + 4 * g + j;
-                    if (keep) {
-                        float2 *c = &P.cand[(size_t)row * P.V + t];
-                        if (k < kStash)
-                            *c = float2{stash[k * kWaveSize + lane], z[vb][rb][j]};
-                        else
-                            c->y = z[vb][rb][j];
-                        bits |= 1u << (t % 32);
-                    }
-                    ++k;
+                    float2 *c = &P.cand[(size_t)row * P.V + t];
+                    if (bit == lowest)
+                        *c = float2{stash[rb * kWaveSize + lane], z[vb][rb][j]};
+                    else
+                        c->y = z[vb][rb][j];
+                    bits |= 1u << (t % 32);
                 }
+            }
             if (bits) {
                 const int word = (wtok0 + 16 * vb) / 32;
                 atomicOr(&twords[(rb * 16 + n) * kWordsPerTile + word], bits);
