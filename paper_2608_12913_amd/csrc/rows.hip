@@ -19,7 +19,9 @@ namespace dcd {
 namespace {
 
 constexpr int NT = 256;                  // threads of the finish kernel (4 waves)
-constexpr int kTilesPerLane = 8;         // vocabulary tiles a lane takes per pass
+constexpr int kTileU4 = kWordsPerTile / 4;  // 16-byte bitmap words per vocabulary tile
+constexpr int kTilesPerLane = kTileTokens <= 256 ? 8 : 4;  // tiles a lane takes per pass
+static_assert(kWordsPerTile % 4 == 0, "a tile's bitmap is whole 16-byte words");
 constexpr int kPass = kWaveSize * kTilesPerLane;
 constexpr int kList = 1024;              // candidate ids gathered per round
 
@@ -122,18 +124,21 @@ __device__ __forceinline__ uint4 mask4(uint4 v, uint32_t m) {
     return uint4{v.x & m, v.y & m, v.z & m, v.w & m};
 }
 
-__device__ __forceinline__ int popc8(const uint4 (&w)[2]) {
-    return __popc(w[0].x) + __popc(w[0].y) + __popc(w[0].z) + __popc(w[0].w) + __popc(w[1].x) +
-           __popc(w[1].y) + __popc(w[1].z) + __popc(w[1].w);
+__device__ __forceinline__ int popc_tile(const uint4 (&w)[kTileU4]) {
+    int c = 0;
+#pragma unroll
+    for (int q = 0; q < kTileU4; ++q) c += __popc(w[q].x) + __popc(w[q].y) + __popc(w[q].z) + __popc(w[q].w);
+    return c;
 }
 
-// Writes the ids of the set bits of one tile's 8 bitmap words whose running
-// index (*idx, advanced over every set bit) falls in [lo, lo + kList) to list[].
-__device__ __forceinline__ void emit_ids(const uint4 (&w)[2], int tile, int lo, int *idx, int *list) {
-    const uint32_t ws[8] = {w[0].x, w[0].y, w[0].z, w[0].w, w[1].x, w[1].y, w[1].z, w[1].w};
+// Writes the ids of the set bits of one tile's bitmap words whose running index
+// (*idx, advanced over every set bit) falls in [lo, lo + kList) to list[].
+__device__ __forceinline__ void emit_ids(const uint4 (&w)[kTileU4], int tile, int lo, int *idx,
+                                         int *list) {
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-        uint32_t b = ws[e];
+    for (int e = 0; e < kWordsPerTile; ++e) {
+        const uint4 q = w[e / 4];
+        uint32_t b = e % 4 == 0 ? q.x : e % 4 == 1 ? q.y : e % 4 == 2 ? q.z : q.w;
         while (b) {
             if (*idx >= lo && *idx < lo + kList)
                 list[*idx - lo] = (tile * kWordsPerTile + e) * 32 + __ffs(b) - 1;
@@ -200,7 +205,7 @@ __device__ void combine_row(const Plan &P, const Inputs &in, int row, int lane, 
 
     // the first pass's partials, counts and bitmap words are fetched together
     float4 v[kTilesPerLane];
-    uint4 w[kTilesPerLane][2];
+    uint4 w[kTilesPerLane][kTileU4];
     // Loads are issued unconditionally from clamped indices and masked
     // afterwards (with selects), so that all of them are in flight together.
     int c[kTilesPerLane];
@@ -213,8 +218,8 @@ __device__ void combine_row(const Plan &P, const Inputs &in, int row, int lane, 
         for (int k = 0; k < kTilesPerLane; ++k) {
             const int t = min(base + lane + k * kWaveSize, P.ntiles - 1);
             c[k] = tc[t];
-            w[k][0] = bw[2 * t];
-            w[k][1] = bw[2 * t + 1];
+#pragma unroll
+            for (int q = 0; q < kTileU4; ++q) w[k][q] = bw[kTileU4 * t + q];
         }
     };
     auto mask_partials = [&](int base) {
@@ -229,8 +234,8 @@ __device__ void combine_row(const Plan &P, const Inputs &in, int row, int lane, 
         for (int k = 0; k < kTilesPerLane; ++k) {
             // words of tiles without candidates are stale
             const uint32_t keep = (base + lane + k * kWaveSize < P.ntiles && c[k] > 0) ? ~0u : 0u;
-            w[k][0] = mask4(w[k][0], keep);
-            w[k][1] = mask4(w[k][1], keep);
+#pragma unroll
+            for (int q = 0; q < kTileU4; ++q) w[k][q] = mask4(w[k][q], keep);
         }
     };
     issue_partials(0);
@@ -269,7 +274,7 @@ __device__ void combine_row(const Plan &P, const Inputs &in, int row, int lane, 
         mask_cands(base);
         int nset = 0;
 #pragma unroll
-        for (int k = 0; k < kTilesPerLane; ++k) nset += popc8(w[k]);
+        for (int k = 0; k < kTilesPerLane; ++k) nset += popc_tile(w[k]);
         int total;
         const int first = wave_exclusive_scan(nset, lane, &total);
         for (int lo = 0; lo < total; lo += kList) {
@@ -400,19 +405,19 @@ __device__ int draw_token(const Plan &P, size_t jrow, const float *qrow, float u
     // token order
     const int t0 = (int)((long long)tid * P.ntiles / NT);
     const int t1 = (int)((long long)(tid + 1) * P.ntiles / NT);
-    auto tile_words = [&](int t, uint4 (&w)[2]) {
+    auto tile_words = [&](int t, uint4 (&w)[kTileU4]) {
         const int c = tc[t];
-        w[0] = bw[2 * t];
-        w[1] = bw[2 * t + 1];
+#pragma unroll
+        for (int q = 0; q < kTileU4; ++q) w[q] = bw[kTileU4 * t + q];
         const uint32_t keep = c > 0 ? ~0u : 0u;  // words are stale without candidates
-        w[0] = mask4(w[0], keep);
-        w[1] = mask4(w[1], keep);
+#pragma unroll
+        for (int q = 0; q < kTileU4; ++q) w[q] = mask4(w[q], keep);
     };
     int mine = 0;
     for (int t = t0; t < t1; ++t) {
-        uint4 w[2];
+        uint4 w[kTileU4];
         tile_words(t, w);
-        mine += popc8(w);
+        mine += popc_tile(w);
     }
     int L;
     const int first = group_exclusive_scan(mine, tid, &L, sm);
@@ -427,7 +432,7 @@ __device__ int draw_token(const Plan &P, size_t jrow, const float *qrow, float u
         if (mine > 0 && first < lo + kList && first + mine > lo) {
             int idx = first;
             for (int t = t0; t < t1; ++t) {
-                uint4 w[2];
+                uint4 w[kTileU4];
                 tile_words(t, w);
                 emit_ids(w, t, lo, &idx, sm.list);
             }
