@@ -17,7 +17,9 @@
  *
  * Notation: s = cd_strength (the paper's contrastive strength), theta =
  * plaus_thresh (the paper's plausibility cutoff).  theta = 0 means no mask (the
- * untruncated target the paper's experiments use).
+ * untruncated target the paper's experiments use): every token is in the
+ * support and the target's statistics come from both models' full logits, which
+ * the LM-head step then keeps in the workspace instead of candidate lists.
  *
  * Conventions shared by every entry point
  *  - Rows: a problem holds B sequences of N nodes each; row r = b*N + i is node i
@@ -135,8 +137,11 @@ typedef struct {                 /* device pointers, written by the call        
 /*
  * Bytes of device workspace a call with problem `p` needs (0 if `p` is invalid).
  * The workspace holds per-tile softmax partials, the candidate logits that may
- * fall inside the plausibility mask, and per-row results; it is
- * O(B*N*V) bytes (8.1 bytes per row and vocabulary entry).
+ * fall inside the plausibility mask (theta > 0) or both models' dense logits
+ * (theta = 0, where every token is in the support), and per-row results; it is
+ * O(B*N*V) bytes (about 8.1 bytes per row and vocabulary entry).  The size depends
+ * on the problem, so a workspace sized for one problem may be too small for
+ * another.
  */
 size_t dcd_workspace_bytes(const dcd_problem *p);
 

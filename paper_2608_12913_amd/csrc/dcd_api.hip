@@ -45,6 +45,9 @@ int make_plan(const dcd_problem *p, bool sample, Plan &P) {
     P.wstride = P.ntiles * kWordsPerTile;
     // ln(theta) in double, rounded once; theta = 0 switches the mask off
     P.log_theta = p->plaus_thresh > 0.f ? (float)log((double)p->plaus_thresh) : -INFINITY;
+    P.full = p->plaus_thresh == 0.f;
+    P.store_q = P.full && sample;
+    P.zstride = P.ntiles * kTileTokens;
     P.s = p->cd_strength;
     P.inv_T = sample ? (float)(1.0 / (double)p->temperature) : 1.f;
     const long long groups = (long long)((P.ntiles + 7) / 8) * 8 * P.nrb;
@@ -125,8 +128,14 @@ size_t workspace_layout(Plan &p, char *base) {
     };
     const size_t R = (size_t)p.R;
     p.partials = (float4 *)take(R * p.ntiles * sizeof(float4));
-    p.cand = (float2 *)take(R * (size_t)p.V * sizeof(float2));
-    p.bits = (uint32_t *)take(R * (size_t)p.wstride * sizeof(uint32_t));
+    if (p.full) {  // dense logits of both models, per-tile statistics of y
+        p.zp_full = (float *)take(R * (size_t)p.zstride * sizeof(float));
+        p.zq_full = (float *)take(R * (size_t)p.zstride * sizeof(float));
+        p.ypart = (float4 *)take(R * p.ntiles * 2 * sizeof(float4));
+    } else {  // candidates of the mask
+        p.cand = (float2 *)take(R * (size_t)p.V * sizeof(float2));
+        p.bits = (uint32_t *)take(R * (size_t)p.wstride * sizeof(uint32_t));
+    }
     p.rowinfo = (float *)take(R * kRowInfo * sizeof(float));
     p.tcount = (int *)take(R * p.ntiles * sizeof(int));
     p.bound = (int *)take(R * sizeof(int));

@@ -41,10 +41,21 @@ struct Plan {
     float log_theta;   // ln(plaus_thresh); -inf when the mask is off
     float s;           // cd_strength
     float inv_T;       // 1 / temperature (1 for greedy)
+    int full;          // plaus_thresh = 0: the untruncated target (every token in the support);
+                       // no candidates, dense logits instead
+    int zstride;       // ntiles * kTileTokens: row stride of the dense logit arrays
+    int store_q;       // full and sampled: the amateur logits are kept for the draw
     // workspace carve-up
     float4 *partials;  // [R][ntiles]   (max_p, sumexp_p, max_q, sumexp_q) per vocabulary tile
+    // masked target (full = 0)
     float2 *cand;      // [R][V]        (z_p, z_q) of candidate tokens (sparse)
     uint32_t *bits;    // [R][wstride]  candidate bitmap
+    // untruncated target (full = 1)
+    float *zp_full;    // [R][zstride]  expert logits (divided by T)
+    float *zq_full;    // [R][zstride]  amateur logits (divided by T)
+    float4 *ypart;     // [R][ntiles][2] per tile, over y = (1+s) z_p - s z_q:
+                       //   (max y, sum exp(y - max y), second-best y, sum exp(z_p - max_p)(z_p - z_q))
+                       //   (argmax bits, z_p and z_q at the argmax, -)
     float *rowinfo;    // [R][kRowInfo]
     int *tcount;       // [R][ntiles]   candidates per (row, tile); bitmap words valid where > 0
     int *bound;        // [R]           running lower bound on max z_p (order-preserving int key)
@@ -74,6 +85,30 @@ __device__ __forceinline__ int ordered_key(float f) {
 }
 __device__ __forceinline__ float key_value(int k) {
     return __int_as_float(k >= 0 ? k : k ^ 0x7fffffff);
+}
+
+// Untruncated target: statistics of y = (1+s) z_p - s z_q over a set of tokens.
+// cd = y - (1+s) lse_p + s lse_q, so the argmax, margin and log-normaliser of the
+// cd score follow from these and the two models' normalisers.
+struct YStat {
+    float y1;   // best y (-inf when empty)
+    int i1;     // its token (lowest id on ties; -1 when empty)
+    float y2;   // second-best y
+    float ys;   // sum of exp(y - y1)
+    float zp1, zq1;  // z_p, z_q at i1
+    float a;    // sum of exp(z_p - tile max_p) * (z_p - z_q)
+};
+
+__device__ __forceinline__ YStat ystat_merge(const YStat &u, const YStat &v) {
+    const bool u_wins = v.i1 < 0 || (u.i1 >= 0 && (u.y1 > v.y1 || (u.y1 == v.y1 && u.i1 < v.i1)));
+    const YStat &w = u_wins ? u : v, &l = u_wins ? v : u;
+    YStat r = w;
+    if (l.i1 >= 0) {
+        r.y2 = fmaxf(w.y2, l.y1);
+        r.ys = w.ys + l.ys * __builtin_amdgcn_exp2f((l.y1 - w.y1) * 1.4426950408889634f);
+    }
+    r.a = u.a + v.a;
+    return r;
 }
 
 size_t workspace_layout(Plan &p, char *base);  // fills the pointers when base != nullptr

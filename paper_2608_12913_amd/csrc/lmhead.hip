@@ -321,19 +321,25 @@ __device__ __forceinline__ void tile_softmax(const f32x4 (&acc)[VB][RB], const f
     __syncthreads();  // the pairs are reused
 }
 
+__device__ __forceinline__ YStat ystat_shfl_xor(const YStat &x, int m) {
+    return YStat{__shfl_xor(x.y1, m), __shfl_xor(x.i1, m), __shfl_xor(x.y2, m), __shfl_xor(x.ys, m),
+                 __shfl_xor(x.zp1, m), __shfl_xor(x.zq1, m), __shfl_xor(x.a, m)};
+}
+
 constexpr int kHTiles = 2;  // hidden-state tiles in LDS
 // epilogue scratch (row reductions, candidate words and counts) reuses the
 // hidden-state tiles, which are idle between passes
 constexpr size_t kEpilogueBytes = NW * ROWS * sizeof(float2) + ROWS * kWordsPerTile * sizeof(uint32_t) +
                                   ROWS * sizeof(int);
 static_assert(kEpilogueBytes <= (size_t)kHTiles * HTILE, "epilogue scratch must fit the hidden-state tiles");
+static_assert(NW * ROWS * sizeof(YStat) <= (size_t)kHTiles * HTILE, "y statistics must fit the hidden-state tiles");
 // expert logit of a lane's first tile-local candidate of each row block, parked
 // until the amateur epilogue decides whether the tile survives ([rb][lane] per wave)
 constexpr int kStash = RB;
 constexpr size_t kLdsBytes = kHTiles * HTILE + NW * WTILE + 2 * TS * sizeof(float) +
                              NW * kStash * kWaveSize * sizeof(float);
 
-template <int DT, bool RAGGED>
+template <int DT, bool RAGGED, bool FULL>
 __device__ __forceinline__ void tile_body(const Plan &P, const Inputs &in, int tile, int row0,
                                           char *lds) {
     constexpr int ESZ = DT == kBF16 ? 2 : 4;
@@ -377,114 +383,218 @@ __device__ __forceinline__ void tile_body(const Plan &P, const Inputs &in, int t
     sp.issue(0, b);
     run_pass<DT, RAGGED>(sp, &sq, b, hbuf, wbuf, a, acc);
     tile_softmax<RAGGED>(acc, bias_p, P.V, tok0, wtok0, P.inv_T, pairs, z, pmax, psum);
-    // tile-local candidates: z_p within ln(theta) of the tile max (bit vb*4+j of
-    // flags[rb]), found without branches.  The lane's first candidate of each row
-    // block waits in its LDS slot; most tiles are pruned at the end, and global
-    // stores issued here would delay the amateur stream's first loads behind
-    // them.  Further candidates of a row block (rare) are stored at once.
-    bool over = false;
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb) {
-        const int row = row0 + rb * 16 + n;
-        const float thr = pmax[rb] + P.log_theta;
-        uint32_t f = 0;
-        float first = 0.f;
-#pragma unroll
-        for (int vb = 0; vb < VB; ++vb)
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const int t = tok0 + 16 * vb + 4 * g + j;
-                const bool c = (!RAGGED || t < P.V) && z[vb][rb][j] >= thr;
-                first = (c && f == 0) ? z[vb][rb][j] : first;
-                f |= c ? 1u << (vb * 4 + j) : 0u;
-            }
-        f = row < P.R ? f : 0u;
-        flags[rb] = f;
-        stash[rb * kWaveSize + lane] = first;
-        over |= (f & (f - 1)) != 0;
-        // running lower bound on the row's expert max: one update per (row, tile)
-        if (wave == 0 && g == 0 && row < P.R) atomicMax(&P.bound[row], ordered_key(pmax[rb]));
-    }
-    if (__builtin_amdgcn_ballot_w64(over)) {  // wave-uniform: some lane has more than one
+    if constexpr (FULL) {
+        // untruncated target: the expert logits go to the dense array for the
+        // amateur epilogue (16 contiguous bytes per lane and block)
 #pragma unroll
         for (int rb = 0; rb < RB; ++rb) {
             const int row = row0 + rb * 16 + n;
-            uint32_t rest = flags[rb] & (flags[rb] - 1);  // all but the first
-            while (rest) {
-                const int bit = __builtin_ctz(rest);
-                rest &= rest - 1;
-                float v = z[0][rb][0];
+            if (row >= P.R) continue;
 #pragma unroll
-                for (int i = 1; i < 4 * VB; ++i) v = bit == i ? z[i / 4][rb][i % 4] : v;
-                P.cand[(size_t)row * P.V + tok0 + 16 * (bit / 4) + 4 * g + bit % 4].x = v;
+            for (int vb = 0; vb < VB; ++vb)
+                *reinterpret_cast<float4 *>(P.zp_full + (size_t)row * P.zstride + tok0 + 16 * vb + 4 * g) =
+                    float4{z[vb][rb][0], z[vb][rb][1], z[vb][rb][2], z[vb][rb][3]};
+        }
+    } else {
+        // tile-local candidates: z_p within ln(theta) of the tile max (bit vb*4+j of
+        // flags[rb]), found without branches.  The lane's first candidate of each row
+        // block waits in its LDS slot; most tiles are pruned at the end, and global
+        // stores issued here would delay the amateur stream's first loads behind
+        // them.  Further candidates of a row block (rare) are stored at once.
+        bool over = false;
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) {
+            const int row = row0 + rb * 16 + n;
+            const float thr = pmax[rb] + P.log_theta;
+            uint32_t f = 0;
+            float first = 0.f;
+#pragma unroll
+            for (int vb = 0; vb < VB; ++vb)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const int t = tok0 + 16 * vb + 4 * g + j;
+                    const bool c = (!RAGGED || t < P.V) && z[vb][rb][j] >= thr;
+                    first = (c && f == 0) ? z[vb][rb][j] : first;
+                    f |= c ? 1u << (vb * 4 + j) : 0u;
+                }
+            f = row < P.R ? f : 0u;
+            flags[rb] = f;
+            stash[rb * kWaveSize + lane] = first;
+            over |= (f & (f - 1)) != 0;
+            // running lower bound on the row's expert max: one update per (row, tile)
+            if (wave == 0 && g == 0 && row < P.R) atomicMax(&P.bound[row], ordered_key(pmax[rb]));
+        }
+        if (__builtin_amdgcn_ballot_w64(over)) {  // wave-uniform: some lane has more than one
+#pragma unroll
+            for (int rb = 0; rb < RB; ++rb) {
+                const int row = row0 + rb * 16 + n;
+                uint32_t rest = flags[rb] & (flags[rb] - 1);  // all but the first
+                while (rest) {
+                    const int bit = __builtin_ctz(rest);
+                    rest &= rest - 1;
+                    float v = z[0][rb][0];
+#pragma unroll
+                    for (int i = 1; i < 4 * VB; ++i) v = bit == i ? z[i / 4][rb][i % 4] : v;
+                    P.cand[(size_t)row * P.V + tok0 + 16 * (bit / 4) + 4 * g + bit % 4].x = v;
+                }
             }
         }
     }
 
     // ---- amateur head
     run_pass<DT, RAGGED>(sq, nullptr, b, hbuf, wbuf, a, acc);
-    // the running bound of the lane's rows (read before the softmax, so the load
-    // latency overlaps it); the hidden-state tiles are idle: clear the candidate
-    // words and counts (ordered before their use by the barriers in tile_softmax)
-    float bnd[RB];
+    if constexpr (FULL) {
+        tile_softmax<RAGGED>(acc, bias_q, P.V, tok0, wtok0, P.inv_T, pairs, z, qmax, qsum);
+        // the lane's expert logits back from the dense array
+        float zp[VB][RB][4];
 #pragma unroll
-    for (int rb = 0; rb < RB; ++rb) {
-        const int row = min(row0 + rb * 16 + n, P.R - 1);
-        bnd[rb] = flags[rb] ? key_value(__atomic_load_n(&P.bound[row], __ATOMIC_RELAXED)) : 0.f;
-    }
-    for (int i = tid; i < ROWS * kWordsPerTile; i += NT) twords[i] = 0;
-    if (tid < ROWS) tcnt[tid] = 0;
-    tile_softmax<RAGGED>(acc, bias_q, P.V, tok0, wtok0, P.inv_T, pairs, z, qmax, qsum);
+        for (int rb = 0; rb < RB; ++rb) {
+            const int row = min(row0 + rb * 16 + n, P.R - 1);
 #pragma unroll
-    for (int rb = 0; rb < RB; ++rb) {
-        const int row = row0 + rb * 16 + n;
-        // a tile whose expert max is below the row bound + ln(theta) holds no mask member
-        const uint32_t f = pmax[rb] >= bnd[rb] + P.log_theta ? flags[rb] : 0u;
-        if (!__builtin_amdgcn_ballot_w64(f != 0)) continue;  // wave-uniform skip
-        const uint32_t lowest = f & (0u - f);  // the candidate parked in LDS
+            for (int vb = 0; vb < VB; ++vb) {
+                const float4 v = *reinterpret_cast<const float4 *>(
+                    P.zp_full + (size_t)row * P.zstride + tok0 + 16 * vb + 4 * g);
+                zp[vb][rb][0] = v.x;
+                zp[vb][rb][1] = v.y;
+                zp[vb][rb][2] = v.z;
+                zp[vb][rb][3] = v.w;
+            }
+        }
+        if (P.store_q) {  // sampled verification draws from the whole vocabulary later
 #pragma unroll
-        for (int vb = 0; vb < VB; ++vb) {
-            uint32_t bits = 0;
+            for (int rb = 0; rb < RB; ++rb) {
+                const int row = row0 + rb * 16 + n;
+                if (row >= P.R) continue;
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const uint32_t bit = 1u << (vb * 4 + j);
-                if (f & bit) {
+                for (int vb = 0; vb < VB; ++vb)
+                    *reinterpret_cast<float4 *>(P.zq_full + (size_t)row * P.zstride + tok0 + 16 * vb + 4 * g) =
+                        float4{z[vb][rb][0], z[vb][rb][1], z[vb][rb][2], z[vb][rb][3]};
+            }
+        }
+        // per row: statistics of y over the lane's tokens (ascending, so a strict
+        // comparison keeps the lowest id on ties), merged over the wave's lanes of
+        // that row and then over the waves in order
+        constexpr float kLog2e = 1.4426950408889634f;
+        const float s1 = 1.f + P.s;
+        YStat *ys_lds = reinterpret_cast<YStat *>(lds);  // [NW][64], over the idle hidden-state tiles
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) {
+            YStat st{-INFINITY, -1, -INFINITY, 0.f, 0.f, 0.f, 0.f};
+            float y[VB][4];
+#pragma unroll
+            for (int vb = 0; vb < VB; ++vb)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
                     const int t = tok0 + 16 * vb + 4 * g + j;
-                    float2 *c = &P.cand[(size_t)row * P.V + t];
-                    if (bit == lowest)
-                        *c = float2{stash[rb * kWaveSize + lane], z[vb][rb][j]};
-                    else
-                        c->y = z[vb][rb][j];
-                    bits |= 1u << (t % 32);
+                    const bool ok = !RAGGED || t < P.V;
+                    const float p = zp[vb][rb][j], q = z[vb][rb][j];
+                    y[vb][j] = ok ? s1 * p - P.s * q : -INFINITY;
+                    st.a += ok ? __builtin_amdgcn_exp2f((p - pmax[rb]) * kLog2e) * (p - q) : 0.f;
+                    if (ok && y[vb][j] > st.y1) {
+                        st.y2 = st.y1;
+                        st.y1 = y[vb][j];
+                        st.i1 = t;
+                        st.zp1 = p;
+                        st.zq1 = q;
+                    } else if (ok) {
+                        st.y2 = fmaxf(st.y2, y[vb][j]);
+                    }
+                }
+            if (st.i1 >= 0) {
+                const float ml = st.y1 * kLog2e;
+#pragma unroll
+                for (int vb = 0; vb < VB; ++vb)
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) st.ys += __builtin_amdgcn_exp2f(fmaf(y[vb][j], kLog2e, -ml));
+            }
+            st = ystat_merge(st, ystat_shfl_xor(st, 16));
+            st = ystat_merge(st, ystat_shfl_xor(st, 32));
+            if (g == 0) ys_lds[wave * ROWS + rb * 16 + n] = st;
+        }
+        __syncthreads();
+        if (wave == 0 && g == 0) {
+#pragma unroll
+            for (int rb = 0; rb < RB; ++rb) {
+                const int row = row0 + rb * 16 + n;
+                YStat st = ys_lds[rb * 16 + n];
+#pragma unroll
+                for (int w = 1; w < NW; ++w) st = ystat_merge(st, ys_lds[w * ROWS + rb * 16 + n]);
+                if (row >= P.R) continue;
+                float4 *dst = P.ypart + ((size_t)row * P.ntiles + tile) * 2;
+                dst[0] = float4{st.y1, st.ys, st.y2, st.a};
+                dst[1] = float4{__int_as_float(st.i1), st.zp1, st.zq1, 0.f};
+            }
+        }
+    } else {
+        // the running bound of the lane's rows (read before the softmax, so the load
+        // latency overlaps it); the hidden-state tiles are idle: clear the candidate
+        // words and counts (ordered before their use by the barriers in tile_softmax)
+        float bnd[RB];
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) {
+            const int row = min(row0 + rb * 16 + n, P.R - 1);
+            bnd[rb] = flags[rb] ? key_value(__atomic_load_n(&P.bound[row], __ATOMIC_RELAXED)) : 0.f;
+        }
+        for (int i = tid; i < ROWS * kWordsPerTile; i += NT) twords[i] = 0;
+        if (tid < ROWS) tcnt[tid] = 0;
+        tile_softmax<RAGGED>(acc, bias_q, P.V, tok0, wtok0, P.inv_T, pairs, z, qmax, qsum);
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) {
+            const int row = row0 + rb * 16 + n;
+            // a tile whose expert max is below the row bound + ln(theta) holds no mask member
+            const uint32_t f = pmax[rb] >= bnd[rb] + P.log_theta ? flags[rb] : 0u;
+            if (!__builtin_amdgcn_ballot_w64(f != 0)) continue;  // wave-uniform skip
+            const uint32_t lowest = f & (0u - f);  // the candidate parked in LDS
+#pragma unroll
+            for (int vb = 0; vb < VB; ++vb) {
+                uint32_t bits = 0;
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const uint32_t bit = 1u << (vb * 4 + j);
+                    if (f & bit) {
+                        const int t = tok0 + 16 * vb + 4 * g + j;
+                        float2 *c = &P.cand[(size_t)row * P.V + t];
+                        if (bit == lowest)
+                            *c = float2{stash[rb * kWaveSize + lane], z[vb][rb][j]};
+                        else
+                            c->y = z[vb][rb][j];
+                        bits |= 1u << (t % 32);
+                    }
+                }
+                if (bits) {
+                    const int word = (wtok0 + 16 * vb) / 32;
+                    atomicOr(&twords[(rb * 16 + n) * kWordsPerTile + word], bits);
+                    atomicAdd(&tcnt[rb * 16 + n], __popc(bits));
                 }
             }
-            if (bits) {
-                const int word = (wtok0 + 16 * vb) / 32;
-                atomicOr(&twords[(rb * 16 + n) * kWordsPerTile + word], bits);
-                atomicAdd(&tcnt[rb * 16 + n], __popc(bits));
+        }
+        __syncthreads();
+        // per (row, tile): the candidate count and the bitmap words where it is nonzero
+        for (int i = tid; i < ROWS * kWordsPerTile; i += NT) {
+            const int r = i / kWordsPerTile, row = row0 + r;
+            if (row < P.R && tcnt[r] > 0)
+                P.bits[(size_t)row * P.wstride + tile * kWordsPerTile + i % kWordsPerTile] = twords[i];
+        }
+        if (wave == 0 && g == 0) {
+#pragma unroll
+            for (int rb = 0; rb < RB; ++rb) {
+                const int row = row0 + rb * 16 + n;
+                if (row < P.R) P.tcount[(size_t)row * P.ntiles + tile] = tcnt[rb * 16 + n];
             }
         }
     }
-    __syncthreads();
-    // per (row, tile): the candidate count, the bitmap words where it is nonzero,
-    // and the softmax partials of both models
-    for (int i = tid; i < ROWS * kWordsPerTile; i += NT) {
-        const int r = i / kWordsPerTile, row = row0 + r;
-        if (row < P.R && tcnt[r] > 0)
-            P.bits[(size_t)row * P.wstride + tile * kWordsPerTile + i % kWordsPerTile] = twords[i];
-    }
+    // per (row, tile): the softmax partials of both models
     if (wave == 0 && g == 0) {
 #pragma unroll
         for (int rb = 0; rb < RB; ++rb) {
             const int row = row0 + rb * 16 + n;
             if (row >= P.R) continue;
             P.partials[(size_t)row * P.ntiles + tile] = float4{pmax[rb], psum[rb], qmax[rb], qsum[rb]};
-            P.tcount[(size_t)row * P.ntiles + tile] = tcnt[rb * 16 + n];
         }
     }
 }
 
-template <int DT>
+template <int DT, bool FULL>
 __global__ __launch_bounds__(NT, DCD_LMHEAD_MIN_BLOCKS) void lmhead_kernel(Plan P, Inputs in) {
     extern __shared__ __align__(16) char lds[];
     // workgroup -> (vocabulary tile, row block); the row blocks of one tile are
@@ -496,9 +606,9 @@ __global__ __launch_bounds__(NT, DCD_LMHEAD_MIN_BLOCKS) void lmhead_kernel(Plan 
     if (tile >= P.ntiles) return;
     const int row0 = rblk * ROWS;
     if ((tile + 1) * TS > P.V)  // workgroup-uniform: only the last tile is ragged
-        tile_body<DT, true>(P, in, tile, row0, lds);
+        tile_body<DT, true, FULL>(P, in, tile, row0, lds);
     else
-        tile_body<DT, false>(P, in, tile, row0, lds);
+        tile_body<DT, false, FULL>(P, in, tile, row0, lds);
 }
 
 // Row bounds start at -inf and the per-sequence row counters of the finishing
@@ -514,22 +624,32 @@ __global__ void init_kernel(int *bound, int R, int *seqdone, int B) {
 hipError_t launch_lmhead(const Plan &p, const Inputs &in, hipStream_t st) {
     // the tile may need more than 64 KB of LDS (gfx950 has 160 KB per CU)
     static const hipError_t attr = [] {
-        hipError_t e = hipFuncSetAttribute((const void *)lmhead_kernel<kBF16>,
-                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsBytes);
-        if (e == hipSuccess)
-            e = hipFuncSetAttribute((const void *)lmhead_kernel<kF32>,
-                                    hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsBytes);
-        return e;
+        const void *k[4] = {(const void *)lmhead_kernel<kBF16, false>, (const void *)lmhead_kernel<kBF16, true>,
+                            (const void *)lmhead_kernel<kF32, false>, (const void *)lmhead_kernel<kF32, true>};
+        for (const void *f : k) {
+            const hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsBytes);
+            if (e != hipSuccess) return e;
+        }
+        return hipSuccess;
     }();
     if (attr != hipSuccess) return attr;
     const int groups = ((p.ntiles + 7) / 8) * 8 * p.nrb;
     const int ninit = p.R > p.B ? p.R : p.B;
     hipLaunchKernelGGL(init_kernel, dim3((ninit + 255) / 256), dim3(256), 0, st, p.bound, p.R, p.seqdone,
                        p.B);
-    if (p.dtype == kBF16)
-        hipLaunchKernelGGL(lmhead_kernel<kBF16>, dim3(groups), dim3(NT), kLdsBytes, st, p, in);
-    else
-        hipLaunchKernelGGL(lmhead_kernel<kF32>, dim3(groups), dim3(NT), kLdsBytes, st, p, in);
+    // the untruncated target (plaus_thresh = 0) has its own kernels: dense logits, no candidates
+    const dim3 grid(groups), block(NT);
+    if (p.dtype == kBF16) {
+        if (p.full)
+            hipLaunchKernelGGL((lmhead_kernel<kBF16, true>), grid, block, kLdsBytes, st, p, in);
+        else
+            hipLaunchKernelGGL((lmhead_kernel<kBF16, false>), grid, block, kLdsBytes, st, p, in);
+    } else {
+        if (p.full)
+            hipLaunchKernelGGL((lmhead_kernel<kF32, true>), grid, block, kLdsBytes, st, p, in);
+        else
+            hipLaunchKernelGGL((lmhead_kernel<kF32, false>), grid, block, kLdsBytes, st, p, in);
+    }
     return hipGetLastError();
 }
 

@@ -158,6 +158,71 @@ struct Smem {
     int ints[4];
 };
 
+// Writes a row's results: rowinfo (for the sequence phase) and the optional outputs.
+__device__ __forceinline__ void write_row(const Plan &P, int row, const float (&ri)[kRowInfo],
+                                          int32_t *row_argmax, float *row_stats) {
+    float4 *dst = reinterpret_cast<float4 *>(P.rowinfo + (size_t)row * kRowInfo);
+#pragma unroll
+    for (int k = 0; k < kRowInfo / 4; ++k) dst[k] = float4{ri[4 * k], ri[4 * k + 1], ri[4 * k + 2], ri[4 * k + 3]};
+    if (row_argmax) row_argmax[row] = __float_as_int(ri[RI_ARGMAX]);
+    if (row_stats) {
+#pragma unroll
+        for (int k = 0; k < 8; ++k) row_stats[(size_t)row * 8 + k] = ri[k];
+    }
+}
+
+// Row statistics of the untruncated target (wave 0): the two models' normalisers
+// from the per-tile (max, sum exp) pairs and the statistics of
+// y = (1+s) z_p - s z_q from the per-tile y statistics, both fetched in one round;
+// cd = y - (1+s) lse_p + s lse_q over the whole vocabulary.
+__device__ void row_stats_full(const Plan &P, int row, int lane, int32_t *row_argmax,
+                               float *row_stats) {
+    const float4 *pr = P.partials + (size_t)row * P.ntiles;
+    const float4 *yp = P.ypart + (size_t)row * P.ntiles * 2;
+    Lse lp{-INFINITY, 0.f}, lq{-INFINITY, 0.f};
+    YStat st{-INFINITY, -1, -INFINITY, 0.f, 0.f, 0.f, 0.f};
+    for (int base = 0; base < P.ntiles; base += kPass) {
+        float4 v[kTilesPerLane], u[kTilesPerLane], w2[kTilesPerLane];
+#pragma unroll
+        for (int k = 0; k < kTilesPerLane; ++k) {
+            const int t = min(base + lane + k * kWaveSize, P.ntiles - 1);
+            v[k] = pr[t];
+            u[k] = yp[2 * t];
+            w2[k] = yp[2 * t + 1];
+        }
+#pragma unroll
+        for (int k = 0; k < kTilesPerLane; ++k) {
+            if (base + lane + k * kWaveSize >= P.ntiles) continue;
+            lp = lse_merge(lp, Lse{v[k].x, v[k].y});
+            lq = lse_merge(lq, Lse{v[k].z, v[k].w});
+            st = ystat_merge(st, YStat{u[k].x, __float_as_int(w2[k].x), u[k].z, u[k].y, w2[k].y, w2[k].z, 0.f});
+        }
+    }
+    lp = wave_lse(lp);
+    lq = wave_lse(lq);
+#pragma unroll
+    for (int d = kWaveSize / 2; d > 0; d >>= 1)
+        st = ystat_merge(st, YStat{__shfl_down(st.y1, d, kWaveSize), __shfl_down(st.i1, d, kWaveSize),
+                                   __shfl_down(st.y2, d, kWaveSize), __shfl_down(st.ys, d, kWaveSize),
+                                   __shfl_down(st.zp1, d, kWaveSize), __shfl_down(st.zq1, d, kWaveSize),
+                                   0.f});
+    if (lane != 0) return;
+    const float max_p = lp.m, lse_p = lp.m + __logf(lp.s), lse_q = lq.m + __logf(lq.s);
+    const float shift = -(1.f + P.s) * lse_p + P.s * lse_q;  // cd - y
+    float ri[kRowInfo] = {};
+    ri[RI_MAXP] = max_p;
+    ri[RI_LSEP] = lse_p;
+    ri[RI_LSEQ] = lse_q;
+    ri[RI_LOGZ] = st.y1 + __logf(st.ys) + shift;
+    ri[RI_TOP1] = st.y1 + shift;
+    ri[RI_MARGIN] = st.y1 - st.y2;  // +inf with a single token
+    ri[RI_COUNT] = (float)P.V;
+    ri[RI_SIGNAL] = st.i1 >= 0 ? (st.zp1 - lse_p) - (st.zq1 - lse_q) : NAN;
+    ri[RI_THRESH] = max_p + P.log_theta;  // -inf: no mask
+    ri[RI_ARGMAX] = __int_as_float(st.i1);
+    write_row(P, row, ri, row_argmax, row_stats);
+}
+
 // ---------------------------------------------------------------------------
 // Row phase.  wave 0: the row's statistics; wave 1: the row as a draft node.
 template <int DT>
@@ -172,6 +237,21 @@ __device__ void combine_row(const Plan &P, const Inputs &in, int row, int lane, 
         const int j = in.parents[row], x = in.tokens[row];
         if (j < 0 || j >= i || x < 0 || x >= P.V) return;  // the sequence is rejected later
         const size_t rowj = (size_t)(row - i + j);
+        if (P.full) {  // every token is in the support; the expert logit is stored densely
+            const size_t esz = DT == kBF16 ? 2 : 4;
+            const float zp = P.zp_full[rowj * P.zstride + x];
+            float zq = 0.f;
+            if (P.store_q) {
+                zq = P.zq_full[rowj * P.zstride + x];
+            } else if (want_node_logits) {
+                zq = wave_dot<DT>((const char *)in.hq + rowj * P.dq * esz,
+                                  (const char *)in.wq + (size_t)x * P.dq * esz, P.dq, lane);
+                zq = (zq + (in.bq ? in.bq[x] : 0.f)) * P.inv_T;
+            }
+            if (lane == 0) P.nodez[row] = float4{zp, zq, 1.f, 0.f};
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+            return;
+        }
         // count, bitmap word and candidate slot are fetched together
         const int tcnt = P.tcount[rowj * P.ntiles + x / kTileTokens];
         const uint32_t word = P.bits[rowj * P.wstride + (x >> 5)];
@@ -197,6 +277,10 @@ __device__ void combine_row(const Plan &P, const Inputs &in, int row, int lane, 
         return;
     }
     if (wave != 0) return;
+    if (P.full) {
+        row_stats_full(P, row, lane, row_argmax, row_stats);
+        return;
+    }
 
     const float4 *pr = P.partials + (size_t)row * P.ntiles;
     const int *tc = P.tcount + (size_t)row * P.ntiles;
@@ -320,15 +404,7 @@ __device__ void combine_row(const Plan &P, const Inputs &in, int row, int lane, 
         ri[RI_SIGNAL] = signal;
         ri[RI_THRESH] = thr;
         ri[RI_ARGMAX] = __int_as_float(best.id);
-        float4 *dst = reinterpret_cast<float4 *>(P.rowinfo + (size_t)row * kRowInfo);
-#pragma unroll
-        for (int k = 0; k < kRowInfo / 4; ++k)
-            dst[k] = float4{ri[4 * k], ri[4 * k + 1], ri[4 * k + 2], ri[4 * k + 3]};
-        if (row_argmax) row_argmax[row] = best.id;
-        if (row_stats) {
-#pragma unroll
-            for (int k = 0; k < 8; ++k) row_stats[(size_t)row * 8 + k] = ri[k];
-        }
+        write_row(P, row, ri, row_argmax, row_stats);
     }
 }
 
@@ -504,6 +580,66 @@ __device__ int draw_token(const Plan &P, size_t jrow, const float *qrow, float u
     return -1;  // empty support (a row without mask members)
 }
 
+// Untruncated target: the same draw over the whole vocabulary of row jrow, from
+// the dense logits.  Each thread sums a contiguous token range; thread 0 scans the
+// partial sums in order; the thread whose range holds the target walks it.
+__device__ int draw_token_full(const Plan &P, size_t jrow, const float *qrow, float u, int tid,
+                               Smem &sm) {
+    const float *rj = P.rowinfo + jrow * kRowInfo;
+    const float lse_p = rj[RI_LSEP], lse_q = rj[RI_LSEQ], logZ = rj[RI_LOGZ];
+    const float *zp = P.zp_full + jrow * P.zstride, *zq = P.zq_full + jrow * P.zstride;
+    const int t0 = (int)((long long)tid * P.V / NT), t1 = (int)((long long)(tid + 1) * P.V / NT);
+    auto weight = [&](int t, bool residual) -> double {
+        const float p = __expf((1.f + P.s) * (zp[t] - lse_p) - P.s * (zq[t] - lse_q) - logZ);
+        return residual ? (double)fmaxf(0.f, p - qrow[t]) : (double)p;
+    };
+    double *local = sm.wts, *prefix = sm.wts + NT;  // [NT], [NT + 1]
+    auto scan = [&](bool residual) {
+        double acc = 0.0;
+        for (int t = t0; t < t1; ++t) acc += weight(t, residual);
+        local[tid] = acc;
+        __syncthreads();
+        if (tid == 0) {
+            double run = 0.0;
+            for (int i = 0; i < NT; ++i) {
+                prefix[i] = run;
+                run += local[i];
+            }
+            prefix[NT] = run;
+        }
+        __syncthreads();
+    };
+    bool residual = qrow != nullptr;
+    scan(residual);
+    if (residual && !(prefix[NT] > 0.0)) {  // degenerate residual: fall back to pi_CD
+        __syncthreads();
+        residual = false;
+        scan(false);
+    }
+    const double target = (double)u * prefix[NT];
+    if (tid == 0) sm.ints[1] = -1;
+    __syncthreads();
+    const double mine = local[tid], start = prefix[tid];
+    if (mine > 0.0 && start <= target && target < start + mine) {
+        double run = 0.0;
+        int found = -1, last = -1;
+        for (int t = t0; t < t1; ++t) {
+            const double wt = weight(t, residual);
+            run += wt;
+            if (wt > 0.0) {
+                last = t;
+                if (start + run > target) {
+                    found = t;
+                    break;
+                }
+            }
+        }
+        sm.ints[1] = found >= 0 ? found : last;
+    }
+    __syncthreads();
+    return sm.ints[1];
+}
+
 template <int DT, bool SAMPLE>
 __device__ void verify_sequence(const Plan &P, const Inputs &in, const Outputs &out,
                                 const SampleInputs &smp, int b, int tid, Smem &sm, int *dyn) {
@@ -602,7 +738,8 @@ __device__ void verify_sequence(const Plan &P, const Inputs &in, const Outputs &
     const int k = sm.ints[2];
     const int jrow = k < N ? k - 1 : N - 1;
     const float *qrow = k < N ? smp.draft_probs + (r0 + k) * V : nullptr;
-    const int next = draw_token(P, r0 + jrow, qrow, smp.u_res[r0 + jrow], tid, sm);
+    const int next = P.full ? draw_token_full(P, r0 + jrow, qrow, smp.u_res[r0 + jrow], tid, sm)
+                            : draw_token(P, r0 + jrow, qrow, smp.u_res[r0 + jrow], tid, sm);
     for (int i = tid; i < N; i += NT) out.accept_path[r0 + i] = i < k ? i : -1;
     if (tid == 0) {
         out.status[b] = 0;

@@ -89,6 +89,20 @@ def test_mask_and_strength_settings(theta, s):
     _check_greedy(case, tokens, f"theta={theta} s={s}", theta=theta, s=s)
 
 
+@pytest.mark.parametrize("seed", range(2))
+def test_untruncated_target_ragged(seed):
+    # theta = 0: every token is in the support (dense-logit path); 16 full tiles + 3
+    # tokens, 2 row blocks
+    case = synth.make_case("b8_tree64", 20 + seed, B=2, V=4099, dp=512, dq=256, theta=0.0)
+    g, _, _ = _check_greedy(case, _greedy_tokens(case), f"untruncated ragged seed {seed}")
+    assert np.all(g["row_stats"][:, oracle.RS_COUNT] == case.V)
+
+
+def test_untruncated_target_fp32_ragged_k():
+    case = synth.make_case("tiny_chain8", 22, N=19, V=777, dp=100, dq=36, theta=0.0)
+    _check_greedy(case, _greedy_tokens(case), "untruncated fp32")
+
+
 def test_flat_logits_every_token_in_mask():
     case = synth.make_case("tiny_chain8", 12, N=8, V=1500, dp=64, dq=32)
     case.wp[:] = 0
@@ -211,6 +225,32 @@ def test_sampled_always_accept_and_reject():
     assert np.all(g["accept_len"][:2] == case.N - 1) and np.all(g["accept_len"][2:] == 0)
 
 
+def test_untruncated_sampled_residual_over_vocabulary():
+    """theta = 0: a one-hot proposal on the target's least likely token is rejected at
+    node 1 and the residual, max(0, pi_CD - pi_e), spans the whole vocabulary."""
+    case = synth.make_case("s8_chain16x8", 23, B=4, N=6, V=1500, dp=128, dq=64, theta=0.0)
+    rows = oracle.eval_rows(case.hp, case.hq, case.wp, case.wq, case.bias, case.bias,
+                            theta=0.0, s=case.s, want_lpcd=True)
+    probs = np.zeros((case.R, case.V), np.float32)
+    tokens = np.zeros((case.B, case.N), np.int32)
+    for r in range(case.R):
+        i = r % case.N
+        if i == 0:
+            continue
+        p = np.exp(rows["lpcd"][r - 1])
+        if r // case.N < 2:  # proposal = target: always accepted
+            probs[r] = p
+            tokens[r // case.N, i] = int(np.argmax(p))
+        else:
+            t = int(np.argmin(p))
+            probs[r, t] = 1.0
+            tokens[r // case.N, i] = t
+    case.u_acc = np.maximum(np.minimum(case.u_acc, np.float32(0.99)), np.float32(1e-3))
+    g, o = _check_sample(case, probs, tokens, "untruncated accept / reject")
+    assert np.all(g["accept_len"][:2] == case.N - 1) and np.all(g["accept_len"][2:] == 0)
+    assert np.all(g["row_stats"][:, oracle.RS_COUNT] == case.V)
+
+
 def test_sampled_rejects_trees():
     case = synth.make_case("b8_tree64", 6, N=12, depth=3, max_children=4, V=600, dp=64, dq=32)
     case.cfg["mode"] = "sample"
@@ -230,6 +270,13 @@ def test_full_b8_tree64():
 
 
 @pytest.mark.slow
+def test_full_b8_tree64_untruncated():
+    case = synth.make_case("b8_tree64", 0, theta=0.0)
+    _say("b8_tree64 theta 0: oracle over all 64 rows")
+    _check_greedy(case, _greedy_tokens(case), "b8_tree64 theta 0")
+
+
+@pytest.mark.slow
 def test_full_b70_tree64():
     case = synth.make_case("b70_tree64", 0)
     _say("b70_tree64: oracle over all 64 rows")
@@ -238,8 +285,9 @@ def test_full_b70_tree64():
 
 
 @pytest.mark.slow
-def test_full_s8_chain16x8():
-    case = synth.make_case("s8_chain16x8", 0)
+@pytest.mark.parametrize("theta", [0.1, 0.0])
+def test_full_s8_chain16x8(theta):
+    case = synth.make_case("s8_chain16x8", 0, theta=theta)
     # stand-in drafter: expert logits of every parent row from a plain fp32 matmul
     dev = torch.device("cuda:0")
     hp = torch.from_numpy(synth.bf16_to_f32(case.hp)).to(dev)
@@ -249,7 +297,7 @@ def test_full_s8_chain16x8():
     parent_logits = np.zeros_like(z)
     parent_logits[1:] = z[:-1]
     probs, tokens = synth.sampled_draft(case, parent_logits)
-    _say("s8_chain16x8: oracle over sequences 0, 5, 10, 15")
+    _say(f"s8_chain16x8 theta {theta}: oracle over sequences 0, 5, 10, 15")
     seqs = [0, 5, 10, 15]
     rows = np.concatenate([np.arange(b * 8, b * 8 + 8) for b in seqs])
     o = oracle.verify("sample", len(seqs), 8, case.hp[rows], case.hq[rows], case.wp, case.wq,
