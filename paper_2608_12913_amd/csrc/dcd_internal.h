@@ -23,6 +23,8 @@ constexpr int kTileRows = kTileRBlocks * 16;         // 64 rows per workgroup
 constexpr int kWordsPerTile = kTileTokens / 32;      // candidate bit words per row and tile
 constexpr int kRowInfo = 16;                         // floats of per-row results
 constexpr int kMaxNodes = 4096;                      // nodes per sequence (staged in LDS)
+constexpr int kWideRows = 256;                       // rows per workgroup of the many-row LM-head kernel
+constexpr int kWideMinRows = 512;                    // rows from which that kernel is used
 
 // rowinfo slots (floats; the argmax is stored as an int bit pattern)
 enum {
@@ -115,6 +117,9 @@ size_t workspace_layout(Plan &p, char *base);  // fills the pointers when base !
 
 // LM heads with softmax partials and candidates (clears bound and seqdone first)
 hipError_t launch_lmhead(const Plan &p, const Inputs &in, hipStream_t st);
+// the many-row variant (bf16, masked target, R >= kWideMinRows): same outputs
+bool use_wide_lmhead(const Plan &p);
+hipError_t launch_lmhead_wide(const Plan &p, const Inputs &in, hipStream_t st);
 // per-row combination and per-sequence verification (greedy when smp is null)
 hipError_t launch_finish(const Plan &p, const Inputs &in, const Outputs &out,
                          const SampleInputs *smp, hipStream_t st);

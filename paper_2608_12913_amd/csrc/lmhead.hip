@@ -637,6 +637,7 @@ hipError_t launch_lmhead(const Plan &p, const Inputs &in, hipStream_t st) {
     const int ninit = p.R > p.B ? p.R : p.B;
     hipLaunchKernelGGL(init_kernel, dim3((ninit + 255) / 256), dim3(256), 0, st, p.bound, p.R, p.seqdone,
                        p.B);
+    if (use_wide_lmhead(p)) return launch_lmhead_wide(p, in, st);
     // the untruncated target (plaus_thresh = 0) has its own kernels: dense logits, no candidates
     const dim3 grid(groups), block(NT);
     if (p.dtype == kBF16) {

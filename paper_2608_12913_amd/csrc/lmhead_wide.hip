@@ -1,0 +1,437 @@
+// LM-head projection for many rows (the compute-bound regime), with the same
+// softmax-partials and candidate epilogue as the 64-row kernel (Alg. 1 "parallel
+// model evaluation", the per-tile pieces of Eq. (1) and the plausibility mask of
+// Sec. 2.1).
+//
+// With thousands of rows (many sequences verified together) the projection is a
+// dense GEMM far above the MFMA ridge, so the tile is shaped for reuse rather
+// than for streaming: a workgroup owns 256 tokens x 256 rows and its 4 waves form
+// a 2 x 2 grid of 128 x 128 blocks (64 v_mfma_f32_16x16x32_bf16 blocks, 256 fp32
+// accumulators per lane).  K is walked in 128-byte chunks of every row; a chunk's
+// 256 weight rows and 256 hidden-state rows go through registers into one of two
+// XOR-swizzled LDS stages, one barrier per chunk.  The 8 row tiles of a
+// vocabulary tile are dispatched together on one XCD, so its weights come from
+// HBM once and from that XCD's L2 for the others (ordinary cached loads).
+//
+// Epilogue: as in the 64-row kernel -- per (row, tile) the max and sum of exp of
+// both models, tile-local candidates (z_p within ln(theta) of the tile max)
+// pruned against the running row bound.  It works one 16-row block at a time and
+// recomputes logits from the accumulators; the block's logits also go to an LDS
+// buffer so that a lane can fetch the one of a given token.
+#include "dcd_internal.h"
+
+namespace dcd {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int NT = 256;               // threads per workgroup (4 waves)
+constexpr int TT = kTileTokens;       // tokens per tile (the partials' tile)
+constexpr int TR = kWideRows;         // rows per workgroup
+constexpr int CB = 128;               // bytes of every row per K-chunk
+constexpr int LPR = CB / 16;          // lanes per row in a load instruction
+constexpr int RPI = kWaveSize / LPR;  // rows per load instruction
+constexpr int SLAB = TT / 4;          // rows of each operand one wave loads per chunk
+constexpr int LOADS = SLAB / RPI;     // load instructions per operand, wave and chunk
+constexpr int BV = 8, BR = 8;         // 16-blocks per wave: tokens, rows
+constexpr int KS = CB / 64;           // MFMA k-steps per chunk
+constexpr int OPB = TT * CB;          // bytes of one operand chunk in LDS
+constexpr int WT = 16 * BV;           // tokens per wave (128)
+constexpr int WR = 16 * BR;           // rows per wave (128)
+constexpr int NV = 4 * BV;            // logits per lane and row block (32)
+static_assert(TT == 256 && TR == 256 && NT == 4 * kWaveSize, "2 x 2 waves of 128 x 128");
+static_assert(LPR == RPI && LOADS * RPI == SLAB, "a load instruction covers RPI whole rows");
+static_assert(NV == 32, "one bit per logit of a row block in a 32-bit mask");
+
+// LDS: two stages of [weights 256 x CB | hidden states 256 x CB]; both biases of
+// the tile; the parked candidate logits; the epilogue scratch reuses the stages.
+constexpr size_t kStageBytes = 2 * OPB;
+constexpr int kStash = BR;  // one parked logit per lane and row block
+constexpr size_t kLdsBytes = 2 * kStageBytes + 2 * TT * sizeof(float) + 4 * kStash * kWaveSize * sizeof(float);
+// epilogue scratch: (max, sum) pairs of the two token halves, candidate words and
+// counts, a row block's logits per wave
+constexpr size_t kPairsBytes = 2 * TR * sizeof(float2);
+constexpr size_t kWordsBytes = TR * kWordsPerTile * sizeof(uint32_t);
+constexpr size_t kCountBytes = TR * sizeof(int);
+constexpr size_t kZBytes = 4 * NV * kWaveSize * sizeof(float);
+static_assert(kPairsBytes + kWordsBytes + kCountBytes + kZBytes <= 2 * kStageBytes,
+              "epilogue scratch must fit the stages");
+
+__device__ __forceinline__ u32x4 ld16(const char *p) { return *reinterpret_cast<const u32x4 *>(p); }
+__device__ __forceinline__ void st_lds(char *p, u32x4 v) { *reinterpret_cast<u32x4 *>(p) = v; }
+__device__ __forceinline__ u32x4 ld_lds(const char *p) { return *reinterpret_cast<const u32x4 *>(p); }
+
+__device__ __forceinline__ float wave_max16_32(float x) {
+    x = fmaxf(x, __shfl_xor(x, 16));
+    return fmaxf(x, __shfl_xor(x, 32));
+}
+__device__ __forceinline__ float wave_sum16_32(float x) {
+    x += __shfl_xor(x, 16);
+    return x + __shfl_xor(x, 32);
+}
+
+// The loads of one K-chunk: this wave's quarter of the tile's weight rows and of
+// the workgroup's hidden-state rows.
+struct Batch {
+    u32x4 w[LOADS];
+    u32x4 h[LOADS];
+    bool hok;  // the hidden-state columns are inside the row (false only in the K tail)
+};
+
+// Per-thread load addresses of one model.  Lane (r, c) = (lane / LPR, lane % LPR)
+// reads 16 bytes at column c of rows RPI*q + r of the wave's slab: address =
+// wave-uniform row base + a 32-bit lane offset.  RAGGED (the tile reaches past the
+// vocabulary or past row R): rows past the end are clamped to the last one (their
+// results are discarded).
+template <bool RAGGED>
+struct Stream {
+    const char *wbase, *hbase;
+    uint32_t rowbytes;
+    // RAGGED: the slab's first row may lie past the last valid row, so the base is
+    // the first valid row of the slab (or the last valid row), `skip` the slab rows
+    // before it and `last` the last valid row, both relative to the base (>= 0)
+    int wskip, wlast, hskip, hlast;
+    int nch, r, col16;
+
+    __device__ __forceinline__ void init(const void *h, const void *w, int d, int R, int V, int row0,
+                                         int tile0) {
+        const int lane = threadIdx.x % kWaveSize, wave = threadIdx.x / kWaveSize;
+        r = lane / LPR;
+        col16 = lane % LPR;
+        rowbytes = (uint32_t)d * 2;
+        nch = (int)((rowbytes + CB - 1) / CB);
+        const int ws0 = tile0 + SLAB * wave, hs0 = row0 + SLAB * wave;  // slab first rows
+        const int wb = min(ws0, V - 1), hb = min(hs0, R - 1);
+        wbase = (const char *)w + (size_t)wb * rowbytes;
+        hbase = (const char *)h + (size_t)hb * rowbytes;
+        wskip = ws0 - wb;
+        wlast = V - 1 - wb;
+        hskip = hs0 - hb;
+        hlast = R - 1 - hb;
+    }
+
+    // In the K tail a weight lane past the row end re-reads the row's last 16
+    // bytes (finite values) and the hidden-state columns there are zero.
+    __device__ __forceinline__ void issue(int c, Batch &b) const {
+        const uint32_t col = (uint32_t)c * CB + col16 * 16;
+        const uint32_t wcol = col < rowbytes ? col : rowbytes - 16;
+        b.hok = col < rowbytes;
+        const uint32_t hcol = b.hok ? col : 0u;
+#pragma unroll
+        for (int q = 0; q < LOADS; ++q) {
+            if constexpr (RAGGED)
+                b.w[q] = ld16(wbase + (uint32_t)(min(wskip + RPI * q + r, wlast) * rowbytes + wcol));
+            else
+                b.w[q] = ld16(wbase + (size_t)q * RPI * rowbytes + (uint32_t)(r * rowbytes + wcol));
+        }
+#pragma unroll
+        for (int q = 0; q < LOADS; ++q) {
+            if constexpr (RAGGED)
+                b.h[q] = ld16(hbase + (uint32_t)(min(hskip + RPI * q + r, hlast) * rowbytes + hcol));
+            else
+                b.h[q] = ld16(hbase + (size_t)q * RPI * rowbytes + (uint32_t)(r * rowbytes + hcol));
+        }
+    }
+};
+
+// 16-byte column c of row m of a swizzled [256][CB] operand tile
+__device__ __forceinline__ int swz(int m, int c) { return m * CB + ((c ^ (m % LPR)) << 4); }
+
+// arrived batch -> stage `st` (weights, then hidden states; zero in the K tail)
+__device__ __forceinline__ void stage(const Batch &b, char *st) {
+    const int lane = threadIdx.x % kWaveSize, wave = threadIdx.x / kWaveSize;
+    const int off = swz(SLAB * wave + lane / LPR, lane % LPR);
+#pragma unroll
+    for (int q = 0; q < LOADS; ++q) st_lds(st + off + q * RPI * CB, b.w[q]);
+#pragma unroll
+    for (int q = 0; q < LOADS; ++q)
+        st_lds(st + OPB + off + q * RPI * CB, b.hok ? b.h[q] : u32x4{0u, 0u, 0u, 0u});
+}
+
+// The wave's 128 x 128 block over one staged chunk.  A = weights (tokens as M),
+// B = hidden states (rows as N); lane l supplies row l%16 of a block and K columns
+// 8*(l/16).. of the k-step.
+__device__ __forceinline__ void compute(const char *st, int wt, int wr, f32x4 (&acc)[BV][BR]) {
+    const int lane = threadIdx.x % kWaveSize, n = lane % 16, g = lane / 16;
+    const char *wb = st + (wt * WT + n) * CB, *hb = st + OPB + (wr * WR + n) * CB;
+    // a runtime loop over the k-steps: unrolled, the allocator splits the 256
+    // accumulators across register files and spills
+#pragma unroll 1
+    for (int s = 0; s < KS; ++s) {
+        const int col = ((4 * s + g) ^ (n % LPR)) << 4;
+        u32x4 bfr[BR];
+#pragma unroll
+        for (int rb = 0; rb < BR; ++rb) bfr[rb] = ld_lds(hb + 16 * rb * CB + col);
+#pragma unroll
+        for (int vb = 0; vb < BV; ++vb) {
+            const bf16x8 a = __builtin_bit_cast(bf16x8, ld_lds(wb + 16 * vb * CB + col));
+#pragma unroll
+            for (int rb = 0; rb < BR; ++rb)
+                acc[vb][rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, __builtin_bit_cast(bf16x8, bfr[rb]),
+                                                                      acc[vb][rb], 0, 0, 0);
+        }
+    }
+}
+
+// One pass over a model's K chunks, one batch in flight: stage chunk c into stage
+// c % 2, request chunk c+1, compute chunk c.  One barrier per chunk suffices: the
+// stage chunk c+1 goes to was last read by chunk c-1, which every wave finished
+// before passing chunk c's barrier.  Batch b holds chunk 0 on entry; if `next` is
+// given its chunk 0 is requested after the last chunk was staged.
+template <bool RAGGED>
+__device__ __forceinline__ void run_pass(const Stream<RAGGED> &st, const Stream<RAGGED> *next, Batch &b,
+                                         char *lds, int wt, int wr, f32x4 (&acc)[BV][BR]) {
+#pragma unroll
+    for (int vb = 0; vb < BV; ++vb)
+#pragma unroll
+        for (int rb = 0; rb < BR; ++rb) acc[vb][rb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    int c = 0;
+    for (; c + 1 < st.nch; ++c) {
+        char *sg = lds + (c & 1) * kStageBytes;
+        stage(b, sg);
+        st.issue(c + 1, b);
+        __builtin_amdgcn_sched_barrier(0);
+        __syncthreads();
+        compute(sg, wt, wr, acc);
+    }
+    char *sg = lds + (c & 1) * kStageBytes;
+    stage(b, sg);
+    if (next) next->issue(0, b);
+    __builtin_amdgcn_sched_barrier(0);
+    __syncthreads();
+    compute(sg, wt, wr, acc);
+    __syncthreads();  // the stages are reused by the epilogue
+}
+
+// Logits of row block rb for this lane (token 16vb + 4g + j of the wave's half,
+// row 16rb + n of its half), divided by T; -inf past the vocabulary.
+template <bool RAGGED>
+__device__ __forceinline__ void block_logits(const f32x4 (&acc)[BV][BR], int rb, const float *bias,
+                                             float inv_T, int tok0, int V, float (&z)[BV][4]) {
+    const int g = (threadIdx.x % kWaveSize) / 16;
+#pragma unroll
+    for (int vb = 0; vb < BV; ++vb) {
+        const float4 bv = *reinterpret_cast<const float4 *>(bias + 16 * vb + 4 * g);
+        const float bj[4] = {bv.x, bv.y, bv.z, bv.w};
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            z[vb][j] = fmaf(acc[vb][rb][j], inv_T, bj[j]);
+            if (RAGGED && tok0 + 16 * vb + 4 * g + j >= V) z[vb][j] = -INFINITY;
+        }
+    }
+}
+
+// Per row of the workgroup (this lane's 8 rows): the tile's max and sum of exp of
+// one model, from the two token halves (one LDS exchange, merged in order).
+template <bool RAGGED>
+__device__ __forceinline__ void tile_softmax(const f32x4 (&acc)[BV][BR], const float *bias,
+                                             float inv_T, int tok0, int V, int wt, int wr, float2 *pairs,
+                                             float (&tmax)[BR], float (&tsum)[BR]) {
+    constexpr float kLog2e = 1.4426950408889634f;
+    const int lane = threadIdx.x % kWaveSize, n = lane % 16, g = lane / 16;
+#pragma unroll
+    for (int rb = 0; rb < BR; ++rb) {
+        float z[BV][4];
+        block_logits<RAGGED>(acc, rb, bias, inv_T, tok0, V, z);
+        float m = -INFINITY;
+#pragma unroll
+        for (int vb = 0; vb < BV; ++vb)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) m = fmaxf(m, z[vb][j]);
+        m = wave_max16_32(m);
+        const float ml = m * kLog2e;
+        float s = 0.f;
+#pragma unroll
+        for (int vb = 0; vb < BV; ++vb)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) s += __builtin_amdgcn_exp2f(fmaf(z[vb][j], kLog2e, -ml));
+        if (m == -INFINITY) s = 0.f;
+        s = wave_sum16_32(s);
+        if (g == 0) pairs[wt * TR + wr * WR + rb * 16 + n] = float2{m, s};
+    }
+    __syncthreads();
+#pragma unroll
+    for (int rb = 0; rb < BR; ++rb) {
+        const float2 a = pairs[wr * WR + rb * 16 + n], b = pairs[TR + wr * WR + rb * 16 + n];
+        const float m = fmaxf(a.x, b.x);
+        float s = 0.f;
+        if (m != -INFINITY) {
+            if (a.x != -INFINITY) s += a.y * __expf(a.x - m);
+            if (b.x != -INFINITY) s += b.y * __expf(b.x - m);
+        }
+        tmax[rb] = m;
+        tsum[rb] = s;
+    }
+    __syncthreads();  // the pairs are reused
+}
+
+template <bool RAGGED>
+__device__ __forceinline__ void wide_tile(const Plan &P, const Inputs &in, int tile, int row0, char *lds) {
+    const int tid = threadIdx.x, lane = tid % kWaveSize;
+    const int wave = __builtin_amdgcn_readfirstlane(tid / kWaveSize);
+    const int wt = wave & 1, wr = wave >> 1;
+    const int n = lane % 16, g = lane / 16;
+    const int tile0 = tile * TT;
+    const int tok0 = tile0 + wt * WT;  // first token of the wave's half
+
+    float *bias_p = reinterpret_cast<float *>(lds + 2 * kStageBytes);  // [TT]
+    float *bias_q = bias_p + TT;                                      // [TT]
+    float *stash = bias_q + TT + wave * kStash * kWaveSize;           // [BR][64]
+    float2 *pairs = reinterpret_cast<float2 *>(lds);                  // [2][TR]
+    uint32_t *twords = reinterpret_cast<uint32_t *>(lds + kPairsBytes);                 // [TR][words]
+    int *tcnt = reinterpret_cast<int *>(lds + kPairsBytes + kWordsBytes);              // [TR]
+    float *zbuf = reinterpret_cast<float *>(lds + kPairsBytes + kWordsBytes + kCountBytes) +
+                  wave * NV * kWaveSize;  // [NV][64]: the lane's logits of one row block
+
+    if (tid < TT) {
+        const int t = tile0 + tid;
+        bias_p[tid] = (t < P.V && in.bp) ? in.bp[t] * P.inv_T : 0.f;
+        bias_q[tid] = (t < P.V && in.bq) ? in.bq[t] * P.inv_T : 0.f;
+    }
+
+    Stream<RAGGED> sp, sq;
+    sp.init(in.hp, in.wp, P.dp, P.R, P.V, row0, tile0);
+    sq.init(in.hq, in.wq, P.dq, P.R, P.V, row0, tile0);
+    f32x4 acc[BV][BR];
+    float pmax[BR], psum[BR], qmax[BR], qsum[BR];
+    uint32_t flags[BR];  // bit vb*4 + j: tile-local candidate
+    Batch b;
+
+    // ---- expert head
+    sp.issue(0, b);
+    run_pass<RAGGED>(sp, nullptr, b, lds, wt, wr, acc);
+    const float *bias = bias_p + wt * WT;  // this wave's half of the tile (then bias_q's)
+    tile_softmax<RAGGED>(acc, bias, P.inv_T, tok0, P.V, wt, wr, pairs, pmax, psum);
+    // tile-local candidates; the lane's first of each row block waits in its LDS
+    // slot, further ones (rare) are stored now from the row block's logit buffer
+#pragma unroll
+    for (int rb = 0; rb < BR; ++rb) {
+        const int row = row0 + wr * WR + rb * 16 + n;
+        const float thr = pmax[rb] + P.log_theta;
+        float z[BV][4];
+        block_logits<RAGGED>(acc, rb, bias, P.inv_T, tok0, P.V, z);
+        uint32_t f = 0;
+        float first = 0.f;
+#pragma unroll
+        for (int vb = 0; vb < BV; ++vb)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const bool c = (!RAGGED || tok0 + 16 * vb + 4 * g + j < P.V) && z[vb][j] >= thr;
+                first = (c && f == 0) ? z[vb][j] : first;
+                f |= c ? 1u << (vb * 4 + j) : 0u;
+            }
+        f = row < P.R ? f : 0u;
+        flags[rb] = f;
+        stash[rb * kWaveSize + lane] = first;
+        uint32_t rest = f & (f - 1);
+        if (__builtin_amdgcn_ballot_w64(rest != 0)) {  // wave-uniform
+#pragma unroll
+            for (int vb = 0; vb < BV; ++vb)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) zbuf[(vb * 4 + j) * kWaveSize + lane] = z[vb][j];
+            while (rest) {
+                const int bit = __builtin_ctz(rest);
+                rest &= rest - 1;
+                P.cand[(size_t)row * P.V + tok0 + 16 * (bit / 4) + 4 * g + bit % 4].x =
+                    zbuf[bit * kWaveSize + lane];
+            }
+        }
+        if (wt == 0 && g == 0 && row < P.R) atomicMax(&P.bound[row], ordered_key(pmax[rb]));
+    }
+
+    // ---- amateur head (its first staging overwrites the logit buffers of waves
+    // that may still be in the loop above)
+    sq.issue(0, b);
+    __syncthreads();
+    run_pass<RAGGED>(sq, nullptr, b, lds, wt, wr, acc);
+    float bnd[BR];
+#pragma unroll
+    for (int rb = 0; rb < BR; ++rb) {
+        const int row = min(row0 + wr * WR + rb * 16 + n, P.R - 1);
+        bnd[rb] = flags[rb] ? key_value(__atomic_load_n(&P.bound[row], __ATOMIC_RELAXED)) : 0.f;
+    }
+    bias = bias_q + wt * WT;
+    for (int i = tid; i < TR * kWordsPerTile; i += NT) twords[i] = 0;
+    for (int i = tid; i < TR; i += NT) tcnt[i] = 0;
+    tile_softmax<RAGGED>(acc, bias, P.inv_T, tok0, P.V, wt, wr, pairs, qmax, qsum);
+#pragma unroll
+    for (int rb = 0; rb < BR; ++rb) {
+        const int rloc = wr * WR + rb * 16 + n, row = row0 + rloc;
+        // a tile whose expert max is below the row bound + ln(theta) holds no mask member
+        const uint32_t f = pmax[rb] >= bnd[rb] + P.log_theta ? flags[rb] : 0u;
+        if (!__builtin_amdgcn_ballot_w64(f != 0)) continue;  // wave-uniform skip
+        float z[BV][4];
+        block_logits<RAGGED>(acc, rb, bias, P.inv_T, tok0, P.V, z);
+#pragma unroll
+        for (int vb = 0; vb < BV; ++vb)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) zbuf[(vb * 4 + j) * kWaveSize + lane] = z[vb][j];
+        uint32_t rest = f;
+        const uint32_t lowest = f & (0u - f);  // the candidate parked in LDS
+        while (rest) {
+            const int bit = __builtin_ctz(rest);
+            rest &= rest - 1;
+            const int t = tok0 + 16 * (bit / 4) + 4 * g + bit % 4;
+            float2 *c = &P.cand[(size_t)row * P.V + t];
+            const float zq = zbuf[bit * kWaveSize + lane];
+            if ((1u << bit) == lowest)
+                *c = float2{stash[rb * kWaveSize + lane], zq};
+            else
+                c->y = zq;
+            atomicOr(&twords[rloc * kWordsPerTile + (t - tile0) / 32], 1u << (t % 32));
+        }
+        atomicAdd(&tcnt[rloc], __popc(f));
+    }
+    __syncthreads();
+    // per (row, tile): the candidate count, the bitmap words where it is nonzero,
+    // and the softmax partials of both models
+    for (int i = tid; i < TR * kWordsPerTile; i += NT) {
+        const int r = i / kWordsPerTile, row = row0 + r;
+        if (row < P.R && tcnt[r] > 0)
+            P.bits[(size_t)row * P.wstride + tile * kWordsPerTile + i % kWordsPerTile] = twords[i];
+    }
+    if (wt == 0 && g == 0) {
+#pragma unroll
+        for (int rb = 0; rb < BR; ++rb) {
+            const int rloc = wr * WR + rb * 16 + n, row = row0 + rloc;
+            if (row >= P.R) continue;
+            P.partials[(size_t)row * P.ntiles + tile] = float4{pmax[rb], psum[rb], qmax[rb], qsum[rb]};
+            P.tcount[(size_t)row * P.ntiles + tile] = tcnt[rloc];
+        }
+    }
+}
+
+__global__ __launch_bounds__(NT, 1) void lmhead_wide_kernel(Plan P, Inputs in) {
+    extern __shared__ __align__(16) char lds[];
+    // workgroup -> (vocabulary tile, row tile); the row tiles of one vocabulary tile
+    // are dispatched back to back on the same XCD (workgroup id modulo 8), so the
+    // tile's weights are read from HBM once and from that XCD's L2 otherwise
+    const int nrt = (P.R + TR - 1) / TR;
+    const int id = blockIdx.x, xcd = id % 8, local = id / 8;
+    const int tile = (local / nrt) * 8 + xcd;
+    if (tile >= P.ntiles) return;
+    const int row0 = (local % nrt) * TR;
+    if ((tile + 1) * TT > P.V || row0 + TR > P.R)  // workgroup-uniform
+        wide_tile<true>(P, in, tile, row0, lds);
+    else
+        wide_tile<false>(P, in, tile, row0, lds);
+}
+
+}  // namespace
+
+bool use_wide_lmhead(const Plan &p) { return p.dtype == kBF16 && !p.full && p.R >= kWideMinRows; }
+
+hipError_t launch_lmhead_wide(const Plan &p, const Inputs &in, hipStream_t st) {
+    static const hipError_t attr = hipFuncSetAttribute((const void *)lmhead_wide_kernel,
+                                                       hipFuncAttributeMaxDynamicSharedMemorySize,
+                                                       (int)kLdsBytes);
+    if (attr != hipSuccess) return attr;
+    const int nrt = (p.R + TR - 1) / TR;
+    const int groups = ((p.ntiles + 7) / 8) * 8 * nrt;
+    hipLaunchKernelGGL(lmhead_wide_kernel, dim3(groups), dim3(NT), kLdsBytes, st, p, in);
+    return hipGetLastError();
+}
+
+}  // namespace dcd

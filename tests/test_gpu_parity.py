@@ -77,6 +77,14 @@ def test_ragged_hidden_and_rows():
     _check_greedy(case, _greedy_tokens(case), "ragged K and rows")
 
 
+@pytest.mark.parametrize("seed", range(2))
+def test_many_rows_ragged(seed):
+    # 9 sequences x 64 nodes = 576 rows: the many-row LM-head kernel (256-row tiles,
+    # the last one ragged), a ragged vocabulary and a K tail (200 = 3 chunks + 8 bf16)
+    case = synth.make_case("b8_batch32x64", 30 + seed, B=9, V=4099, dp=512, dq=200)
+    _check_greedy(case, _greedy_tokens(case), f"many rows seed {seed}")
+
+
 def test_ragged_fp32():
     case = synth.make_case("tiny_chain8", 8, N=19, V=777, dp=100, dq=36)
     _check_greedy(case, _greedy_tokens(case), "ragged fp32")
