@@ -127,13 +127,23 @@ def main():
     R = case.R
     nodes_per_s = R / (ms_step * 1e-3)
     kbytes = lmhead_bytes(case)
-    achieved = kbytes / (ms_lmhead * 1e-3) / 1e9
-    # the committed counters cover the default workload only
-    traffic, traffic_src = (counted_traffic() if args.workload == "b8_tree64" and not over
+    flops = 2 * R * (case.dp + case.dq) * case.V
+    # many rows (bf16, masked target) go to the compute-shaped LM-head kernel
+    kernel = ("lmhead_wide_kernel" if case.dtype == "bf16" and case.theta > 0 and R >= 512
+              else "lmhead_kernel")
+    ridge = MFMA_BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9)
+    # the committed counters cover the default workloads of each kernel only
+    traffic, traffic_src = (counted_traffic(kernel, args.workload) if not over
                             else (None, "no counters for this workload"))
-    roofline = dict(bound="hbm", achieved=round(achieved, 1), peak=HBM_PEAK_GBS, unit="GB/s",
-                    frac=round(achieved / HBM_PEAK_GBS, 4), traffic=traffic,
-                    kernel="lmhead_kernel", algorithmic_bytes=kbytes,
+    if case.dtype == "bf16" and flops / kbytes > ridge:
+        achieved = flops / (ms_lmhead * 1e-3) / 1e12
+        roofline = dict(bound="mfma", achieved=round(achieved, 1), peak=MFMA_BF16_PEAK_TFLOPS,
+                        unit="TFLOP/s", frac=round(achieved / MFMA_BF16_PEAK_TFLOPS, 4))
+    else:
+        achieved = kbytes / (ms_lmhead * 1e-3) / 1e9
+        roofline = dict(bound="hbm", achieved=round(achieved, 1), peak=HBM_PEAK_GBS, unit="GB/s",
+                        frac=round(achieved / HBM_PEAK_GBS, 4))
+    roofline.update(traffic=traffic, kernel=kernel, algorithmic_bytes=kbytes, flops=flops,
                     avg_us=round(ms_lmhead * 1e3, 2), traffic_source=traffic_src)
 
     cpu = None
@@ -164,15 +174,16 @@ def main():
     print(json.dumps(line), flush=True)
 
 
-def counted_traffic():
-    """HBM bytes per LM-head launch from the committed profiler counter summary, or
-    None when the kernel sources have changed since the counters were taken."""
+def counted_traffic(kernel, workload):
+    """HBM bytes per LM-head launch from the committed profiler counter summary of this
+    kernel and workload, or None when there is none or the kernel sources have changed
+    since the counters were taken."""
     import hashlib
 
     root = os.path.dirname(os.path.abspath(__file__))
-    path = os.path.join(root, "profiles", "lmhead_kernel_b8_tree64_hbm_counters.txt")
+    path = os.path.join(root, "profiles", f"{kernel}_{workload}_hbm_counters.txt")
     if not os.path.exists(path):
-        return None, None
+        return None, "no counters for this workload"
     fields = {}
     for line in open(path):
         if ":" in line and not line.startswith(" "):
