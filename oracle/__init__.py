@@ -23,6 +23,8 @@ _LIB = os.path.join(_HERE, "liboracle.so")
 
 # row_stats slots
 RS_MAXP, RS_LSEP, RS_LSEQ, RS_LOGZ, RS_TOP1, RS_MARGIN, RS_COUNT, RS_SIGNAL = range(8)
+# row diagnostics slots: argmax pi_p, D_KL(pi_p||pi_q), D_KL(pi_p||pi_CD), expert top-2 logit gap
+RD_ARGMAX_P, RD_KL_PQ, RD_KL_PCD, RD_MARGIN_P = range(4)
 # node_stats slots
 NS_LPP, NS_LPQ, NS_CD, NS_LPCD, NS_INMASK, NS_RATIO = range(6)
 SEQ_OK, SEQ_BAD_TREE, SEQ_BAD_TOKEN, SEQ_NONFINITE, SEQ_NOT_CHAIN = range(5)
@@ -51,14 +53,14 @@ def _load():
         P = ctypes.c_void_p
         i32, f64 = ctypes.c_int, ctypes.c_double
         lib.dco_eval_rows.argtypes = [i32, i32, i32, P, P, P, P, P, P, f64, f64, f64, P, i32,
-                                      P, P, P, P, P, P, i32]
+                                      P, P, P, P, P, P, P, i32]
         lib.dco_eval_rows.restype = i32
         lib.dco_greedy_walk.argtypes = [i32, P, P, P, P, P, P]
         lib.dco_greedy_walk.restype = None
         lib.dco_sample_chain.argtypes = [i32, i32, P, P, P, P, P, P, P, P, P, P]
         lib.dco_sample_chain.restype = None
         lib.dco_verify.argtypes = [i32, i32, i32, i32, i32, i32, P, P, P, P, P, P, P, P,
-                                   f64, f64, f64, P, P, P, P, P, P, P, P, P, P, P, P, i32]
+                                   f64, f64, f64, P, P, P, P, P, P, P, P, P, P, P, P, P, i32]
         lib.dco_verify.restype = i32
         _lib = lib
     return _lib
@@ -84,7 +86,8 @@ def eval_rows(hp, hq, wp, wq, bp, bq, *, theta, s, temperature=1.0, rows=None,
               want_logits=False, want_lpcd=False, nthreads=0):
     """Per-row oracle evaluation.
 
-    Returns dict(argmax [n], stats [n, 8], gap [n], and optionally zp, zq, lpcd [n, V]).
+    Returns dict(argmax [n], stats [n, 8], gap [n], diag [n, 4] (RD_* slots), and
+    optionally zp, zq, lpcd [n, V]).
     """
     hp, hq, wp, wq = as_f32(hp), as_f32(hq), as_f32(wp), as_f32(wq)
     bp = None if bp is None else _c(bp, np.float32)
@@ -93,7 +96,8 @@ def eval_rows(hp, hq, wp, wq, bp, bq, *, theta, s, temperature=1.0, rows=None,
     dq = wq.shape[1]
     ids = None if rows is None else _c(rows, np.int32)
     n = hp.shape[0] if ids is None else len(ids)
-    out = dict(argmax=np.empty(n, np.int32), stats=np.empty((n, 8)), gap=np.empty(n))
+    out = dict(argmax=np.empty(n, np.int32), stats=np.empty((n, 8)), gap=np.empty(n),
+               diag=np.empty((n, 4)))
     if want_logits:
         out["zp"] = np.empty((n, V))
         out["zq"] = np.empty((n, V))
@@ -102,7 +106,7 @@ def eval_rows(hp, hq, wp, wq, bp, bq, *, theta, s, temperature=1.0, rows=None,
     rc = _load().dco_eval_rows(V, dp, dq, _p(hp), _p(hq), _p(wp), _p(wq), _p(bp), _p(bq),
                                float(temperature), float(theta), float(s), _p(ids), n,
                                _p(out["argmax"]), _p(out["stats"]), _p(out["gap"]),
-                               _p(out.get("zp")), _p(out.get("zq")), _p(out.get("lpcd")),
+                               _p(out["diag"]), _p(out.get("zp")), _p(out.get("zq")), _p(out.get("lpcd")),
                                int(nthreads))
     if rc:
         raise RuntimeError(f"dco_eval_rows failed ({rc})")
@@ -155,13 +159,14 @@ def verify(mode, B, N, hp, hq, wp, wq, bp, bq, parents, tokens, *, theta, s,
     o = dict(accept_len=np.zeros(B, np.int32), accept_path=np.zeros((B, N), np.int32),
              next_token=np.zeros(B, np.int32), status=np.zeros(B, np.int32),
              row_argmax=np.zeros(R, np.int32), row_stats=np.zeros((R, 8)),
-             node_stats=np.zeros((R, 6)), row_gap=np.zeros(R), res_gap=np.zeros(B))
+             node_stats=np.zeros((R, 6)), row_diag=np.zeros((R, 4)), row_gap=np.zeros(R),
+             res_gap=np.zeros(B))
     rc = _load().dco_verify(m, B, N, V, dp, dq, _p(hp), _p(hq), _p(wp), _p(wq), _p(bp), _p(bq),
                             _p(parents), _p(tokens), float(theta), float(s), float(temperature),
                             _p(draft_probs), _p(u_acc), _p(u_res), _p(o["accept_len"]),
                             _p(o["accept_path"]), _p(o["next_token"]), _p(o["status"]),
                             _p(o["row_argmax"]), _p(o["row_stats"]), _p(o["node_stats"]),
-                            _p(o["row_gap"]), _p(o["res_gap"]), int(nthreads))
+                            _p(o["row_diag"]), _p(o["row_gap"]), _p(o["res_gap"]), int(nthreads))
     if rc:
         raise RuntimeError(f"dco_verify failed ({rc})")
     return o

@@ -23,6 +23,10 @@
  *                       applied before renormalising (Appendix remark
  *                       "Plausibility-constrained CD").  s is the contrastive
  *                       strength, theta the plausibility cutoff.
+ *   row_diag            diagnostics of Sec. 3.2 and of the KL-decomposition lemma
+ *                       (appendix on distribution alignment): the expert's own
+ *                       top-1 token, D_KL(pi_p || pi_q) and D_KL(pi_p || pi_CD),
+ *                       each summed from its definition.
  *   dco_greedy_walk     greedy (T = 0) verification of a draft tree: a draft
  *                       token is accepted iff it equals the target's argmax
  *                       (Alg. 1 with a one-hot target), walked from the root.
@@ -56,6 +60,8 @@
 
 /* row statistics slots */
 enum { RS_MAXP = 0, RS_LSEP, RS_LSEQ, RS_LOGZ, RS_TOP1, RS_MARGIN, RS_COUNT, RS_SIGNAL, RS_N };
+/* row diagnostics slots */
+enum { RD_ARGMAX_P = 0, RD_KL_PQ, RD_KL_PCD, RD_MARGIN_P, RD_N };
 /* node statistics slots */
 enum { NS_LPP = 0, NS_LPQ, NS_CD, NS_LPCD, NS_INMASK, NS_RATIO, NS_N };
 
@@ -162,15 +168,58 @@ static void cd_row(const double *zp, const double *zq, int V, double theta, doub
 }
 
 /*
+ * Diagnostics of one row, after cd_row:
+ *   RD_ARGMAX_P  argmax_x pi_p(x), the expert's own greedy token (lowest id on ties);
+ *   RD_KL_PQ     D_KL(pi_p || pi_q)  = sum_x pi_p(x) (log pi_p(x) - log pi_q(x));
+ *   RD_KL_PCD    D_KL(pi_p || pi_CD) = sum_x pi_p(x) (log pi_p(x) - log pi_CD(x)), with
+ *                pi_CD the target of cd_row.  Off the mask pi_CD = 0 while pi_p > 0, so
+ *                a mask that leaves out a token with pi_p > 0 gives +inf;
+ *   RD_MARGIN_P  largest minus second-largest expert logit (0 on a tie), the margin
+ *                that decides RD_ARGMAX_P.
+ * Terms with pi_p(x) = 0 contribute 0 (x log x -> 0).
+ */
+static void row_diag(const double *zp, const double *zq, int V, double theta, double s,
+                     const row_result *r, double *diag)
+{
+    const double Mp = r->stats[RS_MAXP], lsep = r->stats[RS_LSEP], lseq = r->stats[RS_LSEQ];
+    const double logZ = r->stats[RS_LOGZ];
+    const double log_theta = theta > 0.0 ? log(theta) : -INFINITY;
+    int amax = -1;
+    double second = -INFINITY;
+    for (int v = 0; v < V; ++v) {
+        if (amax < 0 && zp[v] == Mp)
+            amax = v;
+        else if (zp[v] > second)
+            second = zp[v];
+    }
+    double kl_pq = 0.0, kl_pcd = 0.0;
+    for (int v = 0; v < V; ++v) {
+        const double lpp = zp[v] - lsep, lpq = zq[v] - lseq, pp = exp(lpp);
+        if (pp == 0.0) continue;
+        kl_pq += pp * (lpp - lpq);
+        if ((zp[v] - Mp) >= log_theta) {
+            const double lpcd = (1.0 + s) * lpp - s * lpq - logZ;
+            kl_pcd += pp * (lpp - lpcd);
+        } else {
+            kl_pcd = INFINITY;
+        }
+    }
+    diag[RD_ARGMAX_P] = (double)amax;
+    diag[RD_KL_PQ] = kl_pq;
+    diag[RD_KL_PCD] = kl_pcd;
+    diag[RD_MARGIN_P] = Mp - second;
+}
+
+/*
  * Evaluate n_rows rows (row_ids[i], or i when row_ids is NULL) of an R-row problem.
  * Outputs per evaluated row: argmax, stats[8], boundary gap, and optionally the
- * logits of both models and log pi_CD over the vocabulary.
+ * diagnostics [RD_N], the logits of both models and log pi_CD over the vocabulary.
  */
 int dco_eval_rows(int V, int dp, int dq,
                   const float *hp, const float *hq, const float *wp, const float *wq,
                   const float *bp, const float *bq, double temperature, double theta, double s,
                   const int32_t *row_ids, int n_rows,
-                  int32_t *argmax_out, double *stats_out, double *gap_out,
+                  int32_t *argmax_out, double *stats_out, double *gap_out, double *diag_out,
                   double *zp_out, double *zq_out, double *lpcd_out, int nthreads)
 {
     if (V <= 0 || dp <= 0 || dq <= 0 || n_rows < 0 || !(temperature > 0.0)) return -2;
@@ -187,6 +236,7 @@ int dco_eval_rows(int V, int dp, int dq,
         if (argmax_out) argmax_out[i] = res.argmax;
         if (stats_out) memcpy(stats_out + (size_t)i * RS_N, res.stats, sizeof(res.stats));
         if (gap_out) gap_out[i] = res.gap;
+        if (diag_out) row_diag(zp, zq, V, theta, s, &res, diag_out + (size_t)i * RD_N);
         if (zp_out) memcpy(zp_out + (size_t)i * V, zp, sizeof(double) * (size_t)V);
         if (zq_out) memcpy(zq_out + (size_t)i * V, zq, sizeof(double) * (size_t)V);
     }
@@ -337,7 +387,7 @@ static void reset_sequence(int N, int32_t *accept_len, int32_t *path, int32_t *n
  * Full verification of B sequences of N nodes each (rows are b*N + i).
  * mode 0 = greedy (temperature ignored), mode 1 = sampled chains.
  * Optional outputs may be NULL: row_argmax [R], row_stats [R][8], node_stats [R][6],
- * row_gap [R], res_gap [B].
+ * row_diag [R][RD_N], row_gap [R], res_gap [B].
  */
 int dco_verify(int mode, int B, int N, int V, int dp, int dq,
                const float *hp, const float *hq, const float *wp, const float *wq,
@@ -345,8 +395,8 @@ int dco_verify(int mode, int B, int N, int V, int dp, int dq,
                double theta, double s, double temperature,
                const float *draft_probs, const float *u_acc, const float *u_res,
                int32_t *accept_len, int32_t *accept_path, int32_t *next_token, int32_t *status,
-               int32_t *row_argmax, double *row_stats, double *node_stats, double *row_gap,
-               double *res_gap, int nthreads)
+               int32_t *row_argmax, double *row_stats, double *node_stats, double *row_diag,
+               double *row_gap, double *res_gap, int nthreads)
 {
     if (B <= 0 || N <= 0 || V <= 0) return -2;
     if (mode == 1 && (!draft_probs || !u_acc || !u_res || !(temperature > 0.0))) return -3;
@@ -367,7 +417,8 @@ int dco_verify(int mode, int B, int N, int V, int dp, int dq,
         /* every row of the sequence: logits, stats, log pi_CD */
         int rc = dco_eval_rows(V, dp, dq, hp + (size_t)r0 * dp, hq + (size_t)r0 * dq, wp, wq, bp,
                                bq, T, theta, s, NULL, N, amax + r0, stats + (size_t)r0 * RS_N,
-                               gap + r0, zp, zq, lp_cd, nthreads);
+                               gap + r0, row_diag ? row_diag + (size_t)r0 * RD_N : NULL, zp, zq,
+                               lp_cd, nthreads);
         if (rc) { free(amax); free(stats); free(gap); free(lp_cd); free(zp); free(zq); return rc; }
 
         const int32_t *par = parents + r0, *tok = tokens + r0;

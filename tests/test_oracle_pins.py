@@ -283,6 +283,95 @@ def test_contrastive_signal_statistic():
                                lp[np.arange(4), a] - lq[np.arange(4), a], atol=1e-12)
 
 
+# ---------------------------------------------------------------- row diagnostics
+def test_row_diagnostics_kl_by_library_and_lemma():
+    """D_KL(pi_p||pi_q) equals scipy's relative entropy of the two softmaxes, and the
+    oracle's D_KL(pi_p||pi_CD), summed from its definition, obeys the lemma
+    KL(p||cd) = log Z - s KL(p||q) of the KL-decomposition lemma (untruncated target)."""
+    from scipy.stats import entropy
+    rng = np.random.default_rng(13)
+    hp, hq, wp, wq, b = _random_problem(rng, 700, 24, 16, 5, scale=3.0)
+    for s in (0.1, 0.5, 1.0, 2.5):
+        out = oracle.eval_rows(hp, hq, wp, wq, b, b, theta=0.0, s=s, want_logits=True)
+        d = out["diag"]
+        pp, pq = np.exp(_softmax_log(out["zp"])), np.exp(_softmax_log(out["zq"]))
+        np.testing.assert_allclose(d[:, oracle.RD_KL_PQ], entropy(pp, pq, axis=1), rtol=1e-10)
+        logZ = out["stats"][:, oracle.RS_LOGZ]
+        np.testing.assert_allclose(d[:, oracle.RD_KL_PCD], logZ - s * d[:, oracle.RD_KL_PQ],
+                                   atol=1e-10)
+        assert np.all(d[:, oracle.RD_KL_PQ] > 0) and np.all(d[:, oracle.RD_KL_PCD] > 0)
+
+
+def test_row_diagnostics_two_token_closed_form():
+    """Two tokens, z_p = (0, 1), z_q = (0, 0), s = 1: pi_p = (1, e)/(1+e), pi_q = (1/2, 1/2),
+    pi_CD ∝ pi_p^2 / pi_q ∝ (1, e^2), so KL(p||q) = ln 2 + sum pi_p ln pi_p and
+    KL(p||cd) = sum pi_p ln(pi_p / pi_CD), written out by hand."""
+    import math
+    e = math.e
+    hp, hq, wp, wq, bp, bq = _bias_only_case([0.0, 1.0], [0.0, 0.0])
+    out = oracle.eval_rows(hp, hq, wp, wq, bp, bq, theta=0.0, s=1.0)
+    p0, p1 = 1 / (1 + e), e / (1 + e)
+    c0, c1 = 1 / (1 + e * e), e * e / (1 + e * e)
+    kl_pq = p0 * math.log(2 * p0) + p1 * math.log(2 * p1)
+    kl_pcd = p0 * math.log(p0 / c0) + p1 * math.log(p1 / c1)
+    d = out["diag"][0]
+    assert abs(d[oracle.RD_KL_PQ] - kl_pq) < 1e-14
+    assert abs(d[oracle.RD_KL_PCD] - kl_pcd) < 1e-14
+    assert d[oracle.RD_ARGMAX_P] == 1 and abs(d[oracle.RD_MARGIN_P] - 1.0) < 1e-15
+
+
+def test_row_diagnostics_special_cases():
+    """s = 0 gives pi_CD = pi_p (KL(p||cd) = 0); identical models give KL = 0 for both;
+    a mask that drops a token with pi_p > 0 gives KL(p||cd) = +inf; flat logits keep
+    the whole vocabulary in the mask and every divergence at 0."""
+    rng = np.random.default_rng(14)
+    hp, hq, wp, wq, b = _random_problem(rng, 300, 16, 16, 4, scale=3.0)
+    d = oracle.eval_rows(hp, hq, wp, wq, b, b, theta=0.0, s=0.0)["diag"]
+    np.testing.assert_allclose(d[:, oracle.RD_KL_PCD], 0.0, atol=1e-12)
+    d = oracle.eval_rows(hp, hp, wp, wp, b, b, theta=0.0, s=0.8)["diag"]
+    np.testing.assert_allclose(d[:, [oracle.RD_KL_PQ, oracle.RD_KL_PCD]], 0.0, atol=1e-12)
+    out = oracle.eval_rows(hp, hq, wp, wq, b, b, theta=0.1, s=0.5)
+    assert np.all(out["stats"][:, oracle.RS_COUNT] < 300)
+    assert np.all(np.isposinf(out["diag"][:, oracle.RD_KL_PCD]))
+    assert np.all(np.isfinite(out["diag"][:, oracle.RD_KL_PQ]))
+    z = np.zeros((1, 8), np.float32)
+    w = np.zeros((64, 8), np.float32)
+    d = oracle.eval_rows(z, z, w, w, None, None, theta=0.3, s=0.5)["diag"][0]
+    assert d[oracle.RD_KL_PQ] == 0.0 and abs(d[oracle.RD_KL_PCD]) < 1e-15
+    assert d[oracle.RD_ARGMAX_P] == 0 and d[oracle.RD_MARGIN_P] == 0.0
+
+
+def test_expert_top1_by_sort_and_agreement_with_cd():
+    """The expert's top-1 is the first index of the largest expert logit (stable sort),
+    its margin the gap to the runner-up; with s = 0, or with theta = 1 (a one-token
+    mask), the CD argmax is the expert's top-1."""
+    rng = np.random.default_rng(15)
+    hp, hq, wp, wq, b = _random_problem(rng, 211, 16, 8, 12, scale=4.0)
+    for theta, s in ((0.0, 0.0), (0.1, 0.0), (1.0, 0.7), (0.05, 0.9)):
+        out = oracle.eval_rows(hp, hq, wp, wq, b, b, theta=theta, s=s, want_logits=True)
+        d = out["diag"]
+        for r in range(12):
+            order = np.argsort(-out["zp"][r], kind="stable")
+            assert d[r, oracle.RD_ARGMAX_P] == order[0]
+            assert d[r, oracle.RD_MARGIN_P] == out["zp"][r, order[0]] - out["zp"][r, order[1]]
+        if s == 0.0 or theta == 1.0:
+            assert np.array_equal(d[:, oracle.RD_ARGMAX_P], out["argmax"])
+    # an exact tie of the two largest expert logits goes to the lower id
+    hp_, hq_, wp_, wq_, bp_, bq_ = _bias_only_case([0.0, 2.0, 1.0, 2.0], [0.0, 0.0, 0.0, 0.0])
+    d = oracle.eval_rows(hp_, hq_, wp_, wq_, bp_, bq_, theta=0.0, s=0.5)["diag"][0]
+    assert d[oracle.RD_ARGMAX_P] == 1 and d[oracle.RD_MARGIN_P] == 0.0
+
+
+def test_verify_returns_row_diagnostics_of_every_row():
+    rng = np.random.default_rng(16)
+    hp, hq, wp, wq, b = _random_problem(rng, 150, 16, 8, 6, scale=3.0)
+    parents = np.array([[-1, 0, 1], [-1, 0, 0]], np.int32)
+    tokens = np.array([[0, 3, 4], [0, 5, 6]], np.int32)
+    o = oracle.verify("greedy", 2, 3, hp, hq, wp, wq, b, b, parents, tokens, theta=0.0, s=0.5)
+    d = oracle.eval_rows(hp, hq, wp, wq, b, b, theta=0.0, s=0.5)["diag"]
+    np.testing.assert_array_equal(o["row_diag"], d)
+
+
 # ---------------------------------------------------------------- greedy walk
 def _parse_ints(s):
     return np.array([int(x) for x in s.split(",")], np.int32)
