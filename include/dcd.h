@@ -97,6 +97,16 @@ enum {
     DCD_NODE_IN_MASK = 4,/* 1 if tok_i is in the parent row's mask, else 0            */
     DCD_NODE_RATIO = 5   /* sampled: pi_CD(tok_i) / pi_e(tok_i) (+inf if pi_e = 0); greedy: NaN */
 };
+/*
+ * row_kl slots (2 floats per row): the divergences of the KL-decomposition lemma
+ * (appendix on distribution alignment), per row and over the whole vocabulary.
+ *   DCD_KL_P_Q   D_KL(pi_p || pi_q)
+ *   DCD_KL_P_CD  D_KL(pi_p || pi_CD) = log Z_CD - s * D_KL(pi_p || pi_q) (the lemma)
+ * Both need both models' logits at every token, which only the untruncated target
+ * (plaus_thresh = 0) keeps; with a mask DCD_KL_P_Q is NaN and DCD_KL_P_CD is +inf
+ * (pi_p > 0 where pi_CD = 0) when the mask leaves out any token, NaN otherwise.
+ */
+enum { DCD_KL_P_Q = 0, DCD_KL_P_CD = 1 };
 
 typedef struct {
     int32_t batch;       /* B >= 1 sequences                                            */
@@ -132,6 +142,12 @@ typedef struct {                 /* device pointers, written by the call        
                                     ties go to the lowest token id                        */
     float *row_stats;            /* [B*N, 8] optional: DCD_ROW_* slots                    */
     float *node_stats;           /* [B*N, 6] optional: DCD_NODE_* slots                   */
+    /* diagnostics of Sec. 3.2 (signal and top-1 agreement at x* = argmax pi_CD; the
+       signal itself is DCD_ROW_SIGNAL) and of the appendix's KL lemma             */
+    int32_t *row_argmax_expert;  /* [B*N] optional: argmax of pi_p, the expert's own greedy
+                                    token (lowest id on ties); top-1 agreement with the
+                                    target is row_argmax_expert == row_argmax          */
+    float *row_kl;               /* [B*N, 2] optional: DCD_KL_* slots                     */
 } dcd_outputs;
 
 /*
@@ -194,7 +210,7 @@ int dcd_lmhead_partials(const dcd_problem *p, const dcd_inputs *in, int sampled,
 /* static description of a return code (never NULL) */
 const char *dcd_error_string(int code);
 
-/* ABI version of this header: 1 */
+/* ABI version of this header: 2 (dcd_outputs gained row_argmax_expert and row_kl) */
 int dcd_abi_version(void);
 
 #ifdef __cplusplus

@@ -67,7 +67,8 @@ int check_io(const dcd_inputs *in, const dcd_outputs *out) {
         return DCD_ERR_ALIGN;
     const void *four[] = {in->bias_expert, in->bias_amateur, in->parents, in->tokens,
                           out->accept_len, out->accept_path, out->next_token, out->status,
-                          out->row_argmax, out->row_stats, out->node_stats};
+                          out->row_argmax, out->row_stats, out->node_stats,
+                          out->row_argmax_expert, out->row_kl};
     for (const void *q : four)
         if (q && !aligned(q, 4)) return DCD_ERR_ALIGN;
     return DCD_OK;
@@ -91,8 +92,9 @@ int run(const dcd_problem *p, const dcd_inputs *in, const SampleInputs *smp,
 
     const Inputs I{in->h_expert, in->h_amateur, in->w_expert, in->w_amateur,
                    in->bias_expert, in->bias_amateur, in->parents, in->tokens};
-    const Outputs O{out->accept_len, out->accept_path, out->next_token, out->status,
-                    out->row_argmax, out->row_stats, out->node_stats};
+    const Outputs O{out->accept_len,        out->accept_path, out->next_token, out->status,
+                    out->row_argmax,        out->row_stats,   out->node_stats,
+                    out->row_argmax_expert, out->row_kl};
     hipStream_t st = (hipStream_t)stream;
     if (launch_lmhead(P, I, st) != hipSuccess) return DCD_ERR_HIP;
     if (launch_finish(P, I, O, smp, st) != hipSuccess) return DCD_ERR_HIP;
@@ -185,6 +187,6 @@ const char *dcd_error_string(int code) {
     }
 }
 
-int dcd_abi_version(void) { return 1; }
+int dcd_abi_version(void) { return 2; }
 
 }  // extern "C"

@@ -29,7 +29,7 @@ constexpr int kWideMinRows = 512;                    // rows from which that ker
 // rowinfo slots (floats; the argmax is stored as an int bit pattern)
 enum {
     RI_MAXP = 0, RI_LSEP, RI_LSEQ, RI_LOGZ, RI_TOP1, RI_MARGIN, RI_COUNT, RI_SIGNAL,
-    RI_THRESH = 8, RI_ARGMAX = 9
+    RI_THRESH = 8, RI_ARGMAX = 9, RI_ARGMAX_P = 10, RI_KL_PQ = 11, RI_KL_PCD = 12
 };
 
 enum ElemType { kF32 = 0, kBF16 = 1 };
@@ -57,7 +57,8 @@ struct Plan {
     float *zq_full;    // [R][zstride]  amateur logits (divided by T)
     float4 *ypart;     // [R][ntiles][2] per tile, over y = (1+s) z_p - s z_q:
                        //   (max y, sum exp(y - max y), second-best y, sum exp(z_p - max_p)(z_p - z_q))
-                       //   (argmax bits, z_p and z_q at the argmax, -)
+                       //   (argmax bits, z_p and z_q at the argmax, bits of the lowest
+                       //    token whose z_p is the tile's expert max)
     float *rowinfo;    // [R][kRowInfo]
     int *tcount;       // [R][ntiles]   candidates per (row, tile); bitmap words valid where > 0
     int *bound;        // [R]           running lower bound on max z_p (order-preserving int key)
@@ -74,6 +75,8 @@ struct Inputs {
 struct Outputs {
     int32_t *accept_len, *accept_path, *next_token, *status, *row_argmax;
     float *row_stats, *node_stats;
+    int32_t *row_argmax_p;  // argmax of pi_p per row
+    float *row_kl;          // [R][2] D_KL(pi_p||pi_q), D_KL(pi_p||pi_CD)
 };
 
 struct SampleInputs {
@@ -99,6 +102,7 @@ struct YStat {
     float ys;   // sum of exp(y - y1)
     float zp1, zq1;  // z_p, z_q at i1
     float a;    // sum of exp(z_p - tile max_p) * (z_p - z_q)
+    int ip;     // lowest token whose z_p equals the tile's expert max (-1: none seen)
 };
 
 __device__ __forceinline__ YStat ystat_merge(const YStat &u, const YStat &v) {
@@ -110,6 +114,7 @@ __device__ __forceinline__ YStat ystat_merge(const YStat &u, const YStat &v) {
         r.ys = w.ys + l.ys * __builtin_amdgcn_exp2f((l.y1 - w.y1) * 1.4426950408889634f);
     }
     r.a = u.a + v.a;
+    r.ip = (int)min((unsigned)u.ip, (unsigned)v.ip);  // -1 (none) is the largest unsigned
     return r;
 }
 

@@ -323,7 +323,7 @@ __device__ __forceinline__ void tile_softmax(const f32x4 (&acc)[VB][RB], const f
 
 __device__ __forceinline__ YStat ystat_shfl_xor(const YStat &x, int m) {
     return YStat{__shfl_xor(x.y1, m), __shfl_xor(x.i1, m), __shfl_xor(x.y2, m), __shfl_xor(x.ys, m),
-                 __shfl_xor(x.zp1, m), __shfl_xor(x.zq1, m), __shfl_xor(x.a, m)};
+                 __shfl_xor(x.zp1, m), __shfl_xor(x.zq1, m), __shfl_xor(x.a, m), __shfl_xor(x.ip, m)};
 }
 
 constexpr int kHTiles = 2;  // hidden-state tiles in LDS
@@ -479,7 +479,7 @@ __device__ __forceinline__ void tile_body(const Plan &P, const Inputs &in, int t
         YStat *ys_lds = reinterpret_cast<YStat *>(lds);  // [NW][64], over the idle hidden-state tiles
 #pragma unroll
         for (int rb = 0; rb < RB; ++rb) {
-            YStat st{-INFINITY, -1, -INFINITY, 0.f, 0.f, 0.f, 0.f};
+            YStat st{-INFINITY, -1, -INFINITY, 0.f, 0.f, 0.f, 0.f, -1};
             float y[VB][4];
 #pragma unroll
             for (int vb = 0; vb < VB; ++vb)
@@ -490,6 +490,8 @@ __device__ __forceinline__ void tile_body(const Plan &P, const Inputs &in, int t
                     const float p = zp[vb][rb][j], q = z[vb][rb][j];
                     y[vb][j] = ok ? s1 * p - P.s * q : -INFINITY;
                     st.a += ok ? __builtin_amdgcn_exp2f((p - pmax[rb]) * kLog2e) * (p - q) : 0.f;
+                    // the expert's own top-1: the lowest token holding the tile max
+                    st.ip = (ok && st.ip < 0 && p == pmax[rb]) ? t : st.ip;
                     if (ok && y[vb][j] > st.y1) {
                         st.y2 = st.y1;
                         st.y1 = y[vb][j];
@@ -522,7 +524,7 @@ __device__ __forceinline__ void tile_body(const Plan &P, const Inputs &in, int t
                 if (row >= P.R) continue;
                 float4 *dst = P.ypart + ((size_t)row * P.ntiles + tile) * 2;
                 dst[0] = float4{st.y1, st.ys, st.y2, st.a};
-                dst[1] = float4{__int_as_float(st.i1), st.zp1, st.zq1, 0.f};
+                dst[1] = float4{__int_as_float(st.i1), st.zp1, st.zq1, __int_as_float(st.ip)};
             }
         }
     } else {

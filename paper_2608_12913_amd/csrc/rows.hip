@@ -36,6 +36,29 @@ __device__ __forceinline__ Lse lse_merge(Lse a, Lse b) {
     return Lse{m, a.s * __expf(a.m - m) + b.s * __expf(b.m - m)};
 }
 
+// log-sum-exp with a weighted sum alongside: value = m + log(s), and
+// sum_x exp(z_x - m) w_x = a (rescaled with s)
+struct LseW {
+    float m, s, a;
+};
+
+__device__ __forceinline__ LseW lsew_merge(LseW x, LseW y) {
+    if (x.m == -INFINITY) return y;
+    if (y.m == -INFINITY) return x;
+    const float m = fmaxf(x.m, y.m), fx = __expf(x.m - m), fy = __expf(y.m - m);
+    return LseW{m, x.s * fx + y.s * fy, x.a * fx + y.a * fy};
+}
+
+// largest value with the lowest id on ties (-1 = none, ordered last)
+struct Best {
+    float v;
+    int id;
+};
+
+__device__ __forceinline__ Best best_merge(Best x, Best y) {
+    return (x.v > y.v || (x.v == y.v && (unsigned)x.id < (unsigned)y.id)) ? x : y;
+}
+
 struct Top2 {  // best value and id, runner-up value
     float v;
     int id;
@@ -63,6 +86,28 @@ __device__ __forceinline__ Top2 wave_top2(Top2 x) {
     for (int d = kWaveSize / 2; d > 0; d >>= 1)
         x = top2_merge(x, Top2{__shfl_down(x.v, d, kWaveSize), __shfl_down(x.id, d, kWaveSize),
                                __shfl_down(x.v2, d, kWaveSize)});
+    return x;
+}
+
+__device__ __forceinline__ LseW wave_lsew(LseW x) {
+#pragma unroll
+    for (int d = kWaveSize / 2; d > 0; d >>= 1)
+        x = lsew_merge(x, LseW{__shfl_down(x.m, d, kWaveSize), __shfl_down(x.s, d, kWaveSize),
+                               __shfl_down(x.a, d, kWaveSize)});
+    return x;
+}
+
+__device__ __forceinline__ Best wave_best(Best x) {
+#pragma unroll
+    for (int d = kWaveSize / 2; d > 0; d >>= 1)
+        x = best_merge(x, Best{__shfl_down(x.v, d, kWaveSize), __shfl_down(x.id, d, kWaveSize)});
+    return x;
+}
+
+__device__ __forceinline__ int wave_min_unsigned(int x) {
+#pragma unroll
+    for (int d = kWaveSize / 2; d > 0; d >>= 1)
+        x = (int)min((unsigned)x, (unsigned)__shfl_down(x, d, kWaveSize));
     return x;
 }
 
@@ -160,27 +205,37 @@ struct Smem {
 
 // Writes a row's results: rowinfo (for the sequence phase) and the optional outputs.
 __device__ __forceinline__ void write_row(const Plan &P, int row, const float (&ri)[kRowInfo],
-                                          int32_t *row_argmax, float *row_stats) {
+                                          const Outputs &out) {
     float4 *dst = reinterpret_cast<float4 *>(P.rowinfo + (size_t)row * kRowInfo);
 #pragma unroll
     for (int k = 0; k < kRowInfo / 4; ++k) dst[k] = float4{ri[4 * k], ri[4 * k + 1], ri[4 * k + 2], ri[4 * k + 3]};
-    if (row_argmax) row_argmax[row] = __float_as_int(ri[RI_ARGMAX]);
-    if (row_stats) {
+    if (out.row_argmax) out.row_argmax[row] = __float_as_int(ri[RI_ARGMAX]);
+    if (out.row_stats) {
 #pragma unroll
-        for (int k = 0; k < 8; ++k) row_stats[(size_t)row * 8 + k] = ri[k];
+        for (int k = 0; k < 8; ++k) out.row_stats[(size_t)row * 8 + k] = ri[k];
+    }
+    if (out.row_argmax_p) out.row_argmax_p[row] = __float_as_int(ri[RI_ARGMAX_P]);
+    if (out.row_kl) {
+        out.row_kl[(size_t)row * 2] = ri[RI_KL_PQ];
+        out.row_kl[(size_t)row * 2 + 1] = ri[RI_KL_PCD];
     }
 }
 
 // Row statistics of the untruncated target (wave 0): the two models' normalisers
 // from the per-tile (max, sum exp) pairs and the statistics of
 // y = (1+s) z_p - s z_q from the per-tile y statistics, both fetched in one round;
-// cd = y - (1+s) lse_p + s lse_q over the whole vocabulary.
-__device__ void row_stats_full(const Plan &P, int row, int lane, int32_t *row_argmax,
-                               float *row_stats) {
+// cd = y - (1+s) lse_p + s lse_q over the whole vocabulary.  Alongside: the
+// expert's top-1 (the first tile holding max z_p, and that tile's lowest token at
+// its max) and D_KL(pi_p || pi_q) = sum_x pi_p (z_p - z_q) - lse_p + lse_q, whose sum
+// is merged like the expert's sum of exp (per tile: sum exp(z_p - tile max)(z_p - z_q));
+// D_KL(pi_p || pi_CD) = log Z - s D_KL(pi_p || pi_q) by the KL-decomposition lemma.
+__device__ void row_stats_full(const Plan &P, int row, int lane, const Outputs &out) {
     const float4 *pr = P.partials + (size_t)row * P.ntiles;
     const float4 *yp = P.ypart + (size_t)row * P.ntiles * 2;
-    Lse lp{-INFINITY, 0.f}, lq{-INFINITY, 0.f};
-    YStat st{-INFINITY, -1, -INFINITY, 0.f, 0.f, 0.f, 0.f};
+    LseW lp{-INFINITY, 0.f, 0.f};
+    Lse lq{-INFINITY, 0.f};
+    Best top_p{-INFINITY, -1};
+    YStat st{-INFINITY, -1, -INFINITY, 0.f, 0.f, 0.f, 0.f, -1};
     for (int base = 0; base < P.ntiles; base += kPass) {
         float4 v[kTilesPerLane], u[kTilesPerLane], w2[kTilesPerLane];
 #pragma unroll
@@ -193,19 +248,22 @@ __device__ void row_stats_full(const Plan &P, int row, int lane, int32_t *row_ar
 #pragma unroll
         for (int k = 0; k < kTilesPerLane; ++k) {
             if (base + lane + k * kWaveSize >= P.ntiles) continue;
-            lp = lse_merge(lp, Lse{v[k].x, v[k].y});
+            lp = lsew_merge(lp, LseW{v[k].x, v[k].y, u[k].w});
             lq = lse_merge(lq, Lse{v[k].z, v[k].w});
-            st = ystat_merge(st, YStat{u[k].x, __float_as_int(w2[k].x), u[k].z, u[k].y, w2[k].y, w2[k].z, 0.f});
+            top_p = best_merge(top_p, Best{v[k].x, __float_as_int(w2[k].w)});
+            st = ystat_merge(st, YStat{u[k].x, __float_as_int(w2[k].x), u[k].z, u[k].y, w2[k].y, w2[k].z,
+                                       0.f, -1});
         }
     }
-    lp = wave_lse(lp);
+    lp = wave_lsew(lp);
     lq = wave_lse(lq);
+    top_p = wave_best(top_p);
 #pragma unroll
     for (int d = kWaveSize / 2; d > 0; d >>= 1)
         st = ystat_merge(st, YStat{__shfl_down(st.y1, d, kWaveSize), __shfl_down(st.i1, d, kWaveSize),
                                    __shfl_down(st.y2, d, kWaveSize), __shfl_down(st.ys, d, kWaveSize),
                                    __shfl_down(st.zp1, d, kWaveSize), __shfl_down(st.zq1, d, kWaveSize),
-                                   0.f});
+                                   0.f, -1});
     if (lane != 0) return;
     const float max_p = lp.m, lse_p = lp.m + __logf(lp.s), lse_q = lq.m + __logf(lq.s);
     const float shift = -(1.f + P.s) * lse_p + P.s * lse_q;  // cd - y
@@ -220,14 +278,19 @@ __device__ void row_stats_full(const Plan &P, int row, int lane, int32_t *row_ar
     ri[RI_SIGNAL] = st.i1 >= 0 ? (st.zp1 - lse_p) - (st.zq1 - lse_q) : NAN;
     ri[RI_THRESH] = max_p + P.log_theta;  // -inf: no mask
     ri[RI_ARGMAX] = __int_as_float(st.i1);
-    write_row(P, row, ri, row_argmax, row_stats);
+    ri[RI_ARGMAX_P] = __int_as_float(top_p.id);
+    const float kl_pq = lp.a / lp.s - lse_p + lse_q;
+    ri[RI_KL_PQ] = kl_pq;
+    ri[RI_KL_PCD] = ri[RI_LOGZ] - P.s * kl_pq;
+    write_row(P, row, ri, out);
 }
 
 // ---------------------------------------------------------------------------
 // Row phase.  wave 0: the row's statistics; wave 1: the row as a draft node.
 template <int DT>
-__device__ void combine_row(const Plan &P, const Inputs &in, int row, int lane, int wave,
-                            int32_t *row_argmax, float *row_stats, bool want_node_logits, int *list) {
+__device__ void combine_row(const Plan &P, const Inputs &in, const Outputs &out, int row, int lane,
+                            int wave, int *list) {
+    const bool want_node_logits = out.node_stats != nullptr;
     if (wave == 1) {
         // this row's draft token under the parent row: from the parent's
         // candidates when the token is one (the numbers the mask saw), otherwise
@@ -278,7 +341,7 @@ __device__ void combine_row(const Plan &P, const Inputs &in, int row, int lane, 
     }
     if (wave != 0) return;
     if (P.full) {
-        row_stats_full(P, row, lane, row_argmax, row_stats);
+        row_stats_full(P, row, lane, out);
         return;
     }
 
@@ -353,6 +416,7 @@ __device__ void combine_row(const Plan &P, const Inputs &in, int row, int lane, 
     Lse lc{-INFINITY, 0.f};
     Top2 best{-INFINITY, -1, -INFINITY};
     int count = 0;
+    int top_p = -1;  // the expert's top-1: the lowest candidate whose z_p is max_p
     for (int base = 0; base < P.ntiles; base += kPass) {
         if (base > 0) issue_cands(base);
         mask_cands(base);
@@ -375,6 +439,7 @@ __device__ void combine_row(const Plan &P, const Inputs &in, int row, int lane, 
                 const float2 c = cz[t];
                 if (!(c.x >= thr)) continue;
                 ++count;
+                top_p = c.x == max_p ? (int)min((unsigned)top_p, (unsigned)t) : top_p;
                 const float cd = (1.f + s) * (c.x - lse_p) - s * (c.y - lse_q);
                 best = top2_merge(best, Top2{cd, t, -INFINITY});
                 lc = lse_merge(lc, Lse{cd, 1.f});
@@ -385,6 +450,7 @@ __device__ void combine_row(const Plan &P, const Inputs &in, int row, int lane, 
     lc = wave_lse(lc);
     best = wave_top2(best);
     count = wave_sum(count);
+    top_p = wave_min_unsigned(top_p);
 
     if (lane == 0) {
         const float logZ = lc.m + __logf(lc.s);
@@ -404,7 +470,13 @@ __device__ void combine_row(const Plan &P, const Inputs &in, int row, int lane, 
         ri[RI_SIGNAL] = signal;
         ri[RI_THRESH] = thr;
         ri[RI_ARGMAX] = __int_as_float(best.id);
-        write_row(P, row, ri, row_argmax, row_stats);
+        ri[RI_ARGMAX_P] = __int_as_float(top_p);
+        // the divergences need every token's logits of both models, which only the
+        // untruncated target keeps; with tokens outside the mask pi_p has mass
+        // where pi_CD = 0
+        ri[RI_KL_PQ] = NAN;
+        ri[RI_KL_PCD] = count < P.V ? INFINITY : NAN;
+        write_row(P, row, ri, out);
     }
 }
 
@@ -757,8 +829,7 @@ __global__ __launch_bounds__(NT) void finish_kernel(Plan P, Inputs in, Outputs o
     __shared__ int last;
     extern __shared__ int dyn[];
     const int row = blockIdx.x, tid = threadIdx.x;
-    combine_row<DT>(P, in, row, tid % kWaveSize, tid / kWaveSize, out.row_argmax, out.row_stats,
-                    out.node_stats != nullptr, sm.list);
+    combine_row<DT>(P, in, out, row, tid % kWaveSize, tid / kWaveSize, sm.list);
     // count the row once both of its waves are done; the release half of the
     // atomic publishes wave 0's results, wave 1 released its own
     __syncthreads();

@@ -44,7 +44,8 @@ class Inputs(ctypes.Structure):
 
 class Outputs(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in ("accept_len", "accept_path", "next_token", "status",
-                                                "row_argmax", "row_stats", "node_stats")]
+                                                "row_argmax", "row_stats", "node_stats",
+                                                "row_argmax_expert", "row_kl")]
 
 
 _lib = None
@@ -112,9 +113,9 @@ def make_inputs(h_expert, h_amateur, w_expert, w_amateur, bias_expert, bias_amat
 
 
 def make_outputs(accept_len, accept_path, next_token, status, row_argmax=None, row_stats=None,
-                 node_stats=None) -> Outputs:
+                 node_stats=None, row_argmax_expert=None, row_kl=None) -> Outputs:
     return Outputs(*(ptr(a) for a in (accept_len, accept_path, next_token, status, row_argmax,
-                                      row_stats, node_stats)))
+                                      row_stats, node_stats, row_argmax_expert, row_kl)))
 
 
 def workspace_bytes(problem: Problem) -> int:

@@ -47,6 +47,8 @@ class DeviceProblem:
         self.row_argmax = torch.empty(R, **i32) if row_outputs else None
         self.row_stats = torch.empty(R, 8, **f32) if row_outputs else None
         self.node_stats = torch.empty(R, 6, **f32) if row_outputs else None
+        self.row_argmax_expert = torch.empty(R, **i32) if row_outputs else None
+        self.row_kl = torch.empty(R, 2, **f32) if row_outputs else None
         self.ws_bytes = dcd.workspace_bytes(self.problem)
         if self.ws_bytes == 0:
             raise dcd.DcdError(dcd.DCD_ERR_SHAPE)
@@ -55,7 +57,7 @@ class DeviceProblem:
                                       self.parents, self.tokens)
         self.outputs = dcd.make_outputs(self.accept_len, self.accept_path, self.next_token,
                                         self.status, self.row_argmax, self.row_stats,
-                                        self.node_stats)
+                                        self.node_stats, self.row_argmax_expert, self.row_kl)
 
     @classmethod
     def from_case(cls, case, tokens, draft_probs=None, device="cuda:0", row_outputs=True,
@@ -99,5 +101,7 @@ class DeviceProblem:
         if self.row_argmax is not None:
             out.update(row_argmax=self.row_argmax.cpu().numpy(),
                        row_stats=self.row_stats.cpu().numpy(),
-                       node_stats=self.node_stats.cpu().numpy())
+                       node_stats=self.node_stats.cpu().numpy(),
+                       row_argmax_expert=self.row_argmax_expert.cpu().numpy(),
+                       row_kl=self.row_kl.cpu().numpy())
         return out

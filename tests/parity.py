@@ -55,6 +55,35 @@ def compare_rows(g, o, rows, report):
     return amb
 
 
+def compare_diagnostics(g, o, rows, theta, s, V, report):
+    """Per-row diagnostics of GPU rows `rows` against the oracle's (same order): the
+    expert's top-1 exactly where the oracle's top-2 expert-logit gap exceeds
+    MARGIN_GATE; with the untruncated target (theta = 0) D_KL(pi_p||pi_q) within
+    ATOL and D_KL(pi_p||pi_CD) = log Z - s D_KL(pi_p||pi_q) within (1+s) ATOL (its
+    error is log Z's plus s times the other's); with a mask the divergences are not
+    computed (NaN) except D_KL(pi_p||pi_CD) = +inf when the mask leaves out a token."""
+    od = o["row_diag"] if "row_diag" in o else o["diag"]
+    ostats = o["row_stats"] if "row_stats" in o else o["stats"]
+    ga = g["row_argmax_expert"][rows]
+    gk = g["row_kl"][rows].astype(np.float64)
+    key = [oracle.RS_MAXP, oracle.RS_LSEP, oracle.RS_LSEQ, oracle.RS_LOGZ]
+    fin = np.all(np.isfinite(ostats[:, key]), axis=1)
+    clear = fin & (od[:, oracle.RD_MARGIN_P] > MARGIN_GATE)
+    bad = np.flatnonzero(clear & (ga != od[:, oracle.RD_ARGMAX_P]))
+    assert len(bad) == 0, f"expert top-1 differs on rows {np.asarray(rows)[bad][:8]}"
+    if theta == 0.0:
+        d = np.abs(gk[fin, 0] - od[fin, oracle.RD_KL_PQ])
+        assert np.all(d <= ATOL), f"KL(p||q): max diff {d.max()}"
+        d = np.abs(gk[fin, 1] - od[fin, oracle.RD_KL_PCD])
+        assert np.all(d <= (1 + s) * ATOL), f"KL(p||cd): max diff {d.max()}"
+    else:
+        assert np.all(np.isnan(gk[:, 0]))
+        partial = g["row_stats"][rows, oracle.RS_COUNT] < V
+        assert np.all(np.isposinf(gk[partial, 1])) and np.all(np.isnan(gk[~partial, 1]))
+        assert np.all(np.isposinf(od[fin & partial, oracle.RD_KL_PCD]))
+    report["diag_rows"] = report.get("diag_rows", 0) + int(clear.sum())
+
+
 def compare_nodes(g, o, parents, amb, report):
     """Draft-token statistics of every node whose parent row is unambiguous."""
     B, N = parents.shape

@@ -24,7 +24,32 @@ def test_library_exports_every_declared_function():
     L = dcd.lib()
     for n in names:
         assert hasattr(L, n), n
-    assert L.dcd_abi_version() == 1
+    assert L.dcd_abi_version() == 2
+
+
+def test_struct_layouts_match_the_header(tmp_path):
+    """The ctypes structs of the binding have the header's sizes and field offsets
+    (a C program built with the header against the same names)."""
+    import subprocess
+    structs = {"dcd_problem": dcd.Problem, "dcd_inputs": dcd.Inputs, "dcd_outputs": dcd.Outputs}
+    lines = ["#include <stdio.h>", "#include <stddef.h>", '#include "dcd.h"', "int main(void) {"]
+    for cname, py in structs.items():
+        lines.append(f'printf("{cname} size %zu\\n", sizeof({cname}));')
+        for f, _ in py._fields_:
+            lines.append(f'printf("{cname} {f} %zu\\n", offsetof({cname}, {f}));')
+    lines += ["return 0;", "}"]
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines) + "\n")
+    exe = tmp_path / "layout"
+    subprocess.check_call(["gcc", "-std=c11", "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe)])
+    got = {}
+    for line in subprocess.check_output([str(exe)], text=True).splitlines():
+        cname, field, val = line.split()
+        got[(cname, field)] = int(val)
+    for cname, py in structs.items():
+        assert got[(cname, "size")] == ctypes.sizeof(py), cname
+        for f, _ in py._fields_:
+            assert got[(cname, f)] == getattr(py, f).offset, (cname, f)
 
 
 def test_error_strings():

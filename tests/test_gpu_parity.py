@@ -50,6 +50,8 @@ def _check_greedy(case, tokens, label, **kw):
     g = dp.run("greedy")
     report = {}
     amb = parity.compare_rows(g, o, np.arange(case.R), report)
+    parity.compare_diagnostics(g, o, np.arange(case.R), kw.get("theta", case.theta),
+                               kw.get("s", case.s), case.V, report)
     parity.compare_nodes(g, o, case.parents, amb, report)
     parity.compare_greedy(g, o, case.parents, amb, report)
     parity.check_walk_consistent(g, case.parents, tokens)
@@ -118,8 +120,9 @@ def test_flat_logits_every_token_in_mask():
     case.bias[:] = 0
     tokens = _greedy_tokens(case)
     g, o, _ = _check_greedy(case, tokens, "flat logits")
-    assert np.all(g["row_argmax"] == 0)
+    assert np.all(g["row_argmax"] == 0) and np.all(g["row_argmax_expert"] == 0)
     assert np.all(g["row_stats"][:, oracle.RS_COUNT] == 1500)
+    assert np.all(np.isnan(g["row_kl"]))  # the mask holds every token: not computed
     np.testing.assert_allclose(g["row_stats"][:, oracle.RS_LOGZ], o["row_stats"][:, oracle.RS_LOGZ],
                                atol=1e-4)
 
@@ -144,6 +147,34 @@ def test_exact_integer_logits_theta_one():
     assert np.array_equal(g["accept_path"], o["accept_path"])
     np.testing.assert_allclose(g["row_stats"][:, oracle.RS_MAXP], o["row_stats"][:, oracle.RS_MAXP],
                                rtol=0, atol=0)
+    # the expert's top-1 among the tied tokens: the lowest id, exactly
+    assert np.array_equal(g["row_argmax_expert"], o["row_diag"][:, oracle.RD_ARGMAX_P])
+
+
+def test_exact_integer_logits_untruncated_expert_top1():
+    """theta = 0 with exact integer logits: many tokens tie at the expert max across
+    vocabulary tiles; the expert's top-1 is the lowest of them, merged over tiles."""
+    rng = np.random.default_rng(14)
+    V = 4099
+    case = synth.make_case("b8_tree64", 14, N=16, depth=4, max_children=4, V=V, dp=128, dq=64,
+                           theta=0.0)
+    for name, d in (("hp", 128), ("hq", 64)):
+        setattr(case, name, synth.bf16_bits(rng.integers(-1, 2, (case.R, d)).astype(np.float32)))
+    case.wp = synth.bf16_bits(rng.integers(-1, 2, (V, 128)).astype(np.float32))
+    case.wq = synth.bf16_bits(rng.integers(-1, 2, (V, 64)).astype(np.float32))
+    case.bias[:] = 0
+    tokens = _greedy_tokens(case)
+    _say("exact integer logits, theta 0")
+    o = _oracle_greedy(case, tokens)
+    g = _runner().from_case(case, tokens).run("greedy")
+    zp = oracle.eval_rows(case.hp, case.hq, case.wp, case.wq, case.bias, case.bias, theta=0.0,
+                          s=case.s, want_logits=True)["zp"]
+    cross = sum(len(set(np.flatnonzero(z == z.max()) // 256)) > 1 for z in zp)
+    assert cross >= 4, "the case must tie the expert max across tiles"
+    assert np.array_equal(g["row_argmax_expert"], o["row_diag"][:, oracle.RD_ARGMAX_P])
+    np.testing.assert_allclose(g["row_kl"][:, 0], o["row_diag"][:, oracle.RD_KL_PQ], atol=parity.ATOL)
+    np.testing.assert_allclose(g["row_kl"][:, 1], o["row_diag"][:, oracle.RD_KL_PCD],
+                               atol=(1 + case.s) * parity.ATOL)
 
 
 def test_duplicate_sibling_tokens():
@@ -192,6 +223,7 @@ def _check_sample(case, probs, tokens, label, seqs=None):
     g = _runner().from_case(case, tokens, draft_probs=probs).run("sample")
     report = {}
     amb = parity.compare_rows(g, o, np.arange(case.R), report)
+    parity.compare_diagnostics(g, o, np.arange(case.R), case.theta, case.s, case.V, report)
     parity.compare_nodes(g, o, case.parents, amb, report)
     boundary = o["row_gap"] <= parity.BOUNDARY_GATE
     parity.compare_sample(g, o, case, tokens, probs, boundary, report, seqs)
@@ -316,9 +348,11 @@ def test_full_s8_chain16x8(theta):
     sel = dict(accept_len=g["accept_len"][seqs], accept_path=g["accept_path"][seqs],
                next_token=g["next_token"][seqs], status=g["status"][seqs],
                row_argmax=g["row_argmax"][rows], row_stats=g["row_stats"][rows],
-               node_stats=g["node_stats"][rows])
+               node_stats=g["node_stats"][rows], row_argmax_expert=g["row_argmax_expert"][rows],
+               row_kl=g["row_kl"][rows])
     report = {}
     amb = parity.compare_rows(sel, o, np.arange(len(rows)), report)
+    parity.compare_diagnostics(sel, o, np.arange(len(rows)), case.theta, case.s, case.V, report)
     parity.compare_nodes(sel, o, case.parents[seqs], amb, report)
 
     class _Sub:
@@ -349,9 +383,11 @@ def test_full_b8_batch32x64():
     sel = dict(accept_len=g["accept_len"][seqs], accept_path=g["accept_path"][seqs],
                next_token=g["next_token"][seqs], status=g["status"][seqs],
                row_argmax=g["row_argmax"][rows], row_stats=g["row_stats"][rows],
-               node_stats=g["node_stats"][rows])
+               node_stats=g["node_stats"][rows], row_argmax_expert=g["row_argmax_expert"][rows],
+               row_kl=g["row_kl"][rows])
     report = {}
     amb = parity.compare_rows(sel, o, np.arange(len(rows)), report)
+    parity.compare_diagnostics(sel, o, np.arange(len(rows)), case.theta, case.s, case.V, report)
     parity.compare_nodes(sel, o, case.parents[seqs], amb, report)
     parity.compare_greedy(sel, o, case.parents[seqs], amb, report)
     parity.check_walk_consistent(g, case.parents, tokens)
@@ -360,4 +396,5 @@ def test_full_b8_batch32x64():
     o_spot = oracle.eval_rows(case.hp, case.hq, case.wp, case.wq, case.bias, case.bias,
                               theta=case.theta, s=case.s, rows=spot)
     parity.compare_rows(g, o_spot, spot, report)
+    parity.compare_diagnostics(g, o_spot, spot, case.theta, case.s, case.V, report)
     _say(f"b8_batch32x64: ok {report}")
