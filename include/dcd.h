@@ -99,7 +99,7 @@ enum {
 };
 /*
  * row_kl slots (2 floats per row): the divergences of the KL-decomposition lemma
- * (appendix on distribution alignment), per row and over the whole vocabulary.
+ * (App. B.1), per row and over the whole vocabulary.
  *   DCD_KL_P_Q   D_KL(pi_p || pi_q)
  *   DCD_KL_P_CD  D_KL(pi_p || pi_CD) = log Z_CD - s * D_KL(pi_p || pi_q) (the lemma)
  * Both need both models' logits at every token, which only the untruncated target
@@ -142,8 +142,8 @@ typedef struct {                 /* device pointers, written by the call        
                                     ties go to the lowest token id                        */
     float *row_stats;            /* [B*N, 8] optional: DCD_ROW_* slots                    */
     float *node_stats;           /* [B*N, 6] optional: DCD_NODE_* slots                   */
-    /* diagnostics of Sec. 3.2 (signal and top-1 agreement at x* = argmax pi_CD; the
-       signal itself is DCD_ROW_SIGNAL) and of the appendix's KL lemma             */
+    /* diagnostics of Sec. 3.1 (signal and top-1 agreement at x* = argmax pi_CD; the
+       signal itself is DCD_ROW_SIGNAL) and of the KL lemma of App. B.1        */
     int32_t *row_argmax_expert;  /* [B*N] optional: argmax of pi_p, the expert's own greedy
                                     token (lowest id on ties); top-1 agreement with the
                                     target is row_argmax_expert == row_argmax          */

@@ -23,8 +23,8 @@
  *                       applied before renormalising (Appendix remark
  *                       "Plausibility-constrained CD").  s is the contrastive
  *                       strength, theta the plausibility cutoff.
- *   row_diag            diagnostics of Sec. 3.2 and of the KL-decomposition lemma
- *                       (appendix on distribution alignment): the expert's own
+ *   row_diag            diagnostics of Sec. 3.1 and of the KL-decomposition lemma
+ *                       (App. B.1): the expert's own
  *                       top-1 token, D_KL(pi_p || pi_q) and D_KL(pi_p || pi_CD),
  *                       each summed from its definition.
  *   dco_greedy_walk     greedy (T = 0) verification of a draft tree: a draft
