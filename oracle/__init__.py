@@ -57,10 +57,10 @@ def _load():
         lib.dco_eval_rows.restype = i32
         lib.dco_greedy_walk.argtypes = [i32, P, P, P, P, P, P]
         lib.dco_greedy_walk.restype = None
-        lib.dco_sample_chain.argtypes = [i32, i32, P, P, P, P, P, P, P, P, P, P]
-        lib.dco_sample_chain.restype = None
+        lib.dco_sample_tree.argtypes = [i32, i32, P, P, P, P, P, P, P, P, P, P, P, P]
+        lib.dco_sample_tree.restype = None
         lib.dco_verify.argtypes = [i32, i32, i32, i32, i32, i32, P, P, P, P, P, P, P, P,
-                                   f64, f64, f64, P, P, P, P, P, P, P, P, P, P, P, P, P, i32]
+                                   f64, f64, f64, P, P, P, P, P, P, P, P, P, P, P, P, P, P, i32]
         lib.dco_verify.restype = i32
         _lib = lib
     return _lib
@@ -124,9 +124,9 @@ def greedy_walk(parents, tokens, row_argmax):
     return int(L[0]), path, int(nxt[0])
 
 
-def sample_chain(tokens, lp_cd, draft_probs, u_acc, u_res):
-    """Alg. 1 accept/residual/bonus over one chain, given log pi_CD rows [N, V]."""
-    tokens = _c(tokens, np.int32)
+def sample_tree(parents, tokens, lp_cd, draft_probs, u_acc, u_res):
+    """Alg. 1 accept/residual/bonus over one draft tree, given log pi_CD rows [N, V]."""
+    parents, tokens = _c(parents, np.int32), _c(tokens, np.int32)
     lp_cd = _c(lp_cd, np.float64)
     q = _c(draft_probs, np.float32)
     u_acc, u_res = _c(u_acc, np.float32), _c(u_res, np.float32)
@@ -135,11 +135,18 @@ def sample_chain(tokens, lp_cd, draft_probs, u_acc, u_res):
     path = np.empty(N, np.int32)
     nxt = np.zeros(1, np.int32)
     ratio = np.full(N, np.nan)
+    walk = np.full(N, np.nan)
     gap = np.zeros(1)
-    _load().dco_sample_chain(N, V, _p(tokens), _p(lp_cd), _p(q), _p(u_acc), _p(u_res), _p(L),
-                             _p(path), _p(nxt), _p(ratio), _p(gap))
+    _load().dco_sample_tree(N, V, _p(parents), _p(tokens), _p(lp_cd), _p(q), _p(u_acc), _p(u_res),
+                            _p(L), _p(path), _p(nxt), _p(ratio), _p(walk), _p(gap))
     return dict(accept_len=int(L[0]), path=path, next_token=int(nxt[0]), ratio=ratio,
-                res_gap=float(gap[0]))
+                walk_ratio=walk, res_gap=float(gap[0]))
+
+
+def sample_chain(tokens, lp_cd, draft_probs, u_acc, u_res):
+    """sample_tree on a chain (parents[i] = i - 1)."""
+    N = len(tokens)
+    return sample_tree(np.arange(-1, N - 1), tokens, lp_cd, draft_probs, u_acc, u_res)
 
 
 def verify(mode, B, N, hp, hq, wp, wq, bp, bq, parents, tokens, *, theta, s,
@@ -160,13 +167,14 @@ def verify(mode, B, N, hp, hq, wp, wq, bp, bq, parents, tokens, *, theta, s,
              next_token=np.zeros(B, np.int32), status=np.zeros(B, np.int32),
              row_argmax=np.zeros(R, np.int32), row_stats=np.zeros((R, 8)),
              node_stats=np.zeros((R, 6)), row_diag=np.zeros((R, 4)), row_gap=np.zeros(R),
-             res_gap=np.zeros(B))
+             res_gap=np.zeros(B), walk_ratio=np.zeros(R))
     rc = _load().dco_verify(m, B, N, V, dp, dq, _p(hp), _p(hq), _p(wp), _p(wq), _p(bp), _p(bq),
                             _p(parents), _p(tokens), float(theta), float(s), float(temperature),
                             _p(draft_probs), _p(u_acc), _p(u_res), _p(o["accept_len"]),
                             _p(o["accept_path"]), _p(o["next_token"]), _p(o["status"]),
                             _p(o["row_argmax"]), _p(o["row_stats"]), _p(o["node_stats"]),
-                            _p(o["row_diag"]), _p(o["row_gap"]), _p(o["res_gap"]), int(nthreads))
+                            _p(o["row_diag"]), _p(o["row_gap"]), _p(o["res_gap"]),
+                            _p(o["walk_ratio"]), int(nthreads))
     if rc:
         raise RuntimeError(f"dco_verify failed ({rc})")
     return o

@@ -30,7 +30,12 @@
  *   dco_greedy_walk     greedy (T = 0) verification of a draft tree: a draft
  *                       token is accepted iff it equals the target's argmax
  *                       (Alg. 1 with a one-hot target), walked from the root.
- *   dco_sample_chain    Alg. 1 speculative accept / residual / bonus steps.
+ *   dco_sample_tree     Alg. 1 speculative accept / residual / bonus steps, on a
+ *                       tree: the children of a node are tried in turn, each
+ *                       against the residual left by the siblings rejected before
+ *                       it (multi-draft speculative sampling as in SpecInfer, Miao
+ *                       et al. 2024; the paper runs sampled verification on chains
+ *                       only, where this is exactly Alg. 1).
  *
  * Readings where the paper is silent (all documented with the design notes):
  *   - mask test in log space: z_p - max z_p >= ln(theta); theta = 0 means no mask;
@@ -39,7 +44,8 @@
  *   - accept iff pi_CD(tok) > 0 and u <= pi_CD(tok) / pi_e(tok); pi_e(tok) = 0
  *     gives ratio = +inf;
  *   - "sample" = inverse CDF in token-id order with one uniform; a residual
- *     that sums to zero falls back to pi_CD;
+ *     that sums to zero (rounding only) leaves the distribution as it was;
+ *   - siblings are tried in increasing node index;
  *   - temperature divides both models' logits before everything (sampled mode);
  *     greedy mode uses the models' own distributions (T = 1).
  */
@@ -306,70 +312,89 @@ static double cdf_gap(const double *w, int V, double u)
 }
 
 /*
- * Alg. 1 speculative accept / fallback over one chain of N nodes (parents[i] = i-1).
+ * Alg. 1 speculative accept / fallback over one draft tree of N nodes (parents[i] < i).
  *   lp_cd    [N][V]  log pi_CD of each row (-inf off the mask)
  *   q        [N][V]  node-indexed proposal probabilities: row i is pi_e^(i),
  *                    the distribution draft token i was drawn from (row 0 unused)
  *   u_acc[i] decides node i; u_res[j] draws the token emitted after row j.
- * Node i (i >= 1) is accepted iff pi_CD^(i-1)(tok_i) > 0 and
- * u_acc[i] <= pi_CD^(i-1)(tok_i) / pi_e^(i)(tok_i).  At the first rejection
- * (node k) the emitted token is drawn from Normalize(max(0, pi_CD^(k-1) - pi_e^(k)));
- * if every node is accepted the bonus token is drawn from pi_CD^(N-1).
- * ratio_out[i] receives the acceptance ratio of node i (all i >= 1).
- * Returns through res_gap the relative distance of the final draw to its CDF
- * breakpoints (the parity gate for the emitted token).
+ * The walk starts at the root with p = pi_CD of the current row.  The children
+ * c_1 < c_2 < ... of the current node are tried in index order: c_m (token x,
+ * proposal q_m) is accepted iff p(x) > 0 and u_acc[c_m] <= p(x) / q_m(x), and the walk
+ * moves to it with p = pi_CD of its row; a rejection replaces p by the residual
+ * Normalize(max(0, p - q_m)) (p stays as it was if that sums to zero).  When every
+ * child of the current node is rejected, or it has none, the emitted token is drawn
+ * from p with u_res of the current node.  On a chain (one child per node) this is
+ * Alg. 1: the first rejected node k is replaced by a draw from
+ * Normalize(max(0, pi_CD^(k-1) - pi_e^(k))), and a fully accepted chain gets the
+ * bonus token from pi_CD^(N-1).
+ * ratio_out[i] receives pi_CD(tok_i) / pi_e^(i)(tok_i) under the parent row (all
+ * i >= 1); walk_ratio[i] the ratio node i was actually tested with (its parent's
+ * residual), NaN for nodes the walk never tested.  res_gap receives the relative
+ * distance of the final draw to its CDF breakpoints (the parity gate for the
+ * emitted token).
  */
-void dco_sample_chain(int N, int V, const int32_t *tokens, const double *lp_cd,
-                      const float *q, const float *u_acc, const float *u_res,
-                      int32_t *accept_len, int32_t *path, int32_t *next_token,
-                      double *ratio_out, double *res_gap)
+void dco_sample_tree(int N, int V, const int32_t *parents, const int32_t *tokens,
+                     const double *lp_cd, const float *q, const float *u_acc, const float *u_res,
+                     int32_t *accept_len, int32_t *path, int32_t *next_token, double *ratio_out,
+                     double *walk_ratio, double *res_gap)
 {
+    double *p = (double *)malloc(sizeof(double) * (size_t)V);
     double *w = (double *)malloc(sizeof(double) * (size_t)V);
-    for (int i = 0; i < N; ++i) path[i] = -1;
-    path[0] = 0;
-    int k = N; /* first rejected node; N means none */
-    for (int i = 1; i < N; ++i) {
-        double p_cd = exp(lp_cd[(size_t)(i - 1) * V + tokens[i]]);
-        double p_e = (double)q[(size_t)i * V + tokens[i]];
-        double ratio = p_e > 0.0 ? p_cd / p_e : INFINITY;
-        if (ratio_out) ratio_out[i] = ratio;
-        int accept = p_cd > 0.0 && (double)u_acc[i] <= ratio;
-        if (!accept && k == N) k = i;
+    for (int i = 0; i < N; ++i) {
+        path[i] = -1;
+        if (walk_ratio) walk_ratio[i] = NAN;
+        if (ratio_out) ratio_out[i] = NAN;
     }
-    for (int i = 1; i < k; ++i) path[i] = i;
-    *accept_len = k - 1;
-    int row = k - 1;
-    const double *lrow = lp_cd + (size_t)row * V;
-    if (k < N) {
-        const float *qk = q + (size_t)k * V;
-        double total = 0.0;
-        for (int v = 0; v < V; ++v) {
-            double r = exp(lrow[v]) - (double)qk[v];
-            w[v] = r > 0.0 ? r : 0.0;
-            total += w[v];
+    if (ratio_out)
+        for (int i = 1; i < N; ++i) {
+            double p_cd = exp(lp_cd[(size_t)parents[i] * V + tokens[i]]);
+            double p_e = (double)q[(size_t)i * V + tokens[i]];
+            ratio_out[i] = p_e > 0.0 ? p_cd / p_e : INFINITY;
         }
-        if (!(total > 0.0))
-            for (int v = 0; v < V; ++v) w[v] = exp(lrow[v]);
-    } else {
-        for (int v = 0; v < V; ++v) w[v] = exp(lrow[v]);
+    path[0] = 0;
+    int cur = 0, len = 0;
+    for (;;) {
+        const double *lrow = lp_cd + (size_t)cur * V;
+        for (int v = 0; v < V; ++v) p[v] = exp(lrow[v]);
+        int next = -1;
+        for (int c = cur + 1; c < N && next < 0; ++c) {
+            if (parents[c] != cur) continue;
+            const float *qc = q + (size_t)c * V;
+            const int x = tokens[c];
+            double ratio = qc[x] > 0.0f ? p[x] / (double)qc[x] : INFINITY;
+            if (walk_ratio) walk_ratio[c] = ratio;
+            if (p[x] > 0.0 && (double)u_acc[c] <= ratio) {
+                next = c;
+                break;
+            }
+            double total = 0.0;
+            for (int v = 0; v < V; ++v) {
+                double r = p[v] - (double)qc[v];
+                w[v] = r > 0.0 ? r : 0.0;
+                total += w[v];
+            }
+            if (total > 0.0)
+                for (int v = 0; v < V; ++v) p[v] = w[v] / total;
+        }
+        if (next < 0) break;
+        path[++len] = next;
+        cur = next;
     }
-    *next_token = inverse_cdf(w, V, (double)u_res[row]);
-    if (res_gap) *res_gap = cdf_gap(w, V, (double)u_res[row]);
+    *accept_len = len;
+    *next_token = inverse_cdf(p, V, (double)u_res[cur]);
+    if (res_gap) *res_gap = cdf_gap(p, V, (double)u_res[cur]);
+    free(p);
     free(w);
 }
 
 /* status of one sequence from its tree and tokens (before any numerics) */
-static int check_sequence(int N, int V, const int32_t *parents, const int32_t *tokens,
-                          int need_chain)
+static int check_sequence(int N, int V, const int32_t *parents, const int32_t *tokens)
 {
     if (parents[0] != -1) return SEQ_BAD_TREE;
     for (int i = 1; i < N; ++i)
         if (parents[i] < 0 || parents[i] >= i) return SEQ_BAD_TREE;
     for (int i = 1; i < N; ++i)
         if (tokens[i] < 0 || tokens[i] >= V) return SEQ_BAD_TOKEN;
-    if (need_chain)
-        for (int i = 1; i < N; ++i)
-            if (parents[i] != i - 1) return SEQ_NOT_CHAIN;
     return SEQ_OK;
 }
 
@@ -385,9 +410,10 @@ static void reset_sequence(int N, int32_t *accept_len, int32_t *path, int32_t *n
 
 /*
  * Full verification of B sequences of N nodes each (rows are b*N + i).
- * mode 0 = greedy (temperature ignored), mode 1 = sampled chains.
+ * mode 0 = greedy (temperature ignored), mode 1 = sampled (dco_sample_tree).
  * Optional outputs may be NULL: row_argmax [R], row_stats [R][8], node_stats [R][6],
- * row_diag [R][RD_N], row_gap [R], res_gap [B].
+ * row_diag [R][RD_N], row_gap [R], res_gap [B], walk_ratio [R] (sampled: the ratio
+ * each node was tested with, NaN if untested).
  */
 int dco_verify(int mode, int B, int N, int V, int dp, int dq,
                const float *hp, const float *hq, const float *wp, const float *wq,
@@ -396,7 +422,7 @@ int dco_verify(int mode, int B, int N, int V, int dp, int dq,
                const float *draft_probs, const float *u_acc, const float *u_res,
                int32_t *accept_len, int32_t *accept_path, int32_t *next_token, int32_t *status,
                int32_t *row_argmax, double *row_stats, double *node_stats, double *row_diag,
-               double *row_gap, double *res_gap, int nthreads)
+               double *row_gap, double *res_gap, double *walk_ratio, int nthreads)
 {
     if (B <= 0 || N <= 0 || V <= 0) return -2;
     if (mode == 1 && (!draft_probs || !u_acc || !u_res || !(temperature > 0.0))) return -3;
@@ -424,7 +450,7 @@ int dco_verify(int mode, int B, int N, int V, int dp, int dq,
         const int32_t *par = parents + r0, *tok = tokens + r0;
         int32_t *path = accept_path + r0;
         double *ns = node_stats ? node_stats + (size_t)r0 * NS_N : NULL;
-        int st = check_sequence(N, V, par, tok, mode == 1);
+        int st = check_sequence(N, V, par, tok);
         if (st == SEQ_OK) {
             for (int i = 0; i < N; ++i) {
                 const double *rs = stats + (size_t)(r0 + i) * RS_N;
@@ -436,6 +462,8 @@ int dco_verify(int mode, int B, int N, int V, int dp, int dq,
         status[b] = st;
         if (st != SEQ_OK) {
             reset_sequence(N, accept_len + b, path, next_token + b, ns);
+            if (walk_ratio)
+                for (int i = 0; i < N; ++i) walk_ratio[r0 + i] = NAN;
             if (res_gap) res_gap[b] = INFINITY;
             continue;
         }
@@ -459,11 +487,14 @@ int dco_verify(int mode, int B, int N, int V, int dp, int dq,
         if (mode == 0) {
             dco_greedy_walk(N, par, tok, amax + r0, accept_len + b, path, next_token + b);
             if (res_gap) res_gap[b] = INFINITY;
+            if (walk_ratio)
+                for (int i = 0; i < N; ++i) walk_ratio[r0 + i] = NAN;
         } else {
             double *ratio = (double *)malloc(sizeof(double) * (size_t)N);
             double g = INFINITY;
-            dco_sample_chain(N, V, tok, lp_cd, draft_probs + (size_t)r0 * V, u_acc + r0,
-                             u_res + r0, accept_len + b, path, next_token + b, ratio, &g);
+            dco_sample_tree(N, V, par, tok, lp_cd, draft_probs + (size_t)r0 * V, u_acc + r0,
+                            u_res + r0, accept_len + b, path, next_token + b, ratio,
+                            walk_ratio ? walk_ratio + r0 : NULL, &g);
             if (ns)
                 for (int i = 1; i < N; ++i) ns[i * NS_N + NS_RATIO] = ratio[i];
             if (res_gap) res_gap[b] = g;

@@ -497,11 +497,12 @@ def test_sequence_status_codes():
     hp[4, 0] = np.inf
     o = oracle.verify("greedy", 1, case.N, hp, *args[1:], case.parents, tokens, theta=0.1, s=0.5)
     assert o["status"][0] == oracle.SEQ_NONFINITE
+    # sampled verification takes trees as well as chains
     tree = synth.make_case("tiny_chain8", 0, N=8, tree="tree", depth=3, max_children=3)
     probs = np.full((8, case.V), 1.0 / case.V, np.float32)
     o = oracle.verify("sample", 1, 8, *args, tree.parents, tokens, theta=0.1, s=0.5,
                       draft_probs=probs, u_acc=case.u_acc, u_res=case.u_res)
-    assert o["status"][0] == oracle.SEQ_NOT_CHAIN
+    assert o["status"][0] == oracle.SEQ_OK
 
 
 # ---------------------------------------------------------------- sampled verification
@@ -512,7 +513,7 @@ def _tiny_target(rng, V, theta, s, N):
 
 
 class _ChainCall:
-    """Repeated calls of the oracle's chain sampler on fixed buffers (fast loop)."""
+    """Repeated calls of the oracle's sampler on a chain, on fixed buffers (fast loop)."""
 
     def __init__(self, lp_cd, q):
         import ctypes
@@ -520,6 +521,7 @@ class _ChainCall:
         self.N, self.V = lp_cd.shape
         self.lp = np.ascontiguousarray(lp_cd, np.float64)
         self.q = np.ascontiguousarray(q, np.float32)
+        self.par = np.arange(-1, self.N - 1, dtype=np.int32)
         self.tok = np.zeros(self.N, np.int32)
         self.ua = np.full(self.N, 0.5, np.float32)
         self.ur = np.full(self.N, 0.5, np.float32)
@@ -527,11 +529,11 @@ class _ChainCall:
         self.path = np.zeros(self.N, np.int32)
         self.nxt = np.zeros(1, np.int32)
         p = lambda a: a.ctypes.data_as(ctypes.c_void_p)  # noqa: E731
-        self.args = (self.N, self.V, p(self.tok), p(self.lp), p(self.q), p(self.ua), p(self.ur),
-                     p(self.L), p(self.path), p(self.nxt), None, None)
+        self.args = (self.N, self.V, p(self.par), p(self.tok), p(self.lp), p(self.q), p(self.ua),
+                     p(self.ur), p(self.L), p(self.path), p(self.nxt), None, None, None)
 
     def __call__(self):
-        self.lib.dco_sample_chain(*self.args)
+        self.lib.dco_sample_tree(*self.args)
         return int(self.L[0]), int(self.nxt[0])
 
 
@@ -563,6 +565,86 @@ def test_lossless_theorem_by_enumeration(theta, s):
                     emitted[x if L == 1 else nxt] += pe[x] / (G * G)
         np.testing.assert_allclose(emitted, target, atol=2.0 / G)
         assert np.all(emitted[target == 0] == 0)
+
+
+@pytest.fixture(scope="module")
+def sweep_lib(tmp_path_factory):
+    """The brute-force sweep driver (tests/native/lossless_sweep.c) built against the
+    oracle library."""
+    import ctypes
+    import subprocess
+    lib = oracle.build(force=False)
+    out = tmp_path_factory.mktemp("sweep") / "libsweep.so"
+    src = os.path.join(os.path.dirname(__file__), "native", "lossless_sweep.c")
+    subprocess.check_call(["gcc", "-O2", "-std=c11", "-fPIC", "-shared", src, lib, "-o", str(out),
+                           f"-Wl,-rpath,{os.path.dirname(lib)}"])
+    L = ctypes.CDLL(str(out))
+    P = ctypes.c_void_p
+    L.sweep_star.argtypes = [ctypes.c_int, ctypes.c_int, P, P, ctypes.c_int, P]
+    L.sweep_star.restype = ctypes.c_int
+    return L
+
+
+@pytest.mark.parametrize("K,V,G,theta,s", [(2, 5, 96, 0.0, 0.5), (2, 5, 96, 0.1, 1.0),
+                                           (3, 3, 24, 0.0, 0.5)])
+def test_lossless_theorem_on_trees_by_enumeration(sweep_lib, K, V, G, theta, s):
+    """The lossless property with several drafted children per node: a root with K
+    children drafted independently from different proposals (one of them with a zero
+    entry, one one-hot on the target's least likely token).  Enumerating every token
+    assignment and a midpoint grid of every uniform, the first emitted token is
+    distributed as pi_CD of the root."""
+    rng = np.random.default_rng(30 + K)
+    lp_cd = np.zeros((K + 1, V))
+    lp_cd[0] = _tiny_target(rng, V, theta, s, 1)[0]
+    target = np.exp(lp_cd[0])
+    props = [rng.dirichlet(np.ones(V)), np.r_[0.0, rng.dirichlet(np.ones(V - 1))],
+             np.eye(V)[int(np.argmin(target))]]
+    q = np.zeros((K + 1, V), np.float32)
+    for k in range(K):
+        q[k + 1] = props[k]
+    out = np.zeros(V)
+    P = lambda a: a.ctypes.data_as(__import__("ctypes").c_void_p)  # noqa: E731
+    assert sweep_lib.sweep_star(K, V, P(lp_cd), P(q), G, P(out)) == 0
+    np.testing.assert_allclose(out, target, atol=2.0 / G)
+    assert np.all(out[target == 0] == 0)
+
+
+def test_tree_sampler_hand_worked_example():
+    """Root with two children, V = 2, pi_CD(root) = (1/2, 1/2).  Child 1 is one-hot on
+    token 0 (q_1 = (1, 0)): ratio 1/2, rejected at u = 0.7, leaving the residual
+    max(0, p - q_1) = (0, 1/2) -> (0, 1).  Child 2 (q_2 = (1/2, 1/2)) then carries
+    token 0, with p(0) = 0: rejected whatever u is; the residual is
+    max(0, (0, 1) - (1/2, 1/2)) = (0, 1/2) -> (0, 1), so the draw is token 1.  Carrying
+    token 1 instead, its ratio is 1 / (1/2) = 2 and it is accepted; the bonus is drawn
+    from pi_CD of its own row."""
+    lp = np.log(np.array([[0.5, 0.5], [0.5, 0.5], [0.25, 0.75]]))
+    q = np.array([[0, 0], [1, 0], [0.5, 0.5]], np.float32)
+    par = [-1, 0, 0]
+    o = oracle.sample_tree(par, [0, 0, 0], lp, q, [0.5, 0.7, 0.01], [0.1, 0.5, 0.5])
+    assert o["accept_len"] == 0 and o["next_token"] == 1
+    np.testing.assert_allclose(o["walk_ratio"][1:], [0.5, 0.0])
+    o = oracle.sample_tree(par, [0, 0, 1], lp, q, [0.5, 0.7, 0.99], [0.5, 0.5, 0.2])
+    assert o["accept_len"] == 1 and list(o["path"][:2]) == [0, 2]
+    assert o["next_token"] == 0  # 0.2 < 0.25: the first token of (1/4, 3/4)
+    np.testing.assert_allclose(o["walk_ratio"][1:], [0.5, 2.0])
+    # child 1 accepted (u = 0.3 <= 1/2): child 2 is never tested
+    o = oracle.sample_tree(par, [0, 0, 1], lp, q, [0.5, 0.3, 0.5], [0.5, 0.9, 0.5])
+    assert o["accept_len"] == 1 and o["path"][1] == 1 and o["next_token"] == 1
+    assert np.isnan(o["walk_ratio"][2])
+
+
+def test_tree_walk_descends_after_acceptance():
+    """Depth 2: an accepted child's own children are tested against its row."""
+    lp = np.log(np.array([[0.5, 0.5], [0.9, 0.1], [0.2, 0.8], [0.5, 0.5]]))
+    q = np.array([[0, 0], [0, 1], [1, 0], [0, 1]], np.float32)
+    par = [-1, 0, 1, 0]
+    # node 1 (token 1 under the root: ratio 1/2, u 0.4 -> accept); node 2 (token 0 under
+    # row 1: ratio 0.9, u 0.5 -> accept); node 3 is a sibling of node 1, never tested
+    o = oracle.sample_tree(par, [0, 1, 0, 1], lp, q, [0.5, 0.4, 0.5, 0.01], [0.5, 0.5, 0.3, 0.5])
+    assert o["accept_len"] == 2 and list(o["path"][:3]) == [0, 1, 2]
+    # node 2 is a leaf: the bonus comes from row 2, (0.2, 0.8), at u = 0.3 -> token 1
+    assert o["next_token"] == 1 and np.isnan(o["walk_ratio"][3])
+    np.testing.assert_allclose(o["walk_ratio"][1:3], [0.5, 0.9])
 
 
 def test_proposal_equal_to_target_accepts_everything():
