@@ -12,7 +12,7 @@
  *      and renormalised (Sec. 2.1 and the appendix remark on
  *      plausibility-constrained CD);
  *   3. verifies the draft tokens against pi_CD: greedily (T = 0) by walking the
- *      tree from the root, or by speculative rejection sampling along chains
+ *      tree from the root, or by speculative rejection sampling (chains and trees)
  *      (Alg. 1: accept test, residual resampling, bonus token).
  *
  * Notation: s = cd_strength (the paper's contrastive strength), theta =
@@ -71,7 +71,7 @@ enum {
     DCD_SEQ_BAD_TREE = 1,   /* parents[b,0] != -1 or parents[b,i] outside [0, i) */
     DCD_SEQ_BAD_TOKEN = 2,  /* a draft token (i >= 1) outside [0, vocab) */
     DCD_SEQ_NONFINITE = 3,  /* a row of the sequence has a non-finite max, log-normaliser or log Z */
-    DCD_SEQ_NOT_CHAIN = 4   /* sampled verification needs parents[b,i] = i-1 */
+    DCD_SEQ_NOT_CHAIN = 4   /* not produced since ABI 3 (sampled verification takes trees) */
 };
 
 /* element type of hidden states and LM-head weights (bias is always fp32) */
@@ -176,20 +176,27 @@ int dcd_verify_greedy(const dcd_problem *p, const dcd_inputs *in, const dcd_outp
                       void *workspace, size_t workspace_bytes, void *hip_stream);
 
 /*
- * Sampled verification (Alg. 1) of B chains (parents[b,i] must be i-1, else the
- * sequence gets DCD_SEQ_NOT_CHAIN).
+ * Sampled verification (Alg. 1) of B draft trees (chains included).
  *   draft_probs [B*N, V] fp32 device: row b*N+i is pi_e^(i), the proposal draft
  *               token i was drawn from (row b*N+0 unused)
  *   u_accept    [B*N] fp32 device, in (0,1): u_accept[b*N+i] decides node i
  *   u_resample  [B*N] fp32 device, in (0,1): u_resample[b*N+j] draws the token
  *               emitted after row j
- * Node i is accepted iff pi_CD^(i-1)(tok_i) > 0 and
- * u_accept <= pi_CD^(i-1)(tok_i) / pi_e^(i)(tok_i); verification stops at the first
- * rejected node k, whose replacement is drawn from the residual
- * Normalize(max(0, pi_CD^(k-1) - pi_e^(k))) (from pi_CD^(k-1) if that is zero);
- * if every node is accepted the bonus token is drawn from pi_CD^(N-1).  A draw
- * is the inverse CDF in token-id order: the smallest token whose cumulative
- * weight exceeds u_resample times the total.
+ * The walk starts at the root with p = pi_CD of the root's row.  The children of
+ * the current node are tried in increasing node index: child c with token x is
+ * accepted iff p(x) > 0 and u_accept[c] <= p(x) / pi_e^(c)(x), and the walk moves
+ * to it with p = pi_CD of its row; a rejected child replaces p by the residual
+ * Normalize(max(0, p - pi_e^(c))) (p is kept if that sums to zero).  When every
+ * child of the current node is rejected, or it has none, the emitted token
+ * (next_token) is drawn from p with u_resample of the current node.  On a chain
+ * this is Alg. 1: stop at the first rejected node k and draw from
+ * Normalize(max(0, pi_CD^(k-1) - pi_e^(k))), or draw the bonus token from
+ * pi_CD^(N-1).  The paper runs sampled verification on chains only; for trees
+ * this is multi-draft speculative sampling (SpecInfer's rule), lossless when
+ * siblings are drafted independently from their pi_e.  A draw is the inverse CDF
+ * in token-id order: the smallest token whose cumulative weight exceeds
+ * u_resample times the total.  node_stats[DCD_NODE_RATIO] is pi_CD / pi_e of the
+ * node's token under its parent row (the ratio of a first sibling).
  */
 int dcd_verify_sample(const dcd_problem *p, const dcd_inputs *in, const float *draft_probs,
                       const float *u_accept, const float *u_resample, const dcd_outputs *out,
@@ -210,7 +217,8 @@ int dcd_lmhead_partials(const dcd_problem *p, const dcd_inputs *in, int sampled,
 /* static description of a return code (never NULL) */
 const char *dcd_error_string(int code);
 
-/* ABI version of this header: 2 (dcd_outputs gained row_argmax_expert and row_kl) */
+/* ABI version of this header: 3 (2: dcd_outputs gained row_argmax_expert and row_kl;
+   3: dcd_verify_sample takes trees) */
 int dcd_abi_version(void);
 
 #ifdef __cplusplus

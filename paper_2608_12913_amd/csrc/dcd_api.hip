@@ -187,6 +187,6 @@ const char *dcd_error_string(int code) {
     }
 }
 
-int dcd_abi_version(void) { return 2; }
+int dcd_abi_version(void) { return 3; }
 
 }  // extern "C"

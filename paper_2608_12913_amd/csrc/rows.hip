@@ -201,6 +201,7 @@ struct Smem {
     int wave_tot[NT / kWaveSize];
     int flag[4];
     int ints[4];
+    double dbl;
 };
 
 // Writes a row's results: rowinfo (for the sequence phase) and the optional outputs.
@@ -537,13 +538,35 @@ __device__ int group_exclusive_scan(int x, int tid, int *total, Smem &sm) {
     return before + in_wave;
 }
 
-// Draws one token from the mask members of row jrow (the support of pi_CD): with
-// weights max(0, pi_CD - pi_e) when qrow is given (Alg. 1's residual), else
-// pi_CD itself (the bonus draw, or a residual that sums to zero); inverse CDF in
-// token-id order with uniform u: the smallest token whose cumulative weight
-// exceeds u times the total.  Called by the whole group; returns the token.
-__device__ int draw_token(const Plan &P, size_t jrow, const float *qrow, float u, int tid,
-                          Smem &sm) {
+// The target at a node after the rejection of some of its drafted children, as a
+// weight per token t (Alg. 1's residual, applied once per rejected sibling, in
+// order): starting from p0 = pi_CD(t) of the node's row, each rejected sibling j
+// (proposal q_j, normaliser 1/Z_j; 0 when that residual summed to zero and was not
+// applied) maps w -> max(0, w - q_j(t)) / Z_j.  With `qnext`, the unnormalised
+// residual of one more rejection, max(0, w - qnext(t)), whose sum is the next Z.
+struct Residual {
+    const float *dprobs;  // draft_probs rows of the sequence (row i = pi_e^(i))
+    const int *rej;       // rejected siblings in order (LDS)
+    const double *invz;   // their 1/Z (LDS)
+    int nrej;
+    const float *qnext;
+    int V;
+    __device__ double operator()(float p0, int t) const {
+        double w = (double)p0;
+        for (int m = 0; m < nrej; ++m)
+            if (invz[m] > 0.0) w = fmax(0.0, w - (double)dprobs[(size_t)rej[m] * V + t]) * invz[m];
+        if (qnext) w = fmax(0.0, w - (double)qnext[t]);
+        return w;
+    }
+};
+
+// Over the mask members of row jrow (the support of pi_CD), in token-id order: the
+// sum of the residual's weights, and with `draw` the inverse-CDF draw at u times
+// that sum (the smallest token whose cumulative weight exceeds it; the last token
+// of positive weight if rounding leaves none).  Called by the whole group; returns
+// the drawn token (-1 without `draw` or with an empty support), *total the sum.
+__device__ int masked_scan(const Plan &P, size_t jrow, const Residual &res, bool draw, float u,
+                           double *total_out, int tid, Smem &sm) {
     const float *rj = P.rowinfo + jrow * kRowInfo;
     const float thr = rj[RI_THRESH], lse_p = rj[RI_LSEP], lse_q = rj[RI_LSEQ], logZ = rj[RI_LOGZ];
     const int *tc = P.tcount + jrow * P.ntiles;
@@ -569,11 +592,10 @@ __device__ int draw_token(const Plan &P, size_t jrow, const float *qrow, float u
     }
     int L;
     const int first = group_exclusive_scan(mine, tid, &L, sm);
-    auto weight = [&](int t, bool residual) -> double {
+    auto weight = [&](int t) -> double {
         const float2 c = cz[t];
         if (!(c.x >= thr)) return 0.0;
-        const float p = __expf((1.f + P.s) * (c.x - lse_p) - P.s * (c.y - lse_q) - logZ);
-        return residual ? (double)fmaxf(0.f, p - qrow[t]) : (double)p;
+        return res(__expf((1.f + P.s) * (c.x - lse_p) - P.s * (c.y - lse_q) - logZ), t);
     };
     // ids of list positions [lo, lo + kList) into sm.list
     auto fill = [&](int lo) {
@@ -587,39 +609,31 @@ __device__ int draw_token(const Plan &P, size_t jrow, const float *qrow, float u
         }
         __syncthreads();
     };
-    auto weigh = [&](int lo, bool residual) {
+    auto weigh = [&](int lo) {
         const int n = min(kList, L - lo);
-        for (int m = tid; m < n; m += NT) sm.wts[m] = weight(sm.list[m], residual);
+        for (int m = tid; m < n; m += NT) sm.wts[m] = weight(sm.list[m]);
         __syncthreads();
         return n;
     };
     const bool one_round = L <= kList;
     // pass 1: the total, summed sequentially in token order by thread 0
-    auto total_of = [&](bool residual) {
-        double run = 0.0;
-        for (int lo = 0; lo < L; lo += kList) {
-            fill(lo);
-            const int n = weigh(lo, residual);
-            if (tid == 0)
-                for (int m = 0; m < n; ++m) run += sm.wts[m];
-            __syncthreads();
-        }
-        return run;
-    };
-    bool residual = qrow != nullptr;
-    double total = total_of(residual);
-    if (tid == 0) sm.ints[0] = residual && !(total > 0.0);
-    __syncthreads();
-    if (sm.ints[0]) {  // degenerate residual: fall back to pi_CD
-        __syncthreads();
-        residual = false;
-        total = total_of(false);
-    }
-    // pass 2: the first token whose cumulative weight exceeds u * total (the last
-    // token of positive weight if rounding leaves none); with one round the ids
-    // and weights of pass 1 are still in place
-    const double target = (double)u * total;
     double run = 0.0;
+    for (int lo = 0; lo < L; lo += kList) {
+        fill(lo);
+        const int n = weigh(lo);
+        if (tid == 0)
+            for (int m = 0; m < n; ++m) run += sm.wts[m];
+        __syncthreads();
+    }
+    if (tid == 0) sm.dbl = run;
+    __syncthreads();
+    const double total = sm.dbl;
+    *total_out = total;
+    __syncthreads();
+    if (!draw) return -1;
+    // pass 2: with one round the ids and weights of pass 1 are still in place
+    const double target = (double)u * total;
+    run = 0.0;
     int last = -1;
     if (tid == 0) sm.ints[1] = -1;
     __syncthreads();
@@ -627,7 +641,7 @@ __device__ int draw_token(const Plan &P, size_t jrow, const float *qrow, float u
         int n = min(kList, L - lo);
         if (!one_round) {
             fill(lo);
-            n = weigh(lo, residual);
+            n = weigh(lo);
         }
         if (tid == 0) {
             int found = -1;
@@ -652,41 +666,36 @@ __device__ int draw_token(const Plan &P, size_t jrow, const float *qrow, float u
     return -1;  // empty support (a row without mask members)
 }
 
-// Untruncated target: the same draw over the whole vocabulary of row jrow, from
-// the dense logits.  Each thread sums a contiguous token range; thread 0 scans the
+// Untruncated target: the same over the whole vocabulary of row jrow, from the
+// dense logits.  Each thread sums a contiguous token range; thread 0 scans the
 // partial sums in order; the thread whose range holds the target walks it.
-__device__ int draw_token_full(const Plan &P, size_t jrow, const float *qrow, float u, int tid,
-                               Smem &sm) {
+__device__ int full_scan(const Plan &P, size_t jrow, const Residual &res, bool draw, float u,
+                         double *total_out, int tid, Smem &sm) {
     const float *rj = P.rowinfo + jrow * kRowInfo;
     const float lse_p = rj[RI_LSEP], lse_q = rj[RI_LSEQ], logZ = rj[RI_LOGZ];
     const float *zp = P.zp_full + jrow * P.zstride, *zq = P.zq_full + jrow * P.zstride;
     const int t0 = (int)((long long)tid * P.V / NT), t1 = (int)((long long)(tid + 1) * P.V / NT);
-    auto weight = [&](int t, bool residual) -> double {
-        const float p = __expf((1.f + P.s) * (zp[t] - lse_p) - P.s * (zq[t] - lse_q) - logZ);
-        return residual ? (double)fmaxf(0.f, p - qrow[t]) : (double)p;
+    auto weight = [&](int t) -> double {
+        return res(__expf((1.f + P.s) * (zp[t] - lse_p) - P.s * (zq[t] - lse_q) - logZ), t);
     };
     double *local = sm.wts, *prefix = sm.wts + NT;  // [NT], [NT + 1]
-    auto scan = [&](bool residual) {
-        double acc = 0.0;
-        for (int t = t0; t < t1; ++t) acc += weight(t, residual);
-        local[tid] = acc;
-        __syncthreads();
-        if (tid == 0) {
-            double run = 0.0;
-            for (int i = 0; i < NT; ++i) {
-                prefix[i] = run;
-                run += local[i];
-            }
-            prefix[NT] = run;
+    double acc = 0.0;
+    for (int t = t0; t < t1; ++t) acc += weight(t);
+    local[tid] = acc;
+    __syncthreads();
+    if (tid == 0) {
+        double run = 0.0;
+        for (int i = 0; i < NT; ++i) {
+            prefix[i] = run;
+            run += local[i];
         }
+        prefix[NT] = run;
+    }
+    __syncthreads();
+    *total_out = prefix[NT];
+    if (!draw) {
         __syncthreads();
-    };
-    bool residual = qrow != nullptr;
-    scan(residual);
-    if (residual && !(prefix[NT] > 0.0)) {  // degenerate residual: fall back to pi_CD
-        __syncthreads();
-        residual = false;
-        scan(false);
+        return -1;
     }
     const double target = (double)u * prefix[NT];
     if (tid == 0) sm.ints[1] = -1;
@@ -696,7 +705,7 @@ __device__ int draw_token_full(const Plan &P, size_t jrow, const float *qrow, fl
         double run = 0.0;
         int found = -1, last = -1;
         for (int t = t0; t < t1; ++t) {
-            const double wt = weight(t, residual);
+            const double wt = weight(t);
             run += wt;
             if (wt > 0.0) {
                 last = t;
@@ -709,7 +718,9 @@ __device__ int draw_token_full(const Plan &P, size_t jrow, const float *qrow, fl
         sm.ints[1] = found >= 0 ? found : last;
     }
     __syncthreads();
-    return sm.ints[1];
+    const int got = sm.ints[1];
+    __syncthreads();
+    return got;
 }
 
 template <int DT, bool SAMPLE>
@@ -718,9 +729,12 @@ __device__ void verify_sequence(const Plan &P, const Inputs &in, const Outputs &
     const int N = P.N, V = P.V;
     const size_t r0 = (size_t)b * N;
     int *s_par = dyn, *s_tok = dyn + N, *s_amax = dyn + 2 * N;
+    // sampled: the walk's state (see seq_lds_bytes)
+    float *s_p0 = reinterpret_cast<float *>(dyn + 3 * N), *s_qx = s_p0 + N;
+    int *s_rej = reinterpret_cast<int *>(s_qx + N);
+    double *s_invz = reinterpret_cast<double *>(dyn + 6 * N + (N & 1));
 
     if (tid < 4) sm.flag[tid] = 0;
-    if (tid == 0) sm.ints[2] = N;  // first rejected node (sampled)
     __syncthreads();
     for (int i = tid; i < N; i += NT) {
         const int p = in.parents[r0 + i], x = in.tokens[r0 + i];
@@ -730,12 +744,11 @@ __device__ void verify_sequence(const Plan &P, const Inputs &in, const Outputs &
         s_amax[i] = __float_as_int(r.b.y);
         if (i == 0 ? p != -1 : (p < 0 || p >= i)) atomicOr(&sm.flag[0], 1);
         if (i > 0 && (x < 0 || x >= V)) atomicOr(&sm.flag[1], 1);
-        if (SAMPLE && i > 0 && p != i - 1) atomicOr(&sm.flag[2], 1);
         if (!isfinite(r.a.x) || !isfinite(r.a.y) || !isfinite(r.a.z) || !isfinite(r.a.w))
             atomicOr(&sm.flag[3], 1);
     }
     __syncthreads();
-    const int status = sm.flag[0] ? 1 : sm.flag[1] ? 2 : sm.flag[2] ? 4 : sm.flag[3] ? 3 : 0;
+    const int status = sm.flag[0] ? 1 : sm.flag[1] ? 2 : sm.flag[3] ? 3 : 0;
     if (status != 0) {
         for (int i = tid; i < N; i += NT) {
             out.accept_path[r0 + i] = -1;
@@ -794,28 +807,66 @@ __device__ void verify_sequence(const Plan &P, const Inputs &in, const Outputs &
         return;
     }
 
-    // sampled: node statistics and the first rejection
+    // sampled: node statistics, and per node the target probability of its token
+    // under the parent row and its proposal probability, staged for the walk
     if (out.node_stats && tid < 6) out.node_stats[r0 * 6 + tid] = NAN;
     for (int i = 1 + tid; i < N; i += NT) {
         const int x = s_tok[i];
         const NodeStat n = node_stat(P.nodez[r0 + i], load_rowinfo(P.rowinfo, r0 + s_par[i]), P.s);
         const float pe = smp.draft_probs[(r0 + i) * V + x];
-        const float ratio = pe > 0.f ? __expf(n.lpcd) / pe : INFINITY;
-        const bool accept = n.in_mask && smp.u_acc[r0 + i] <= ratio;
-        if (!accept) atomicMin(&sm.ints[2], i);
-        if (out.node_stats) write_node_stats(out.node_stats + (r0 + i) * 6, n, ratio);
+        const float p0 = n.in_mask ? __expf(n.lpcd) : 0.f;
+        s_p0[i] = p0;
+        s_qx[i] = pe;
+        if (out.node_stats) write_node_stats(out.node_stats + (r0 + i) * 6, n, pe > 0.f ? p0 / pe : INFINITY);
     }
     __syncthreads();
-    // accept nodes 1..k-1; draw from the residual at k or from the bonus row
-    const int k = sm.ints[2];
-    const int jrow = k < N ? k - 1 : N - 1;
-    const float *qrow = k < N ? smp.draft_probs + (r0 + k) * V : nullptr;
-    const int next = P.full ? draw_token_full(P, r0 + jrow, qrow, smp.u_res[r0 + jrow], tid, sm)
-                            : draw_token(P, r0 + jrow, qrow, smp.u_res[r0 + jrow], tid, sm);
-    for (int i = tid; i < N; i += NT) out.accept_path[r0 + i] = i < k ? i : -1;
+    // The walk (Alg. 1 over a tree): the children of the current node are tried in
+    // index order, each against the target left by the siblings rejected before it;
+    // an accepted child becomes the current node; when every child is rejected (or
+    // there is none) the emitted token is drawn from what is left.  Every thread
+    // follows the walk; thread 0 takes the accept decisions.
+    Residual res{smp.draft_probs + r0 * V, s_rej, s_invz, 0, nullptr, V};
+    double total;
+    int cur = 0, len = 0;
+    for (int c = 1; c < N; ++c) {
+        if (s_par[c] != cur) continue;
+        if (tid == 0) {
+            const double w = res(s_p0[c], s_tok[c]);
+            const double ratio = s_qx[c] > 0.f ? w / (double)s_qx[c] : INFINITY;
+            sm.ints[3] = w > 0.0 && (double)smp.u_acc[r0 + c] <= ratio;
+        }
+        __syncthreads();
+        const bool accepted = sm.ints[3] != 0;
+        __syncthreads();
+        if (accepted) {
+            ++len;
+            if (tid == 0) out.accept_path[r0 + len] = c;
+            cur = c;  // its children have larger indices
+            res.nrej = 0;
+            continue;
+        }
+        // rejected: the normaliser of the residual it leaves
+        res.qnext = smp.draft_probs + (r0 + c) * V;
+        if (P.full)
+            full_scan(P, r0 + cur, res, false, 0.f, &total, tid, sm);
+        else
+            masked_scan(P, r0 + cur, res, false, 0.f, &total, tid, sm);
+        res.qnext = nullptr;
+        if (tid == 0) {
+            s_rej[res.nrej] = c;
+            s_invz[res.nrej] = total > 0.0 ? 1.0 / total : 0.0;  // zero sum: not applied
+        }
+        __syncthreads();
+        ++res.nrej;
+    }
+    const float u = smp.u_res[r0 + cur];
+    const int next = P.full ? full_scan(P, r0 + cur, res, true, u, &total, tid, sm)
+                            : masked_scan(P, r0 + cur, res, true, u, &total, tid, sm);
+    for (int i = len + 1 + tid; i < N; i += NT) out.accept_path[r0 + i] = -1;
     if (tid == 0) {
+        out.accept_path[r0] = 0;
         out.status[b] = 0;
-        out.accept_len[b] = k - 1;
+        out.accept_len[b] = len;
         out.next_token[b] = next;
     }
 }
@@ -827,7 +878,7 @@ __global__ __launch_bounds__(NT) void finish_kernel(Plan P, Inputs in, Outputs o
                                                     SampleInputs smp) {
     __shared__ Smem sm;
     __shared__ int last;
-    extern __shared__ int dyn[];
+    extern __shared__ __align__(16) int dyn[];
     const int row = blockIdx.x, tid = threadIdx.x;
     combine_row<DT>(P, in, out, row, tid % kWaveSize, tid / kWaveSize, sm.list);
     // count the row once both of its waves are done; the release half of the
@@ -846,10 +897,30 @@ __global__ __launch_bounds__(NT) void finish_kernel(Plan P, Inputs in, Outputs o
 
 }  // namespace
 
+// dynamic LDS of the sequence phase: parents, tokens and row argmax (12 bytes per
+// node); sampled also the walk's state: target and proposal probability of each
+// node's token, the rejected siblings and their normalisers (20 more bytes per
+// node, the doubles 8-byte aligned)
+size_t seq_lds_bytes(int N, bool sampled) {
+    return sampled ? (size_t)(6 * N + (N & 1)) * sizeof(int) + (size_t)N * sizeof(double)
+                   : (size_t)3 * N * sizeof(int);
+}
+
 hipError_t launch_finish(const Plan &p, const Inputs &in, const Outputs &out,
                          const SampleInputs *smp, hipStream_t st) {
     const SampleInputs s = smp ? *smp : SampleInputs{nullptr, nullptr, nullptr};
-    const size_t lds = (size_t)3 * p.N * sizeof(int);  // parents, tokens, argmax
+    const size_t lds = seq_lds_bytes(p.N, smp != nullptr);
+    // the sampled walk's LDS can exceed the default 64 KB limit of dynamic LDS
+    static const hipError_t attr = [] {
+        const int most = (int)seq_lds_bytes(kMaxNodes, true);
+        hipError_t e = hipFuncSetAttribute((const void *)finish_kernel<kBF16, true>,
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, most);
+        if (e == hipSuccess)
+            e = hipFuncSetAttribute((const void *)finish_kernel<kF32, true>,
+                                    hipFuncAttributeMaxDynamicSharedMemorySize, most);
+        return e;
+    }();
+    if (attr != hipSuccess) return attr;
     if (p.dtype == kBF16) {
         if (smp)
             hipLaunchKernelGGL((finish_kernel<kBF16, true>), dim3(p.R), dim3(NT), lds, st, p, in, out, s);

@@ -153,10 +153,12 @@ def check_walk_consistent(g, parents, tokens):
         assert g["next_token"][b] == amax[b, last]
 
 
-def compare_sample(g, o, case, tokens, draft_probs, amb, report, seqs=None):
-    """Sampled chains: per node the accept decision where |u - ratio| is clear, the
-    first rejection, and the emitted token where the draw is clear."""
-    B, N = case.B, case.N
+def compare_sample(g, o, parents, u_acc, tokens, amb, report, seqs=None):
+    """Sampled walks (chains or trees): the path and length exactly when every accept
+    decision the oracle's walk took is clear (|u - ratio| > RATIO_GATE * ratio, with
+    the ratio against the residual the node was tested with, on unambiguous rows),
+    and the emitted token when the draw is also clear of its CDF breakpoints."""
+    B, N = parents.shape
     seqs = range(B) if seqs is None else seqs
     gated = 0
     for b in seqs:
@@ -165,22 +167,21 @@ def compare_sample(g, o, case, tokens, draft_probs, amb, report, seqs=None):
             continue
         r0 = b * N
         clear = True
-        k = N
         for i in range(1, N):
-            ratio = o["node_stats"][r0 + i, oracle.NS_RATIO]
-            u = float(case.u_acc[r0 + i])
-            if amb[r0 + i - 1] or (np.isfinite(ratio) and abs(u - ratio) <= RATIO_GATE * max(ratio, 1e-30)):
+            ratio = o["walk_ratio"][r0 + i]
+            if np.isnan(ratio):
+                continue  # not tested on the oracle's walk
+            u = float(u_acc[r0 + i])
+            if amb[r0 + parents[b, i]] or (np.isfinite(ratio) and
+                                             abs(u - ratio) <= RATIO_GATE * max(ratio, 1e-30)):
                 clear = False
-                break
-            if not (o["node_stats"][r0 + i, oracle.NS_INMASK] == 1 and u <= ratio):
-                k = i
                 break
         if not clear:
             gated += 1
             continue
-        assert g["accept_len"][b] == o["accept_len"][b] == k - 1, f"seq {b}"
-        assert np.array_equal(g["accept_path"][b], o["accept_path"][b])
-        jrow = r0 + (k - 1 if k < N else N - 1)
+        assert g["accept_len"][b] == o["accept_len"][b], f"seq {b}"
+        assert np.array_equal(g["accept_path"][b], o["accept_path"][b]), f"path seq {b}"
+        jrow = r0 + int(o["accept_path"][b][o["accept_len"][b]])
         if amb[jrow] or o["res_gap"][b] <= CDF_GATE:
             gated += 1
             continue

@@ -24,7 +24,7 @@ def test_library_exports_every_declared_function():
     L = dcd.lib()
     for n in names:
         assert hasattr(L, n), n
-    assert L.dcd_abi_version() == 2
+    assert L.dcd_abi_version() == 3
 
 
 def test_struct_layouts_match_the_header(tmp_path):

@@ -226,7 +226,7 @@ def _check_sample(case, probs, tokens, label, seqs=None):
     parity.compare_diagnostics(g, o, np.arange(case.R), case.theta, case.s, case.V, report)
     parity.compare_nodes(g, o, case.parents, amb, report)
     boundary = o["row_gap"] <= parity.BOUNDARY_GATE
-    parity.compare_sample(g, o, case, tokens, probs, boundary, report, seqs)
+    parity.compare_sample(g, o, case.parents, case.u_acc, tokens, boundary, report, seqs)
     gr = g["node_stats"][:, oracle.NS_RATIO]
     orat = o["node_stats"][:, oracle.NS_RATIO]
     fin = np.isfinite(orat) & (orat > 1e-30)
@@ -291,13 +291,65 @@ def test_untruncated_sampled_residual_over_vocabulary():
     assert np.all(g["row_stats"][:, oracle.RS_COUNT] == case.V)
 
 
-def test_sampled_rejects_trees():
-    case = synth.make_case("b8_tree64", 6, N=12, depth=3, max_children=4, V=600, dp=64, dq=32)
-    case.cfg["mode"] = "sample"
-    probs = np.full((case.R, case.V), 1.0 / case.V, np.float32)
-    tokens = np.ones((1, case.N), np.int32)
-    g = _runner().from_case(case, tokens, draft_probs=probs).run("sample")
-    assert g["status"][0] == oracle.SEQ_NOT_CHAIN and g["next_token"][0] == -1
+def _sampled_tree_setup(case):
+    """Proposals of a tree: node i's from the expert logits of its parent row."""
+    rows = oracle.eval_rows(case.hp, case.hq, case.wp, case.wq, case.bias, case.bias,
+                            theta=case.theta, s=case.s, temperature=case.T, want_logits=True)
+    parent_logits = np.zeros_like(rows["zp"])
+    for r in range(case.R):
+        i = r % case.N
+        if i:
+            parent_logits[r] = rows["zp"][r - i + case.parents[r // case.N, i]]
+    return synth.sampled_draft(case, parent_logits)
+
+
+@pytest.mark.parametrize("seed,theta,s", [(0, 0.1, 0.5), (1, 0.0, 0.5), (2, 0.3, 1.0)])
+def test_sampled_trees_small(seed, theta, s):
+    """Sampled verification of draft trees: siblings tried in index order against the
+    residual of the rejected ones (several rejections per node occur here)."""
+    case = synth.make_case("s8_chain16x8", 40 + seed, B=6, N=24, tree="tree", depth=4,
+                           max_children=5, V=2500, dp=256, dq=128, theta=theta, s=s)
+    probs, tokens = _sampled_tree_setup(case)
+    g, o = _check_sample(case, probs, tokens, f"sampled trees seed {seed}")
+    walked = np.isfinite(o["walk_ratio"]) | np.isinf(o["walk_ratio"])
+    _say(f"sampled trees seed {seed}: {int(walked.sum())} nodes tested on the walks, "
+         f"accept lengths {g['accept_len'].tolist()}")
+
+
+def test_sampled_tree_forced_paths():
+    """Star trees of three children.  Sequence 0: child 1 is one-hot on a masked token
+    (rejected, and its residual is pi_CD itself), child 2 proposes pi_CD exactly and
+    carries its argmax (ratio 1: accepted).  Sequence 1: every child is one-hot on a
+    masked token, so all are rejected and the token is drawn from pi_CD."""
+    case = synth.make_case("s8_chain16x8", 50, B=2, N=4, tree="chain", V=900, dp=128, dq=64)
+    case.parents[:] = np.array([-1, 0, 0, 0])
+    rows = oracle.eval_rows(case.hp, case.hq, case.wp, case.wq, case.bias, case.bias,
+                            theta=case.theta, s=case.s, want_lpcd=True)
+    probs = np.zeros((case.R, case.V), np.float32)
+    tokens = np.zeros((case.B, case.N), np.int32)
+    for b in range(2):
+        p = np.exp(rows["lpcd"][b * 4])
+        masked = np.flatnonzero(p == 0)
+        for i in (1, 2, 3):
+            t = int(masked[7 * i + b])
+            if b == 0 and i == 2:
+                probs[b * 4 + i] = p
+                t = int(np.argmax(p))
+            else:
+                probs[b * 4 + i, t] = 1.0
+            tokens[b, i] = t
+    case.u_acc = np.minimum(case.u_acc, np.float32(0.99))
+    g, o = _check_sample(case, probs, tokens, "sampled star trees")
+    assert list(g["accept_path"][0][:2]) == [0, 2] and g["accept_len"][0] == 1
+    assert g["accept_len"][1] == 0
+
+
+def test_sampled_tree_at_the_node_limit():
+    """4096 nodes (the largest sequence): the walk's state fills most of the LDS."""
+    case = synth.make_case("s8_chain16x8", 51, B=1, N=4096, tree="tree", depth=12,
+                           max_children=6, V=300, dp=64, dq=32, theta=0.1)
+    probs, tokens = _sampled_tree_setup(case)
+    _check_sample(case, probs, tokens, "sampled tree of 4096 nodes")
 
 
 # ------------------------------------------------------------------ full-size workloads
@@ -354,13 +406,8 @@ def test_full_s8_chain16x8(theta):
     amb = parity.compare_rows(sel, o, np.arange(len(rows)), report)
     parity.compare_diagnostics(sel, o, np.arange(len(rows)), case.theta, case.s, case.V, report)
     parity.compare_nodes(sel, o, case.parents[seqs], amb, report)
-
-    class _Sub:
-        B, N = len(seqs), 8
-        u_acc, u_res = case.u_acc[rows], case.u_res[rows]
-
-    parity.compare_sample(sel, o, _Sub, tokens[seqs], probs[rows], o["row_gap"] <= parity.BOUNDARY_GATE,
-                          report)
+    parity.compare_sample(sel, o, case.parents[seqs], case.u_acc[rows], tokens[seqs],
+                          o["row_gap"] <= parity.BOUNDARY_GATE, report)
     assert np.all(g["status"] == 0)
     _say(f"s8_chain16x8: ok {report}; accept lengths {g['accept_len'].tolist()}")
 
