@@ -52,6 +52,8 @@ def main():
     ap.add_argument("--theta", type=float, default=None,
                     help="override the workload's plausibility cutoff (0 = untruncated target)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-probes", action="store_true",
+                    help="skip the measured read-bandwidth and MFMA-rate ceilings")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
                     help="only run a plain device-to-device copy of BYTES bytes 10 times (for "
                          "scaling the HBM byte counters of a profiler run) and exit")
@@ -145,6 +147,11 @@ def main():
                         frac=round(achieved / HBM_PEAK_GBS, 4))
     roofline.update(traffic=traffic, kernel=kernel, algorithmic_bytes=kbytes, flops=flops,
                     avg_us=round(ms_lmhead * 1e3, 2), traffic_source=traffic_src)
+    if not args.no_probes:
+        measured = measured_ceilings(torch, stream, log)
+        roofline["measured_peak"] = measured
+        key = "mfma_bf16_TFLOPs" if roofline["bound"] == "mfma" else "stream_read_GBs"
+        roofline["frac_of_measured"] = round(roofline["achieved"] / measured[key], 4)
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -172,6 +179,38 @@ def main():
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)
+
+
+def measured_ceilings(torch, stream, log):
+    """What this device delivers to a plain streaming read (4 GiB, far above the
+    256 MB MALL) and to a register-only bf16 MFMA loop (include/dcd_probe.h), each
+    timed with HIP events on the bench stream."""
+    from paper_2608_12913_amd import dcd
+
+    def timed(fn, n):
+        fn()
+        fn()  # the first launches also ramp the clocks
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for _ in range(n):
+            fn()
+        b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / n * 1e-3
+
+    nbytes = 4 << 30
+    buf = torch.empty(nbytes, dtype=torch.uint8, device="cuda:0")
+    sink = torch.zeros(256 * 1024, dtype=torch.float32, device="cuda:0")
+    t_read = timed(lambda: dcd.probe_stream_read(buf, nbytes, sink, stream), 10)
+    del buf
+    wg, iters = 1024, 4000
+    flops = dcd.probe_mfma_bf16(wg, iters, sink, stream)
+    t_mfma = timed(lambda: dcd.probe_mfma_bf16(wg, iters, sink, stream), 5)
+    out = {"stream_read_GBs": round(nbytes / t_read / 1e9, 1),
+           "mfma_bf16_TFLOPs": round(flops / t_mfma / 1e12, 1)}
+    log(f"measured ceilings: {out}")
+    return out
 
 
 def counted_traffic(kernel, workload):

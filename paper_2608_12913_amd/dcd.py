@@ -21,7 +21,9 @@ ROW_MAX_P, ROW_LSE_P, ROW_LSE_Q, ROW_LOGZ, ROW_TOP1, ROW_MARGIN, ROW_COUNT, ROW_
 NODE_LOGP_P, NODE_LOGP_Q, NODE_CD, NODE_LOGP_CD, NODE_IN_MASK, NODE_RATIO = range(6)
 
 EXPORTS = ("dcd_workspace_bytes", "dcd_verify_greedy", "dcd_verify_sample",
-           "dcd_lmhead_partials", "dcd_error_string", "dcd_abi_version")
+           "dcd_lmhead_partials", "dcd_error_string", "dcd_abi_version",
+           # include/dcd_probe.h
+           "dcd_probe_stream_read", "dcd_probe_mfma_bf16")
 
 
 class DcdError(RuntimeError):
@@ -74,6 +76,11 @@ def lib() -> ctypes.CDLL:
         L.dcd_error_string.restype = ctypes.c_char_p
         L.dcd_abi_version.argtypes = []
         L.dcd_abi_version.restype = ctypes.c_int
+        L.dcd_probe_stream_read.argtypes = [P, ctypes.c_size_t, P, P]
+        L.dcd_probe_stream_read.restype = ctypes.c_int
+        L.dcd_probe_mfma_bf16.argtypes = [ctypes.c_int, ctypes.c_int, P,
+                                          ctypes.POINTER(ctypes.c_double), P]
+        L.dcd_probe_mfma_bf16.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -144,5 +151,23 @@ def lmhead_partials(problem: Problem, inputs: Inputs, sampled: bool, workspace,
                     workspace_bytes: int, stream=None) -> None:
     rc = lib().dcd_lmhead_partials(ctypes.byref(problem), ctypes.byref(inputs), int(sampled),
                                    ptr(workspace), int(workspace_bytes), _stream(stream))
+    if rc != DCD_OK:
+        raise DcdError(rc)
+
+
+def probe_stream_read(buf, nbytes: int, sink, stream=None) -> None:
+    """Enqueue one streaming read of `nbytes` at `buf` (include/dcd_probe.h)."""
+    _check(lib().dcd_probe_stream_read(ptr(buf), int(nbytes), ptr(sink), _stream(stream)))
+
+
+def probe_mfma_bf16(workgroups: int, iters: int, sink, stream=None) -> float:
+    """Enqueue the bf16 MFMA loop; returns the flops one launch performs."""
+    flops = ctypes.c_double(0.0)
+    _check(lib().dcd_probe_mfma_bf16(int(workgroups), int(iters), ptr(sink), ctypes.byref(flops),
+                                      _stream(stream)))
+    return flops.value
+
+
+def _check(rc: int) -> None:
     if rc != DCD_OK:
         raise DcdError(rc)

@@ -1,6 +1,7 @@
 """C-ABI checks that need no GPU: the library loads, exports every function the
 header declares, and rejects invalid requests on the host before any launch."""
 import ctypes
+import glob
 import os
 import re
 
@@ -9,13 +10,15 @@ import pytest
 from paper_2608_12913_amd import dcd
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-HEADER = os.path.join(ROOT, "include", "dcd.h")
+HEADERS = sorted(glob.glob(os.path.join(ROOT, "include", "*.h")))
 
 
 def _declared_functions():
-    text = open(HEADER).read()
-    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(dcd_[a-z_]+)\s*\(", text)))
+    names = set()
+    for h in HEADERS:
+        text = re.sub(r"/\*.*?\*/", "", open(h).read(), flags=re.S)
+        names |= set(re.findall(r"\b(dcd_[a-z_0-9]+)\s*\(", text))
+    return sorted(names)
 
 
 def test_library_exports_every_declared_function():
@@ -139,3 +142,18 @@ def test_binding_raises():
     with pytest.raises(dcd.DcdError) as e:
         dcd.verify_greedy(p, dcd.Inputs(), dcd.Outputs(), None, 0)
     assert e.value.code == dcd.DCD_ERR_SHAPE
+
+
+def test_probe_host_validation():
+    """The measurement probes reject invalid requests before any launch."""
+    L = dcd.lib()
+    buf = (ctypes.c_char * 64)()
+    a = (ctypes.addressof(buf) + 15) // 16 * 16
+    flops = ctypes.c_double(0.0)
+    assert L.dcd_probe_stream_read(None, 16, a, None) == dcd.DCD_ERR_NULL
+    assert L.dcd_probe_stream_read(a, 0, a, None) == dcd.DCD_ERR_SHAPE
+    assert L.dcd_probe_stream_read(a, 24, a, None) == dcd.DCD_ERR_SHAPE
+    assert L.dcd_probe_stream_read(a + 4, 16, a, None) == dcd.DCD_ERR_ALIGN
+    assert L.dcd_probe_mfma_bf16(0, 10, a, ctypes.byref(flops), None) == dcd.DCD_ERR_SHAPE
+    assert L.dcd_probe_mfma_bf16(4, 0, a, ctypes.byref(flops), None) == dcd.DCD_ERR_SHAPE
+    assert L.dcd_probe_mfma_bf16(4, 10, None, ctypes.byref(flops), None) == dcd.DCD_ERR_NULL
