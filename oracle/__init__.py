@@ -55,6 +55,9 @@ def _load():
         lib.dco_eval_rows.argtypes = [i32, i32, i32, P, P, P, P, P, P, f64, f64, f64, P, i32,
                                       P, P, P, P, P, P, P, i32]
         lib.dco_eval_rows.restype = i32
+        lib.dco_propose.argtypes = [i32, i32, i32, i32, P, P, P, P, P, P, f64, f64, f64, P, P, P, P,
+                                    P, i32]
+        lib.dco_propose.restype = i32
         lib.dco_greedy_walk.argtypes = [i32, P, P, P, P, P, P]
         lib.dco_greedy_walk.restype = None
         lib.dco_sample_tree.argtypes = [i32, i32, P, P, P, P, P, P, P, P, P, P, P, P]
@@ -111,6 +114,26 @@ def eval_rows(hp, hq, wp, wq, bp, bq, *, theta, s, temperature=1.0, rows=None,
     if rc:
         raise RuntimeError(f"dco_eval_rows failed ({rc})")
     return out
+
+
+def propose(he, hf, we, wf, be, bf, u, *, theta, s, temperature=1.0, nthreads=0):
+    """Proposals from the recombined heads: dict(probs [R, V], tokens [R], gap [R],
+    argmax [R])."""
+    he, hf, we, wf = as_f32(he), as_f32(hf), as_f32(we), as_f32(wf)
+    be = None if be is None else _c(be, np.float32)
+    bf = None if bf is None else _c(bf, np.float32)
+    u = _c(u, np.float32)
+    V, de = we.shape
+    df = wf.shape[1]
+    R = he.shape[0]
+    o = dict(probs=np.zeros((R, V)), tokens=np.zeros(R, np.int32), gap=np.zeros(R),
+             argmax=np.zeros(R, np.int32))
+    rc = _load().dco_propose(R, V, de, df, _p(he), _p(hf), _p(we), _p(wf), _p(be), _p(bf),
+                             float(temperature), float(theta), float(s), _p(u), _p(o["tokens"]),
+                             _p(o["probs"]), _p(o["gap"]), _p(o["argmax"]), int(nthreads))
+    if rc:
+        raise RuntimeError(f"dco_propose failed ({rc})")
+    return o
 
 
 def greedy_walk(parents, tokens, row_argmax):

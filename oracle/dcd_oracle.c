@@ -27,6 +27,10 @@
  *                       (App. B.1): the expert's own
  *                       top-1 token, D_KL(pi_p || pi_q) and D_KL(pi_p || pi_CD),
  *                       each summed from its definition.
+ *   dco_propose         the decomposed dual-drafter of Sec. 3.1: the CD target of
+ *                       two drafter heads, pi_hat ~ pi_e^(1+s) pi_f^(-s) (with
+ *                       the same mask), as a proposal distribution per row and a
+ *                       token drawn from it.
  *   dco_greedy_walk     greedy (T = 0) verification of a draft tree: a draft
  *                       token is accepted iff it equals the target's argmax
  *                       (Alg. 1 with a one-hot target), walked from the root.
@@ -385,6 +389,37 @@ void dco_sample_tree(int N, int V, const int32_t *parents, const int32_t *tokens
     if (res_gap) *res_gap = cdf_gap(p, V, (double)u_res[cur]);
     free(p);
     free(w);
+}
+
+/*
+ * Proposals from the contrastive recombination of two heads (Sec. 3.1, decomposed
+ * dual-drafter; App. A.1): for each of R rows, pi_hat = the CD target of the two
+ * heads given as expert and amateur (Eq. (1) with the mask of cd_row, logits
+ * divided by the temperature), written densely to probs_out [R][V]; and a token
+ * drawn from it by inverse CDF with u[r] (tokens_out [R]), with the draw's relative
+ * distance to its CDF breakpoints in gap_out [R] (the parity gate).
+ */
+int dco_propose(int R, int V, int de, int df, const float *he, const float *hf, const float *we,
+                const float *wf, const float *be, const float *bf, double temperature, double theta,
+                double s, const float *u, int32_t *tokens_out, double *probs_out, double *gap_out,
+                int32_t *argmax_out, int nthreads)
+{
+    if (R <= 0 || V <= 0 || !(temperature > 0.0)) return -2;
+    double *lp = (double *)malloc(sizeof(double) * (size_t)R * V);
+    double *p = (double *)malloc(sizeof(double) * (size_t)V);
+    if (!lp || !p) { free(lp); free(p); return -1; }
+    int rc = dco_eval_rows(V, de, df, he, hf, we, wf, be, bf, temperature, theta, s, NULL, R,
+                           argmax_out, NULL, NULL, NULL, NULL, NULL, lp, nthreads);
+    if (rc) { free(lp); free(p); return rc; }
+    for (int r = 0; r < R; ++r) {
+        for (int v = 0; v < V; ++v) p[v] = exp(lp[(size_t)r * V + v]);
+        if (probs_out) memcpy(probs_out + (size_t)r * V, p, sizeof(double) * (size_t)V);
+        if (tokens_out) tokens_out[r] = inverse_cdf(p, V, (double)u[r]);
+        if (gap_out) gap_out[r] = cdf_gap(p, V, (double)u[r]);
+    }
+    free(lp);
+    free(p);
+    return 0;
 }
 
 /* status of one sequence from its tree and tokens (before any numerics) */

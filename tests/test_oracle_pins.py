@@ -372,6 +372,49 @@ def test_verify_returns_row_diagnostics_of_every_row():
     np.testing.assert_array_equal(o["row_diag"], d)
 
 
+# ---------------------------------------------------------------- dual-drafter proposals
+def test_propose_hand_worked_example():
+    """pi_e = (0.2, 0.3, 0.5), pi_f uniform, s = 1, no mask: pi_hat ~ pi_e^2 / pi_f
+    ~ (0.04, 0.09, 0.25) / 0.38; the inverse CDF at u = 0.1, 0.2, 0.5 gives tokens
+    0 (0.105 > 0.1), 1 (0.342 > 0.2) and 2."""
+    hp, hq, wp, wq, bp, bq = _bias_only_case(np.log([0.2, 0.3, 0.5]), [0.0, 0.0, 0.0])
+    he = np.repeat(hp, 3, axis=0)
+    hf = np.repeat(hq, 3, axis=0)
+    o = oracle.propose(he, hf, wp, wq, bp, bq, [0.1, 0.2, 0.5], theta=0.0, s=1.0)
+    np.testing.assert_allclose(o["probs"], np.tile([0.04, 0.09, 0.25], (3, 1)) / 0.38, rtol=1e-6)
+    assert list(o["tokens"]) == [0, 1, 2] and list(o["argmax"]) == [2, 2, 2]
+
+
+def test_propose_special_cases():
+    """An amateur-side head equal to the expert-side one, or s = 0, gives the
+    expert-side head's own softmax (scipy), masked and renormalised under theta."""
+    rng = np.random.default_rng(17)
+    he, hf, we, wf, b = _random_problem(rng, 400, 16, 16, 5, scale=3.0)
+    u = rng.random(5).astype(np.float32)
+    for T in (1.0, 0.7):
+        ze = (he.astype(np.float64) @ we.T.astype(np.float64) + b) / T
+        pe = np.exp(_softmax_log(ze))
+        o = oracle.propose(he, he, we, we, b, b, u, theta=0.0, s=0.8, temperature=T)
+        np.testing.assert_allclose(o["probs"], pe, rtol=1e-9, atol=1e-15)
+        o = oracle.propose(he, hf, we, wf, b, b, u, theta=0.2, s=0.0, temperature=T)
+        keep = pe >= 0.2 * pe.max(axis=1, keepdims=True)
+        np.testing.assert_allclose(o["probs"], np.where(keep, pe, 0) / np.where(keep, pe, 0).sum(1, keepdims=True),
+                                   rtol=1e-9, atol=1e-15)
+
+
+def test_propose_draw_follows_the_distribution():
+    """Sweeping u over a midpoint grid, the drawn tokens' frequencies are the
+    proposal probabilities up to the grid resolution."""
+    rng = np.random.default_rng(18)
+    he, hf, we, wf, b = _random_problem(rng, 12, 8, 8, 1, scale=1.0)
+    G = 2000
+    u = ((np.arange(G) + 0.5) / G).astype(np.float32)
+    o = oracle.propose(np.repeat(he, G, 0), np.repeat(hf, G, 0), we, wf, b, b, u, theta=0.05, s=0.5)
+    freq = np.bincount(o["tokens"], minlength=12) / G
+    np.testing.assert_allclose(freq, o["probs"][0], atol=1.5 / G)
+    assert np.all(o["probs"][0][freq > 0] > 0)
+
+
 # ---------------------------------------------------------------- greedy walk
 def _parse_ints(s):
     return np.array([int(x) for x in s.split(",")], np.int32)
