@@ -203,6 +203,27 @@ int dcd_verify_sample(const dcd_problem *p, const dcd_inputs *in, const float *d
                       void *workspace, size_t workspace_bytes, void *hip_stream);
 
 /*
+ * Proposals from the contrastive recombination of two heads: the decomposed
+ * dual-drafter of Sec. 3.1 (App. A.1), pi_hat(x) ~ pi_e(x)^(1+s) pi_f(x)^(-s), is the
+ * CD target computed by the verify calls with the drafter's expert-aligned head in
+ * the expert slots of `in` and its amateur-aligned head in the amateur slots (any
+ * two heads work; with the models' own heads it is pi_CD itself).  Per row
+ * r < batch*nodes: the logits of both heads divided by the problem's temperature,
+ * the plausibility mask, then
+ *   probs  [B*N, V] fp32 device, optional: pi_hat of every token (0 off the mask);
+ *   tokens [B*N] int32 device, optional: a token drawn from pi_hat with u[r] by
+ *          inverse CDF in token-id order (needs u [B*N] fp32 device in (0,1));
+ *   argmax [B*N] int32 device, optional: argmax of pi_hat, lowest id on ties.
+ * At least one output must be given.  Only h_*, w_* and bias_* of `in` are read;
+ * the rows need no tree.  A row with non-finite logits gets token -1.  Workspace
+ * and errors as for the verify calls.  A proposer that keeps `probs` can pass
+ * them as the draft_probs of a later dcd_verify_sample.
+ */
+int dcd_propose(const dcd_problem *p, const dcd_inputs *in, const float *u, int32_t *tokens,
+                float *probs, int32_t *argmax, void *workspace, size_t workspace_bytes,
+                void *hip_stream);
+
+/*
  * First stage of dcd_verify_greedy / dcd_verify_sample on its own: both LM-head
  * projections of every row with their per-tile softmax partials and plausibility
  * candidates, written to `workspace` (one kernel launch, everything else of the
@@ -217,8 +238,8 @@ int dcd_lmhead_partials(const dcd_problem *p, const dcd_inputs *in, int sampled,
 /* static description of a return code (never NULL) */
 const char *dcd_error_string(int code);
 
-/* ABI version of this header: 3 (2: dcd_outputs gained row_argmax_expert and row_kl;
-   3: dcd_verify_sample takes trees) */
+/* ABI version of this header: 4 (2: dcd_outputs gained row_argmax_expert and row_kl;
+   3: dcd_verify_sample takes trees; 4: dcd_propose) */
 int dcd_abi_version(void);
 
 #ifdef __cplusplus

@@ -119,6 +119,30 @@ int run_lmhead(const dcd_problem *p, const dcd_inputs *in, int sampled, void *ws
     return launch_lmhead(P, I, (hipStream_t)stream) == hipSuccess ? DCD_OK : DCD_ERR_HIP;
 }
 
+int run_propose(const dcd_problem *p, const dcd_inputs *in, const ProposeOutputs &o, void *ws,
+                size_t ws_bytes, void *stream) {
+    Plan P;
+    int rc = make_plan(p, true, P);  // the temperature applies, both heads' logits are kept
+    if (rc) return rc;
+    if (!in) return DCD_ERR_NULL;
+    if (!in->h_expert || !in->h_amateur || !in->w_expert || !in->w_amateur) return DCD_ERR_NULL;
+    if (!o.tokens && !o.probs && !o.argmax) return DCD_ERR_NULL;
+    if (o.tokens && !o.u) return DCD_ERR_NULL;
+    if (!aligned(in->h_expert, 16) || !aligned(in->h_amateur, 16) || !aligned(in->w_expert, 16) ||
+        !aligned(in->w_amateur, 16) || !aligned(in->bias_expert, 4) || !aligned(in->bias_amateur, 4) ||
+        !aligned(o.u, 4) || !aligned(o.tokens, 4) || !aligned(o.probs, 4) || !aligned(o.argmax, 4))
+        return DCD_ERR_ALIGN;
+    const size_t need = workspace_layout(P, nullptr);
+    if (!ws || ws_bytes < need || !aligned(ws, kAlign)) return DCD_ERR_WORKSPACE;
+    workspace_layout(P, (char *)ws);
+    const Inputs I{in->h_expert, in->h_amateur, in->w_expert, in->w_amateur,
+                   in->bias_expert, in->bias_amateur, nullptr, nullptr};
+    hipStream_t st = (hipStream_t)stream;
+    if (launch_lmhead(P, I, st) != hipSuccess) return DCD_ERR_HIP;
+    if (launch_propose(P, I, o, st) != hipSuccess) return DCD_ERR_HIP;
+    return DCD_OK;
+}
+
 }  // namespace
 
 size_t workspace_layout(Plan &p, char *base) {
@@ -168,6 +192,13 @@ int dcd_verify_sample(const dcd_problem *p, const dcd_inputs *in, const float *d
     return dcd::run(p, in, &s, out, workspace, workspace_bytes, hip_stream);
 }
 
+int dcd_propose(const dcd_problem *p, const dcd_inputs *in, const float *u, int32_t *tokens,
+                float *probs, int32_t *argmax, void *workspace, size_t workspace_bytes,
+                void *hip_stream) {
+    return dcd::run_propose(p, in, dcd::ProposeOutputs{u, tokens, probs, argmax}, workspace,
+                            workspace_bytes, hip_stream);
+}
+
 int dcd_lmhead_partials(const dcd_problem *p, const dcd_inputs *in, int sampled, void *workspace,
                         size_t workspace_bytes, void *hip_stream) {
     return dcd::run_lmhead(p, in, sampled, workspace, workspace_bytes, hip_stream);
@@ -187,6 +218,6 @@ const char *dcd_error_string(int code) {
     }
 }
 
-int dcd_abi_version(void) { return 3; }
+int dcd_abi_version(void) { return 4; }
 
 }  // extern "C"

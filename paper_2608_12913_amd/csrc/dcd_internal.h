@@ -125,6 +125,14 @@ hipError_t launch_lmhead(const Plan &p, const Inputs &in, hipStream_t st);
 // the many-row variant (bf16, masked target, R >= kWideMinRows): same outputs
 bool use_wide_lmhead(const Plan &p);
 hipError_t launch_lmhead_wide(const Plan &p, const Inputs &in, hipStream_t st);
+// proposals from the recombined heads (rows only, after launch_lmhead)
+struct ProposeOutputs {
+    const float *u;
+    int32_t *tokens;
+    float *probs;
+    int32_t *argmax;
+};
+hipError_t launch_propose(const Plan &p, const Inputs &in, const ProposeOutputs &out, hipStream_t st);
 // per-row combination and per-sequence verification (greedy when smp is null)
 hipError_t launch_finish(const Plan &p, const Inputs &in, const Outputs &out,
                          const SampleInputs *smp, hipStream_t st);

@@ -293,6 +293,7 @@ __device__ void combine_row(const Plan &P, const Inputs &in, const Outputs &out,
                             int wave, int *list) {
     const bool want_node_logits = out.node_stats != nullptr;
     if (wave == 1) {
+        if (!in.parents) return;  // rows without a tree (proposals)
         // this row's draft token under the parent row: from the parent's
         // candidates when the token is one (the numbers the mask saw), otherwise
         // (node statistics wanted) a dot product
@@ -895,7 +896,58 @@ __global__ __launch_bounds__(NT) void finish_kernel(Plan P, Inputs in, Outputs o
     verify_sequence<DT, SAMPLE>(P, in, out, smp, b, tid, sm, dyn);
 }
 
+// Proposals from the recombined heads: one workgroup per row.  The row phase
+// (wave 0) gives the row's normalisers and argmax; then the whole group draws a
+// token from the row's target and/or writes the target densely (0 off the mask).
+template <int DT>
+__global__ __launch_bounds__(NT) void propose_kernel(Plan P, Inputs in, ProposeOutputs po) {
+    __shared__ Smem sm;
+    const int row = blockIdx.x, tid = threadIdx.x;
+    Outputs out{};
+    out.row_argmax = po.argmax;
+    combine_row<DT>(P, in, out, row, tid % kWaveSize, tid / kWaveSize, sm.list);
+    __syncthreads();  // the row's statistics are visible to the whole group
+    const Residual target{nullptr, nullptr, nullptr, 0, nullptr, P.V};
+    if (po.tokens) {
+        double total;
+        const int t = P.full ? full_scan(P, row, target, true, po.u[row], &total, tid, sm)
+                             : masked_scan(P, row, target, true, po.u[row], &total, tid, sm);
+        if (tid == 0) po.tokens[row] = t;
+    }
+    if (po.probs) {
+        const float *rj = P.rowinfo + (size_t)row * kRowInfo;
+        const float thr = rj[RI_THRESH], lse_p = rj[RI_LSEP], lse_q = rj[RI_LSEQ], logZ = rj[RI_LOGZ];
+        float *dst = po.probs + (size_t)row * P.V;
+        if (P.full) {
+            const float *zp = P.zp_full + (size_t)row * P.zstride, *zq = P.zq_full + (size_t)row * P.zstride;
+            for (int t = tid; t < P.V; t += NT)
+                dst[t] = __expf((1.f + P.s) * (zp[t] - lse_p) - P.s * (zq[t] - lse_q) - logZ);
+        } else {
+            const int *tc = P.tcount + (size_t)row * P.ntiles;
+            const uint32_t *bits = P.bits + (size_t)row * P.wstride;
+            const float2 *cz = P.cand + (size_t)row * P.V;
+            for (int t = tid; t < P.V; t += NT) {
+                float v = 0.f;
+                // bitmap words are valid only in tiles that kept candidates
+                if (tc[t / kTileTokens] > 0 && (bits[t >> 5] >> (t & 31) & 1u)) {
+                    const float2 c = cz[t];
+                    if (c.x >= thr) v = __expf((1.f + P.s) * (c.x - lse_p) - P.s * (c.y - lse_q) - logZ);
+                }
+                dst[t] = v;
+            }
+        }
+    }
+}
+
 }  // namespace
+
+hipError_t launch_propose(const Plan &p, const Inputs &in, const ProposeOutputs &out, hipStream_t st) {
+    if (p.dtype == kBF16)
+        hipLaunchKernelGGL((propose_kernel<kBF16>), dim3(p.R), dim3(NT), 0, st, p, in, out);
+    else
+        hipLaunchKernelGGL((propose_kernel<kF32>), dim3(p.R), dim3(NT), 0, st, p, in, out);
+    return hipGetLastError();
+}
 
 // dynamic LDS of the sequence phase: parents, tokens and row argmax (12 bytes per
 // node); sampled also the walk's state: target and proposal probability of each

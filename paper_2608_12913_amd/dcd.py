@@ -21,7 +21,7 @@ ROW_MAX_P, ROW_LSE_P, ROW_LSE_Q, ROW_LOGZ, ROW_TOP1, ROW_MARGIN, ROW_COUNT, ROW_
 NODE_LOGP_P, NODE_LOGP_Q, NODE_CD, NODE_LOGP_CD, NODE_IN_MASK, NODE_RATIO = range(6)
 
 EXPORTS = ("dcd_workspace_bytes", "dcd_verify_greedy", "dcd_verify_sample",
-           "dcd_lmhead_partials", "dcd_error_string", "dcd_abi_version",
+           "dcd_lmhead_partials", "dcd_propose", "dcd_error_string", "dcd_abi_version",
            # include/dcd_probe.h
            "dcd_probe_stream_read", "dcd_probe_mfma_bf16")
 
@@ -69,6 +69,9 @@ def lib() -> ctypes.CDLL:
         L.dcd_verify_sample.argtypes = [ctypes.POINTER(Problem), ctypes.POINTER(Inputs), P, P, P,
                                         ctypes.POINTER(Outputs), P, ctypes.c_size_t, P]
         L.dcd_verify_sample.restype = ctypes.c_int
+        L.dcd_propose.argtypes = [ctypes.POINTER(Problem), ctypes.POINTER(Inputs), P, P, P, P, P,
+                                  ctypes.c_size_t, P]
+        L.dcd_propose.restype = ctypes.c_int
         L.dcd_lmhead_partials.argtypes = [ctypes.POINTER(Problem), ctypes.POINTER(Inputs),
                                           ctypes.c_int, P, ctypes.c_size_t, P]
         L.dcd_lmhead_partials.restype = ctypes.c_int
@@ -171,3 +174,11 @@ def probe_mfma_bf16(workgroups: int, iters: int, sink, stream=None) -> float:
 def _check(rc: int) -> None:
     if rc != DCD_OK:
         raise DcdError(rc)
+
+
+def propose(problem: Problem, inputs: Inputs, u, tokens, probs, argmax, workspace,
+            workspace_bytes: int, stream=None) -> None:
+    """Enqueue dcd_propose (outputs may be None, but not all three)."""
+    _check(lib().dcd_propose(ctypes.byref(problem), ctypes.byref(inputs), ptr(u), ptr(tokens),
+                             ptr(probs), ptr(argmax), ptr(workspace), int(workspace_bytes),
+                             _stream(stream)))

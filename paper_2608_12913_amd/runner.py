@@ -84,6 +84,22 @@ class DeviceProblem:
             dcd.verify_sample(self.problem, self.inputs, self.draft_probs, self.u_acc, self.u_res,
                               self.outputs, self.workspace, self.ws_bytes, stream)
 
+    def propose(self, u, want_probs=True) -> dict:
+        """dcd_propose on this problem's heads (the expert slots hold one drafter head,
+        the amateur slots the other); synchronous, host copies of the outputs."""
+        R, V = self.B * self.N, self.V
+        i32 = dict(dtype=torch.int32, device=self.device)
+        u = torch.from_numpy(np.asarray(u, np.float32)).to(self.device)
+        tokens, argmax = torch.empty(R, **i32), torch.empty(R, **i32)
+        probs = torch.empty(R, V, dtype=torch.float32, device=self.device) if want_probs else None
+        dcd.propose(self.problem, self.inputs, u, tokens, probs, argmax, self.workspace,
+                    self.ws_bytes, torch.cuda.current_stream(self.device))
+        torch.cuda.synchronize(self.device)
+        out = dict(tokens=tokens.cpu().numpy(), argmax=argmax.cpu().numpy())
+        if probs is not None:
+            out["probs"] = probs.cpu().numpy()
+        return out
+
     def launch_lmhead(self, mode: str, stream=None) -> None:
         """Enqueue only the LM-head projection stage (the dominant kernel)."""
         if stream is None:

@@ -27,7 +27,7 @@ def test_library_exports_every_declared_function():
     L = dcd.lib()
     for n in names:
         assert hasattr(L, n), n
-    assert L.dcd_abi_version() == 3
+    assert L.dcd_abi_version() == 4
 
 
 def test_struct_layouts_match_the_header(tmp_path):
@@ -157,3 +157,23 @@ def test_probe_host_validation():
     assert L.dcd_probe_mfma_bf16(0, 10, a, ctypes.byref(flops), None) == dcd.DCD_ERR_SHAPE
     assert L.dcd_probe_mfma_bf16(4, 0, a, ctypes.byref(flops), None) == dcd.DCD_ERR_SHAPE
     assert L.dcd_probe_mfma_bf16(4, 10, None, ctypes.byref(flops), None) == dcd.DCD_ERR_NULL
+
+
+def test_propose_host_validation():
+    """dcd_propose rejects a call without outputs, a draw without uniforms, misaligned
+    buffers and a short workspace before any launch."""
+    buf, a = _fake_ptrs()
+    p = _problem(nodes=8, vocab=1024, d_expert=256, d_amateur=128)
+    need = dcd.workspace_bytes(p)
+    ins = dcd.Inputs(a, a, a, a, None, None, None, None)  # no tree needed
+
+    def call(u, tokens, probs, argmax, ws=a, n=need, i=ins):
+        return dcd.lib().dcd_propose(ctypes.byref(p), ctypes.byref(i), u, tokens, probs, argmax,
+                                     ws, n, None)
+
+    assert call(None, None, None, None) == dcd.DCD_ERR_NULL
+    assert call(None, a, None, None) == dcd.DCD_ERR_NULL        # tokens need u
+    assert call(a, a + 2, None, None) == dcd.DCD_ERR_ALIGN
+    assert call(None, None, a + 1, None) == dcd.DCD_ERR_ALIGN
+    assert call(None, None, None, a, n=need - 1) == dcd.DCD_ERR_WORKSPACE
+    assert call(None, None, None, a, i=dcd.Inputs(a, None, a, a, None, None, None, None)) == dcd.DCD_ERR_NULL

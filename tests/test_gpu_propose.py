@@ -1,0 +1,103 @@
+"""GPU parity of dcd_propose (the decomposed dual-drafter's recombined proposals)
+against the CPU oracle, through the C ABI."""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2608_12913_amd import synth
+from tests import parity
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2608_12913_amd import dcd
+    dcd.lib()
+
+
+def _drafter_heads(case, rng, noise=0.3):
+    """Stand-in drafter heads: perturbed copies of the two models' heads (the
+    drafter itself is outside the library), rounded to the case's dtype."""
+    out = []
+    for w in (case.wp, case.wq):
+        wf = oracle.as_f32(w)
+        wf = wf + np.float32(noise) * rng.standard_normal(wf.shape).astype(np.float32) / np.float32(np.sqrt(wf.shape[1]))
+        out.append(synth.bf16_bits(wf) if case.dtype == "bf16" else wf.astype(np.float32))
+    return out
+
+
+def _check(case, u, label):
+    from paper_2608_12913_amd.runner import DeviceProblem
+    print(f"[propose] {label}: R={case.R} V={case.V} {case.dtype} theta={case.theta} s={case.s} "
+          f"T={case.T}", flush=True)
+    o = oracle.propose(case.hp, case.hq, case.wp, case.wq, case.bias, case.bias, u, theta=case.theta,
+                       s=case.s, temperature=case.T)
+    rows = oracle.eval_rows(case.hp, case.hq, case.wp, case.wq, case.bias, case.bias,
+                            theta=case.theta, s=case.s, temperature=case.T)
+    amb = (rows["stats"][:, oracle.RS_MARGIN] <= parity.MARGIN_GATE) | (rows["gap"] <= parity.BOUNDARY_GATE)
+    dev = DeviceProblem.from_case(case, np.zeros((case.B, case.N), np.int32), row_outputs=False,
+                                  T=case.T)
+    g = dev.propose(u)
+    ok = ~amb
+    # support exactly, log-probabilities within the parity tolerance
+    pg, po = g["probs"].astype(np.float64), o["probs"]
+    assert np.array_equal(pg[ok] > 0, po[ok] > 0), "support"
+    sup = ok[:, None] & (po > 1e-30)
+    d = np.abs(np.log(pg[sup]) - np.log(po[sup]))
+    assert d.max() <= parity.ATOL, f"log-prob max diff {d.max()}"
+    np.testing.assert_allclose(pg[ok].sum(axis=1), 1.0, atol=1e-4)
+    assert np.array_equal(g["argmax"][ok], o["argmax"][ok])
+    clear = ok & (o["gap"] > parity.CDF_GATE)
+    assert np.array_equal(g["tokens"][clear], o["tokens"][clear]), "drawn tokens"
+    print(f"[propose] {label}: ok, {int(ok.sum())}/{case.R} rows compared, "
+          f"{int(clear.sum())} draws", flush=True)
+    return g, o
+
+
+@pytest.mark.parametrize("theta,T", [(0.1, 1.0), (0.0, 1.0), (0.05, 0.7)])
+def test_propose_drafter_heads_ragged(theta, T):
+    rng = np.random.default_rng(60)
+    case = synth.make_case("s8_chain16x8", 60, B=6, N=8, V=4099, dp=256, dq=128, theta=theta, T=T)
+    case.wp, case.wq = _drafter_heads(case, rng)
+    u = rng.random(case.R).astype(np.float32)
+    _check(case, u, f"drafter heads theta {theta} T {T}")
+
+
+def test_propose_fp32_ragged_k():
+    case = synth.make_case("tiny_chain8", 61, N=19, V=777, dp=100, dq=36, theta=0.02)
+    u = np.random.default_rng(61).random(case.R).astype(np.float32)
+    _check(case, u, "fp32")
+
+
+def test_proposals_feed_sampled_verification():
+    """End to end: the proposal distribution of row i drafts node i+1 of a chain; the
+    proposals' own probabilities then serve as draft_probs of dcd_verify_sample."""
+    from paper_2608_12913_amd.runner import DeviceProblem
+    rng = np.random.default_rng(62)
+    case = synth.make_case("s8_chain16x8", 62, B=4, N=8, V=2000, dp=256, dq=128, theta=0.1)
+    drafter = synth.make_case("s8_chain16x8", 62, B=4, N=8, V=2000, dp=256, dq=128, theta=0.1)
+    drafter.wp, drafter.wq = _drafter_heads(case, rng)
+    u = rng.random(case.R).astype(np.float32)
+    dev = DeviceProblem.from_case(drafter, np.zeros((case.B, case.N), np.int32), row_outputs=False)
+    g = dev.propose(u)
+    tokens = np.zeros((case.B, case.N), np.int32)
+    probs = np.zeros((case.R, case.V), np.float32)
+    for b in range(case.B):
+        for i in range(1, case.N):
+            tokens[b, i] = g["tokens"][b * case.N + i - 1]
+            probs[b * case.N + i] = g["probs"][b * case.N + i - 1]
+    assert np.all(tokens[:, 1:] >= 0)
+    o = oracle.verify("sample", case.B, case.N, case.hp, case.hq, case.wp, case.wq, case.bias,
+                      case.bias, case.parents, tokens, theta=case.theta, s=case.s, temperature=case.T,
+                      draft_probs=probs, u_acc=case.u_acc, u_res=case.u_res)
+    v = DeviceProblem.from_case(case, tokens, draft_probs=probs).run("sample")
+    report = {}
+    amb = parity.compare_rows(v, o, np.arange(case.R), report)
+    parity.compare_sample(v, o, case.parents, case.u_acc, tokens, o["row_gap"] <= parity.BOUNDARY_GATE,
+                          report)
+    print(f"[propose] feeding verification: {report}, accept lengths {v['accept_len'].tolist()}",
+          flush=True)
