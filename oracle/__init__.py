@@ -58,6 +58,8 @@ def _load():
         lib.dco_propose.argtypes = [i32, i32, i32, i32, P, P, P, P, P, P, f64, f64, f64, P, P, P, P,
                                     P, i32]
         lib.dco_propose.restype = i32
+        lib.dco_rmsnorm.argtypes = [i32, i32, P, P, f64, i32, P]
+        lib.dco_rmsnorm.restype = None
         lib.dco_greedy_walk.argtypes = [i32, P, P, P, P, P, P]
         lib.dco_greedy_walk.restype = None
         lib.dco_sample_tree.argtypes = [i32, i32, P, P, P, P, P, P, P, P, P, P, P, P]
@@ -134,6 +136,19 @@ def propose(he, hf, we, wf, be, bf, u, *, theta, s, temperature=1.0, nthreads=0)
     if rc:
         raise RuntimeError(f"dco_propose failed ({rc})")
     return o
+
+
+def rmsnorm(x, g, eps):
+    """Final RMS normalisation of the rows of x with scale g; bf16 data (uint16 bit
+    patterns) stays bf16 (returned as uint16 bits), fp32 stays fp32."""
+    bf16 = np.asarray(x).dtype == np.uint16
+    xf, gf = as_f32(x), as_f32(g)
+    R, d = xf.shape
+    y = np.empty((R, d), np.float32)
+    _load().dco_rmsnorm(R, d, _p(xf), _p(gf), float(eps), int(bf16), _p(y))
+    if bf16:
+        return (y.view(np.uint32) >> 16).astype(np.uint16)
+    return y
 
 
 def greedy_walk(parents, tokens, row_argmax):

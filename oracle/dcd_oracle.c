@@ -31,6 +31,10 @@
  *                       two drafter heads, pi_hat ~ pi_e^(1+s) pi_f^(-s) (with
  *                       the same mask), as a proposal distribution per row and a
  *                       token drawn from it.
+ *   dco_rmsnorm         the models' final RMS normalisation, the step that produces
+ *                       the hidden states the LM heads read (Alg. 1's model
+ *                       evaluation ends with it in the Llama-family models the
+ *                       paper uses).
  *   dco_greedy_walk     greedy (T = 0) verification of a draft tree: a draft
  *                       token is accepted iff it equals the target's argmax
  *                       (Alg. 1 with a one-hot target), walked from the root.
@@ -51,7 +55,10 @@
  *     that sums to zero (rounding only) leaves the distribution as it was;
  *   - siblings are tried in increasing node index;
  *   - temperature divides both models' logits before everything (sampled mode);
- *     greedy mode uses the models' own distributions (T = 1).
+ *     greedy mode uses the models' own distributions (T = 1);
+ *   - final RMS normalisation: y = g * round(x / sqrt(mean(x^2) + eps)) with both the
+ *     normalised value and the product rounded to the input's type (bf16 inputs;
+ *     no rounding for fp32), as Llama-family implementations compute it.
  */
 #include <math.h>
 #include <stdint.h>
@@ -253,6 +260,40 @@ int dco_eval_rows(int V, int dp, int dq,
     free(zp);
     free(zq);
     return 0;
+}
+
+/* round-to-nearest-even of a double to bf16 (8 significant bits), returned as double */
+static double round_bf16(double x)
+{
+    if (!isfinite(x) || x == 0.0) return x;
+    int e;
+    const double m = frexp(x, &e);           /* x = m * 2^e, 0.5 <= |m| < 1 */
+    const double scaled = ldexp(m, 8);       /* 8 significant bits before the point */
+    double r = nearbyint(scaled);            /* ties to even in the default rounding mode */
+    return ldexp(r, e - 8);
+}
+
+/*
+ * Final RMS normalisation of R rows of width d (the step before the LM heads):
+ *   r = 1 / sqrt(mean_k x_k^2 + eps);  y_k = g_k * [x_k * r]
+ * For bf16 data ([.] and the product rounded to bf16, round-to-nearest-even; the
+ * rows, g and y hold bf16 values as floats) and without rounding for fp32.
+ */
+void dco_rmsnorm(int R, int d, const float *x, const float *g, double eps, int bf16, float *y)
+{
+    for (long r = 0; r < R; ++r) {
+        const float *xr = x + (size_t)r * d;
+        double ss = 0.0;
+        for (int k = 0; k < d; ++k) ss += (double)xr[k] * (double)xr[k];
+        const double inv = 1.0 / sqrt(ss / d + eps);
+        for (int k = 0; k < d; ++k) {
+            double v = (double)xr[k] * inv;
+            if (bf16) v = round_bf16(v);
+            v *= (double)g[k];
+            if (bf16) v = round_bf16(v);
+            y[(size_t)r * d + k] = (float)v;
+        }
+    }
 }
 
 /*

@@ -415,6 +415,56 @@ def test_propose_draw_follows_the_distribution():
     assert np.all(o["probs"][0][freq > 0] > 0)
 
 
+# ---------------------------------------------------------------- final RMS normalisation
+def test_rmsnorm_closed_forms():
+    """Constant rows normalise to 1, so the output is g itself; a one-hot row of width
+    64 normalises to +-sqrt(64) = 8, so the output is 8 g at that column and 0
+    elsewhere; a power-of-two scale of the rows changes nothing (eps = 0).  All exact
+    in bf16."""
+    rng = np.random.default_rng(19)
+    d = 64
+    g = synth.bf16_bits(rng.standard_normal(d).astype(np.float32))
+    gf = oracle.as_f32(g)
+    x = synth.bf16_bits(np.full((3, d), [[3.0], [-0.5], [1024.0]], np.float32))
+    y = oracle.as_f32(oracle.rmsnorm(x, g, 1e-6))
+    np.testing.assert_array_equal(y[0], gf)
+    np.testing.assert_array_equal(y[1], -gf)
+    np.testing.assert_array_equal(y[2], gf)
+    x = np.zeros((2, d), np.float32)
+    x[0, 5], x[1, 63] = 0.75, -96.0
+    y = oracle.as_f32(oracle.rmsnorm(synth.bf16_bits(x), g, 0.0))
+    expect = np.zeros((2, d), np.float32)
+    expect[0, 5], expect[1, 63] = 8 * gf[5], -8 * gf[63]
+    np.testing.assert_array_equal(y, expect)
+    x = synth.bf16_bits(rng.standard_normal((4, d)).astype(np.float32))
+    x4 = synth.bf16_bits(oracle.as_f32(x) * np.float32(4.0))
+    np.testing.assert_array_equal(oracle.rmsnorm(x, g, 0.0), oracle.rmsnorm(x4, g, 0.0))
+
+
+def test_rmsnorm_matches_torch():
+    """fp32: torch's rms_norm in fp64.  bf16: the Llama-family reference computation in
+    torch (fp32 statistics, the normalised value cast to bf16, then scaled in bf16);
+    the oracle, in fp64, agrees bit for bit except where the fp32 rounding of the
+    reference falls on the other side of a bf16 rounding boundary (one unit)."""
+    torch = pytest.importorskip("torch")
+    rng = np.random.default_rng(20)
+    R, d, eps = 16, 512, 1e-5
+    x = (rng.standard_normal((R, d)) * 3).astype(np.float32)
+    g = (1 + 0.1 * rng.standard_normal(d)).astype(np.float32)
+    ref = torch.nn.functional.rms_norm(torch.from_numpy(x).double(), (d,), torch.from_numpy(g).double(),
+                                       eps=eps).numpy()
+    np.testing.assert_allclose(oracle.rmsnorm(x, g, eps), ref, rtol=1e-6, atol=1e-7)
+    xb, gb = synth.bf16_bits(x), synth.bf16_bits(g)
+    xt = torch.from_numpy(oracle.as_f32(xb)).to(torch.bfloat16)
+    gt = torch.from_numpy(oracle.as_f32(gb)).to(torch.bfloat16)
+    h = xt.float()
+    h = h * torch.rsqrt(h.pow(2).mean(-1, keepdim=True) + eps)
+    ref = (gt * h.to(torch.bfloat16)).float().numpy()
+    got = oracle.as_f32(oracle.rmsnorm(xb, gb, eps))
+    ulp = np.abs(got.view(np.int32) - ref.view(np.int32)) >> 16
+    assert np.all(ulp <= 1) and (ulp == 0).mean() > 0.99
+
+
 # ---------------------------------------------------------------- greedy walk
 def _parse_ints(s):
     return np.array([int(x) for x in s.split(",")], np.int32)
