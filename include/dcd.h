@@ -119,6 +119,10 @@ typedef struct {
     float cd_strength;   /* s >= 0 (finite)                                             */
     float temperature;   /* sampled mode: T > 0 divides both models' logits before
                             anything else, mask included; ignored by greedy mode         */
+    int32_t final_norm;  /* 1: h_* are the models' hidden states BEFORE their final RMS
+                            normalisation, which the call applies first (norm_* and
+                            norm_eps below); 0: h_* are already normalised            */
+    float norm_eps;      /* final_norm = 1: eps >= 0 of that normalisation            */
 } dcd_problem;
 
 typedef struct {                 /* device pointers, read only                          */
@@ -130,6 +134,13 @@ typedef struct {                 /* device pointers, read only                  
     const float *bias_amateur;   /* [V] fp32, or NULL; may alias bias_expert             */
     const int32_t *parents;      /* [B, N] parent node of each node; parents[b,0] = -1   */
     const int32_t *tokens;       /* [B, N] draft token of each node (entry 0 ignored)    */
+    /* final_norm = 1: the scales g of the models' final RMS normalisation, [d_p] and
+       [d_q] in the dtype of h_*.  Each row x becomes y = g * [x / sqrt(mean(x^2) + eps)]
+       with, for bf16, the normalised value [.] and the product rounded to bf16
+       (round to nearest even; fp32: no rounding), as Llama-family models compute
+       it; the LM heads then read y.  Unused (may be NULL) when final_norm = 0.   */
+    const void *norm_expert;
+    const void *norm_amateur;
 } dcd_inputs;
 
 typedef struct {                 /* device pointers, written by the call                 */
@@ -151,7 +162,9 @@ typedef struct {                 /* device pointers, written by the call        
 } dcd_outputs;
 
 /*
- * Bytes of device workspace a call with problem `p` needs (0 if `p` is invalid).
+ * Bytes of device workspace a call with problem `p` needs (0 if `p` is invalid);
+ * with final_norm = 1 it includes the normalised copies of h_* (B*N*(d_p + d_q)
+ * elements).
  * The workspace holds per-tile softmax partials, the candidate logits that may
  * fall inside the plausibility mask (theta > 0) or both models' dense logits
  * (theta = 0, where every token is in the support), and per-row results; it is
@@ -238,8 +251,8 @@ int dcd_lmhead_partials(const dcd_problem *p, const dcd_inputs *in, int sampled,
 /* static description of a return code (never NULL) */
 const char *dcd_error_string(int code);
 
-/* ABI version of this header: 4 (2: dcd_outputs gained row_argmax_expert and row_kl;
-   3: dcd_verify_sample takes trees; 4: dcd_propose) */
+/* ABI version of this header: 5 (2: dcd_outputs gained row_argmax_expert and row_kl;
+   3: dcd_verify_sample takes trees; 4: dcd_propose; 5: the final RMS normalisation) */
 int dcd_abi_version(void);
 
 #ifdef __cplusplus

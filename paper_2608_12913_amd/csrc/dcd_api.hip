@@ -32,7 +32,11 @@ int make_plan(const dcd_problem *p, bool sample, Plan &P) {
     if (!(p->plaus_thresh >= 0.f && p->plaus_thresh <= 1.f)) return DCD_ERR_PARAM;
     if (!(p->cd_strength >= 0.f) || !isfinite(p->cd_strength)) return DCD_ERR_PARAM;
     if (sample && (!(p->temperature > 0.f) || !isfinite(p->temperature))) return DCD_ERR_PARAM;
+    if (p->final_norm != 0 && p->final_norm != 1) return DCD_ERR_PARAM;
+    if (p->final_norm && (!(p->norm_eps >= 0.f) || !isfinite(p->norm_eps))) return DCD_ERR_PARAM;
     P = Plan{};
+    P.final_norm = p->final_norm;
+    P.norm_eps = p->norm_eps;
     P.B = p->batch;
     P.N = p->nodes;
     P.R = (int)R;
@@ -53,6 +57,24 @@ int make_plan(const dcd_problem *p, bool sample, Plan &P) {
     const long long groups = (long long)((P.ntiles + 7) / 8) * 8 * P.nrb;
     if (groups > 0x7fffffffLL) return DCD_ERR_SHAPE;
     return DCD_OK;
+}
+
+// the final RMS normalisation's scales: required (16-byte aligned) when asked for
+int check_norm(const dcd_problem *p, const dcd_inputs *in) {
+    if (!p->final_norm) return DCD_OK;
+    if (!in->norm_expert || !in->norm_amateur) return DCD_ERR_NULL;
+    if (!aligned(in->norm_expert, 16) || !aligned(in->norm_amateur, 16)) return DCD_ERR_ALIGN;
+    return DCD_OK;
+}
+
+// With the final normalisation the rows are normalised into the workspace first,
+// and every later kernel reads the normalised copies.
+hipError_t normalise(const Plan &P, Inputs &I, hipStream_t st) {
+    if (!P.final_norm) return hipSuccess;
+    const hipError_t e = launch_rmsnorm(P, I, st);
+    I.hp = P.hn_p;
+    I.hq = P.hn_q;
+    return e;
 }
 
 int check_io(const dcd_inputs *in, const dcd_outputs *out) {
@@ -80,6 +102,7 @@ int run(const dcd_problem *p, const dcd_inputs *in, const SampleInputs *smp,
     int rc = make_plan(p, smp != nullptr, P);
     if (rc) return rc;
     if ((rc = check_io(in, out))) return rc;
+    if ((rc = check_norm(p, in))) return rc;
     if (smp) {
         if (!smp->draft_probs || !smp->u_acc || !smp->u_res) return DCD_ERR_NULL;
         if (!aligned(smp->draft_probs, 4) || !aligned(smp->u_acc, 4) || !aligned(smp->u_res, 4))
@@ -90,12 +113,13 @@ int run(const dcd_problem *p, const dcd_inputs *in, const SampleInputs *smp,
     if (!aligned(ws, kAlign)) return DCD_ERR_WORKSPACE;
     workspace_layout(P, (char *)ws);
 
-    const Inputs I{in->h_expert, in->h_amateur, in->w_expert, in->w_amateur,
-                   in->bias_expert, in->bias_amateur, in->parents, in->tokens};
+    Inputs I{in->h_expert, in->h_amateur, in->w_expert, in->w_amateur, in->bias_expert,
+             in->bias_amateur, in->parents, in->tokens, in->norm_expert, in->norm_amateur};
     const Outputs O{out->accept_len,        out->accept_path, out->next_token, out->status,
                     out->row_argmax,        out->row_stats,   out->node_stats,
                     out->row_argmax_expert, out->row_kl};
     hipStream_t st = (hipStream_t)stream;
+    if (normalise(P, I, st) != hipSuccess) return DCD_ERR_HIP;
     if (launch_lmhead(P, I, st) != hipSuccess) return DCD_ERR_HIP;
     if (launch_finish(P, I, O, smp, st) != hipSuccess) return DCD_ERR_HIP;
     return DCD_OK;
@@ -111,11 +135,13 @@ int run_lmhead(const dcd_problem *p, const dcd_inputs *in, int sampled, void *ws
     if (!aligned(in->h_expert, 16) || !aligned(in->h_amateur, 16) || !aligned(in->w_expert, 16) ||
         !aligned(in->w_amateur, 16) || !aligned(in->bias_expert, 4) || !aligned(in->bias_amateur, 4))
         return DCD_ERR_ALIGN;
+    if ((rc = check_norm(p, in))) return rc;
     const size_t need = workspace_layout(P, nullptr);
     if (!ws || ws_bytes < need || !aligned(ws, kAlign)) return DCD_ERR_WORKSPACE;
     workspace_layout(P, (char *)ws);
-    const Inputs I{in->h_expert, in->h_amateur, in->w_expert, in->w_amateur,
-                   in->bias_expert, in->bias_amateur, in->parents, in->tokens};
+    Inputs I{in->h_expert, in->h_amateur, in->w_expert, in->w_amateur, in->bias_expert,
+             in->bias_amateur, in->parents, in->tokens, in->norm_expert, in->norm_amateur};
+    if (normalise(P, I, (hipStream_t)stream) != hipSuccess) return DCD_ERR_HIP;
     return launch_lmhead(P, I, (hipStream_t)stream) == hipSuccess ? DCD_OK : DCD_ERR_HIP;
 }
 
@@ -128,6 +154,7 @@ int run_propose(const dcd_problem *p, const dcd_inputs *in, const ProposeOutputs
     if (!in->h_expert || !in->h_amateur || !in->w_expert || !in->w_amateur) return DCD_ERR_NULL;
     if (!o.tokens && !o.probs && !o.argmax) return DCD_ERR_NULL;
     if (o.tokens && !o.u) return DCD_ERR_NULL;
+    if ((rc = check_norm(p, in))) return rc;
     if (!aligned(in->h_expert, 16) || !aligned(in->h_amateur, 16) || !aligned(in->w_expert, 16) ||
         !aligned(in->w_amateur, 16) || !aligned(in->bias_expert, 4) || !aligned(in->bias_amateur, 4) ||
         !aligned(o.u, 4) || !aligned(o.tokens, 4) || !aligned(o.probs, 4) || !aligned(o.argmax, 4))
@@ -135,9 +162,10 @@ int run_propose(const dcd_problem *p, const dcd_inputs *in, const ProposeOutputs
     const size_t need = workspace_layout(P, nullptr);
     if (!ws || ws_bytes < need || !aligned(ws, kAlign)) return DCD_ERR_WORKSPACE;
     workspace_layout(P, (char *)ws);
-    const Inputs I{in->h_expert, in->h_amateur, in->w_expert, in->w_amateur,
-                   in->bias_expert, in->bias_amateur, nullptr, nullptr};
+    Inputs I{in->h_expert, in->h_amateur, in->w_expert, in->w_amateur, in->bias_expert,
+             in->bias_amateur, nullptr, nullptr, in->norm_expert, in->norm_amateur};
     hipStream_t st = (hipStream_t)stream;
+    if (normalise(P, I, st) != hipSuccess) return DCD_ERR_HIP;
     if (launch_lmhead(P, I, st) != hipSuccess) return DCD_ERR_HIP;
     if (launch_propose(P, I, o, st) != hipSuccess) return DCD_ERR_HIP;
     return DCD_OK;
@@ -167,6 +195,11 @@ size_t workspace_layout(Plan &p, char *base) {
     p.bound = (int *)take(R * sizeof(int));
     p.nodez = (float4 *)take(R * sizeof(float4));
     p.seqdone = (int *)take((size_t)p.B * sizeof(int));
+    if (p.final_norm) {
+        const size_t esz = p.dtype == kBF16 ? 2 : 4;
+        p.hn_p = take(R * p.dp * esz);
+        p.hn_q = take(R * p.dq * esz);
+    }
     return off;
 }
 
@@ -218,6 +251,6 @@ const char *dcd_error_string(int code) {
     }
 }
 
-int dcd_abi_version(void) { return 4; }
+int dcd_abi_version(void) { return 5; }
 
 }  // extern "C"

@@ -47,6 +47,8 @@ struct Plan {
                        // no candidates, dense logits instead
     int zstride;       // ntiles * kTileTokens: row stride of the dense logit arrays
     int store_q;       // full and sampled: the amateur logits are kept for the draw
+    int final_norm;    // the rows of h_* are normalised first (into hn_p, hn_q)
+    float norm_eps;
     // workspace carve-up
     float4 *partials;  // [R][ntiles]   (max_p, sumexp_p, max_q, sumexp_q) per vocabulary tile
     // masked target (full = 0)
@@ -64,12 +66,14 @@ struct Plan {
     int *bound;        // [R]           running lower bound on max z_p (order-preserving int key)
     float4 *nodez;     // [R]           (z_p, z_q, candidate?) of node r's token under its parent row
     int *seqdone;      // [B]           rows of each sequence finished by the combine step
+    void *hn_p, *hn_q; // [R][d_p], [R][d_q] final_norm: the normalised hidden states
 };
 
 struct Inputs {
     const void *hp, *hq, *wp, *wq;
     const float *bp, *bq;
     const int32_t *parents, *tokens;
+    const void *gp, *gq;  // scales of the final RMS normalisation (final_norm)
 };
 
 struct Outputs {
@@ -120,6 +124,8 @@ __device__ __forceinline__ YStat ystat_merge(const YStat &u, const YStat &v) {
 
 size_t workspace_layout(Plan &p, char *base);  // fills the pointers when base != nullptr
 
+// final RMS normalisation of both models' rows into hn_p / hn_q (final_norm)
+hipError_t launch_rmsnorm(const Plan &p, const Inputs &in, hipStream_t st);
 // LM heads with softmax partials and candidates (clears bound and seqdone first)
 hipError_t launch_lmhead(const Plan &p, const Inputs &in, hipStream_t st);
 // the many-row variant (bf16, masked target, R >= kWideMinRows): same outputs

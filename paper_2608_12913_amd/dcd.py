@@ -36,12 +36,14 @@ class Problem(ctypes.Structure):
     _fields_ = [("batch", ctypes.c_int32), ("nodes", ctypes.c_int32), ("vocab", ctypes.c_int32),
                 ("d_expert", ctypes.c_int32), ("d_amateur", ctypes.c_int32),
                 ("dtype", ctypes.c_int32), ("plaus_thresh", ctypes.c_float),
-                ("cd_strength", ctypes.c_float), ("temperature", ctypes.c_float)]
+                ("cd_strength", ctypes.c_float), ("temperature", ctypes.c_float),
+                ("final_norm", ctypes.c_int32), ("norm_eps", ctypes.c_float)]
 
 
 class Inputs(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in ("h_expert", "h_amateur", "w_expert", "w_amateur",
-                                                "bias_expert", "bias_amateur", "parents", "tokens")]
+                                                "bias_expert", "bias_amateur", "parents", "tokens",
+                                                "norm_expert", "norm_amateur")]
 
 
 class Outputs(ctypes.Structure):
@@ -110,16 +112,16 @@ def _stream(stream) -> int | None:
 
 
 def make_problem(batch, nodes, vocab, d_expert, d_amateur, dtype="bf16", plaus_thresh=0.1,
-                 cd_strength=0.5, temperature=1.0) -> Problem:
+                 cd_strength=0.5, temperature=1.0, final_norm=False, norm_eps=0.0) -> Problem:
     dt = {"bf16": DCD_BF16, "f32": DCD_F32}.get(dtype, dtype)
     return Problem(batch, nodes, vocab, d_expert, d_amateur, dt, plaus_thresh, cd_strength,
-                   temperature)
+                   temperature, int(bool(final_norm)), norm_eps)
 
 
 def make_inputs(h_expert, h_amateur, w_expert, w_amateur, bias_expert, bias_amateur, parents,
-                tokens) -> Inputs:
+                tokens, norm_expert=None, norm_amateur=None) -> Inputs:
     return Inputs(*(ptr(a) for a in (h_expert, h_amateur, w_expert, w_amateur, bias_expert,
-                                     bias_amateur, parents, tokens)))
+                                     bias_amateur, parents, tokens, norm_expert, norm_amateur)))
 
 
 def make_outputs(accept_len, accept_path, next_token, status, row_argmax=None, row_stats=None,

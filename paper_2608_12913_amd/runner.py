@@ -23,7 +23,7 @@ class DeviceProblem:
 
     def __init__(self, *, hp, hq, wp, wq, bias_p, bias_q, parents, tokens, B, N, V, dtype,
                  theta, s, T=1.0, draft_probs=None, u_acc=None, u_res=None, device="cuda:0",
-                 row_outputs=True):
+                 row_outputs=True, norm_p=None, norm_q=None, norm_eps=0.0):
         self.device = torch.device(device)
         dv = lambda a: None if a is None else _dev(a, self.device)  # noqa: E731
         self.B, self.N, self.V = B, N, V
@@ -36,7 +36,12 @@ class DeviceProblem:
         self.draft_probs = dv(None if draft_probs is None else np.asarray(draft_probs, np.float32))
         self.u_acc = dv(None if u_acc is None else np.asarray(u_acc, np.float32))
         self.u_res = dv(None if u_res is None else np.asarray(u_res, np.float32))
-        self.problem = dcd.make_problem(B, N, V, hp.shape[1], hq.shape[1], dtype, theta, s, T)
+        # norm_p / norm_q: scales of the models' final RMS normalisation; hp / hq are
+        # then the rows before it
+        self.norm_p, self.norm_q = dv(norm_p), dv(norm_q)
+        final_norm = norm_p is not None
+        self.problem = dcd.make_problem(B, N, V, hp.shape[1], hq.shape[1], dtype, theta, s, T,
+                                        final_norm, norm_eps)
         R = B * N
         i32 = dict(dtype=torch.int32, device=self.device)
         f32 = dict(dtype=torch.float32, device=self.device)
@@ -54,7 +59,7 @@ class DeviceProblem:
             raise dcd.DcdError(dcd.DCD_ERR_SHAPE)
         self.workspace = torch.empty(self.ws_bytes, dtype=torch.uint8, device=self.device)
         self.inputs = dcd.make_inputs(self.hp, self.hq, self.wp, self.wq, self.bias_p, self.bias_q,
-                                      self.parents, self.tokens)
+                                      self.parents, self.tokens, self.norm_p, self.norm_q)
         self.outputs = dcd.make_outputs(self.accept_len, self.accept_path, self.next_token,
                                         self.status, self.row_argmax, self.row_stats,
                                         self.node_stats, self.row_argmax_expert, self.row_kl)

@@ -27,7 +27,7 @@ def test_library_exports_every_declared_function():
     L = dcd.lib()
     for n in names:
         assert hasattr(L, n), n
-    assert L.dcd_abi_version() == 4
+    assert L.dcd_abi_version() == 5
 
 
 def test_struct_layouts_match_the_header(tmp_path):
@@ -177,3 +177,24 @@ def test_propose_host_validation():
     assert call(None, None, a + 1, None) == dcd.DCD_ERR_ALIGN
     assert call(None, None, None, a, n=need - 1) == dcd.DCD_ERR_WORKSPACE
     assert call(None, None, None, a, i=dcd.Inputs(a, None, a, a, None, None, None, None)) == dcd.DCD_ERR_NULL
+
+
+def test_final_norm_host_validation():
+    """The final RMS normalisation needs both scale vectors (16-byte aligned), a flag
+    of 0 or 1 and a finite eps >= 0; its workspace holds the normalised rows."""
+    buf, a = _fake_ptrs()
+    kw = dict(nodes=8, vocab=1024, d_expert=256, d_amateur=128)
+    p0 = _problem(**kw)
+    p1 = _problem(final_norm=True, norm_eps=1e-5, **kw)
+    assert dcd.workspace_bytes(p1) >= dcd.workspace_bytes(p0) + 8 * (256 + 128) * 2
+    p2 = _problem(**kw)
+    p2.final_norm = 2
+    assert dcd.workspace_bytes(p2) == 0
+    assert dcd.workspace_bytes(_problem(final_norm=True, norm_eps=-1.0, **kw)) == 0
+    assert dcd.workspace_bytes(_problem(final_norm=True, norm_eps=float("nan"), **kw)) == 0
+    need = dcd.workspace_bytes(p1)
+    out = dcd.Outputs(a, a, a, a, None, None, None)
+    assert _call_greedy(p1, dcd.Inputs(a, a, a, a, a, a, a, a), out, a, need) == dcd.DCD_ERR_NULL
+    assert _call_greedy(p1, dcd.Inputs(a, a, a, a, a, a, a, a, a, None), out, a, need) == dcd.DCD_ERR_NULL
+    assert _call_greedy(p1, dcd.Inputs(a, a, a, a, a, a, a, a, a + 4, a), out, a, need) == dcd.DCD_ERR_ALIGN
+    assert _call_greedy(p1, dcd.Inputs(a, a, a, a, a, a, a, a, a, a), out, a, need - 1) == dcd.DCD_ERR_WORKSPACE

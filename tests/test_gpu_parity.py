@@ -445,3 +445,68 @@ def test_full_b8_batch32x64():
     parity.compare_rows(g, o_spot, spot, report)
     parity.compare_diagnostics(g, o_spot, spot, case.theta, case.s, case.V, report)
     _say(f"b8_batch32x64: ok {report}")
+
+
+# ------------------------------------------------------------------ final RMS normalisation
+def _pre_norm(case, seed, eps=1e-5):
+    """Un-normalised rows (the normalised synthetic states times a per-row scale in
+    [0.5, 8]) and bf16/fp32 scales g ~ 1 + 0.1 N(0, 1); returns the normalised rows the
+    oracle computes and the inputs the library gets."""
+    rng = np.random.default_rng(seed)
+    to = (lambda a: synth.bf16_bits(a)) if case.dtype == "bf16" else (lambda a: a.astype(np.float32))
+    pre, norms, post = {}, {}, {}
+    for name, d in (("hp", case.dp), ("hq", case.dq)):
+        x = oracle.as_f32(getattr(case, name)) * rng.uniform(0.5, 8.0, (case.R, 1)).astype(np.float32)
+        pre[name] = to(x)
+        norms[name] = to((1 + 0.1 * rng.standard_normal(d)).astype(np.float32))
+        post[name] = oracle.rmsnorm(pre[name], norms[name], eps)
+    return pre, norms, post
+
+
+def _check_final_norm(case, label, mode="greedy", eps=1e-5):
+    pre, norms, post = _pre_norm(case, 70, eps)
+    _say(f"{label}: final norm, B={case.B} N={case.N} V={case.V} {case.dtype} theta={case.theta}")
+    # the oracle on the rows it normalised itself
+    case.hp, case.hq = post["hp"], post["hq"]
+    if mode == "greedy":
+        tokens = _greedy_tokens(case)
+        o = _oracle_greedy(case, tokens)
+        probs = None
+    else:
+        probs, tokens = _sampled_tree_setup(case)
+        o = oracle.verify("sample", case.B, case.N, case.hp, case.hq, case.wp, case.wq, case.bias,
+                          case.bias, case.parents, tokens, theta=case.theta, s=case.s,
+                          temperature=case.T, draft_probs=probs, u_acc=case.u_acc, u_res=case.u_res)
+    # the library on the rows before the normalisation
+    dev = _runner().from_case(case, tokens, draft_probs=probs, hp=pre["hp"], hq=pre["hq"],
+                              norm_p=norms["hp"], norm_q=norms["hq"], norm_eps=eps)
+    g = dev.run(mode)
+    report = {}
+    amb = parity.compare_rows(g, o, np.arange(case.R), report)
+    parity.compare_nodes(g, o, case.parents, amb, report)
+    if mode == "greedy":
+        parity.compare_greedy(g, o, case.parents, amb, report)
+    else:
+        parity.compare_sample(g, o, case.parents, case.u_acc, tokens,
+                              o["row_gap"] <= parity.BOUNDARY_GATE, report)
+    _say(f"{label}: ok {report}")
+
+
+def test_final_norm_masked_bf16():
+    case = synth.make_case("b8_tree64", 71, B=2, V=4099, dp=512, dq=256)
+    _check_final_norm(case, "final norm masked")
+
+
+def test_final_norm_untruncated_bf16():
+    case = synth.make_case("b8_tree64", 72, B=2, V=4099, dp=512, dq=256, theta=0.0)
+    _check_final_norm(case, "final norm untruncated")
+
+
+def test_final_norm_fp32_many_rows_and_sampled():
+    case = synth.make_case("tiny_chain8", 73, N=19, V=777, dp=100, dq=36)
+    _check_final_norm(case, "final norm fp32")
+    case = synth.make_case("b8_batch32x64", 74, B=9, V=4099, dp=512, dq=200)
+    _check_final_norm(case, "final norm many rows")
+    case = synth.make_case("s8_chain16x8", 75, B=4, N=16, tree="tree", depth=4, max_children=4,
+                           V=2000, dp=256, dq=128)
+    _check_final_norm(case, "final norm sampled trees", mode="sample")
