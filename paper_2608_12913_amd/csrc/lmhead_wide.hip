@@ -8,10 +8,11 @@
 // than for streaming: a workgroup owns 256 tokens x 256 rows and its 4 waves form
 // a 2 x 2 grid of 128 x 128 blocks (64 v_mfma_f32_16x16x32_bf16 blocks, 256 fp32
 // accumulators per lane).  K is walked in 128-byte chunks of every row; a chunk's
-// 256 weight rows and 256 hidden-state rows go through registers into one of two
-// XOR-swizzled LDS stages, one barrier per chunk.  The 8 row tiles of a
-// vocabulary tile are dispatched together on one XCD, so its weights come from
-// HBM once and from that XCD's L2 for the others (ordinary cached loads).
+// 256 weight rows and 256 hidden-state rows are loaded straight into one of two
+// XOR-swizzled LDS stages (global_load_lds) while the other stage is multiplied,
+// so the waves spend no instructions on staging; one barrier per chunk.  The 8
+// row tiles of a vocabulary tile are dispatched together on one XCD, so its
+// weights come from HBM once and from that XCD's L2 for the others.
 //
 // Epilogue: as in the 64-row kernel -- per (row, tile) the max and sum of exp of
 // both models, tile-local candidates (z_p within ln(theta) of the tile max)
@@ -45,19 +46,40 @@ static_assert(TT == 256 && TR == 256 && NT == 4 * kWaveSize, "2 x 2 waves of 128
 static_assert(LPR == RPI && LOADS * RPI == SLAB, "a load instruction covers RPI whole rows");
 static_assert(NV == 32, "one bit per logit of a row block in a 32-bit mask");
 
-// LDS: two stages of [weights 256 x CB | hidden states 256 x CB]; both biases of
-// the tile; the parked candidate logits; the epilogue scratch reuses the stages.
+// LDS: two stages of [weights 256 x CB | hidden states 256 x CB] (two separate
+// objects, so the compiler can tell the stage being multiplied from the one being
+// filled and adds no wait for the loads into the latter); both biases of the tile
+// and the parked candidate logits; the epilogue scratch reuses stage 0.
 constexpr size_t kStageBytes = 2 * OPB;
 constexpr int kStash = BR;  // one parked logit per lane and row block
-constexpr size_t kLdsBytes = 2 * kStageBytes + 2 * TT * sizeof(float) + 4 * kStash * kWaveSize * sizeof(float);
+constexpr int kMiscFloats = 2 * TT + 4 * kStash * kWaveSize;
 // epilogue scratch: (max, sum) pairs of the two token halves, candidate words and
 // counts, a row block's logits per wave
 constexpr size_t kPairsBytes = 2 * TR * sizeof(float2);
 constexpr size_t kWordsBytes = TR * kWordsPerTile * sizeof(uint32_t);
 constexpr size_t kCountBytes = TR * sizeof(int);
 constexpr size_t kZBytes = 4 * NV * kWaveSize * sizeof(float);
-static_assert(kPairsBytes + kWordsBytes + kCountBytes + kZBytes <= 2 * kStageBytes,
-              "epilogue scratch must fit the stages");
+static_assert(kPairsBytes + kWordsBytes + kCountBytes + kZBytes <= kStageBytes,
+              "epilogue scratch must fit stage 0");
+
+typedef __attribute__((address_space(3))) void *lds_ptr;
+
+// Waits until every load this wave issued has landed except the two most recent
+// (the L2 prefetch of the chunk after next; loads complete in issue order).  The
+// compiler does not track loads that write LDS directly.
+__device__ __forceinline__ void wait_chunk() { __builtin_amdgcn_s_waitcnt(0x0F72); }  // vmcnt(2)
+
+// Workgroup barrier for LDS data: the wave's LDS reads have returned (lgkmcnt)
+// before it arrives.  Unlike __syncthreads() it does not wait for direct-to-LDS
+// loads still in flight (each wave waits for its own with wait_chunk), so the next
+// chunk stays in flight across it.  The empty asm statements keep the compiler
+// from moving memory operations across.
+__device__ __forceinline__ void lds_barrier() {
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
 
 __device__ __forceinline__ u32x4 ld16(const char *p) { return *reinterpret_cast<const u32x4 *>(p); }
 __device__ __forceinline__ void st_lds(char *p, u32x4 v) { *reinterpret_cast<u32x4 *>(p) = v; }
@@ -72,19 +94,14 @@ __device__ __forceinline__ float wave_sum16_32(float x) {
     return x + __shfl_xor(x, 32);
 }
 
-// The loads of one K-chunk: this wave's quarter of the tile's weight rows and of
-// the workgroup's hidden-state rows.
-struct Batch {
-    u32x4 w[LOADS];
-    u32x4 h[LOADS];
-    bool hok;  // the hidden-state columns are inside the row (false only in the K tail)
-};
-
-// Per-thread load addresses of one model.  Lane (r, c) = (lane / LPR, lane % LPR)
-// reads 16 bytes at column c of rows RPI*q + r of the wave's slab: address =
-// wave-uniform row base + a 32-bit lane offset.  RAGGED (the tile reaches past the
-// vocabulary or past row R): rows past the end are clamped to the last one (their
-// results are discarded).
+// Per-thread load addresses of one model: a wave loads its quarter (slab) of the
+// tile's weight rows and of the workgroup's hidden-state rows.  Instruction q
+// fills the 1 KB of slab rows RPI*q .. RPI*q+RPI-1 in LDS, lane l landing at byte
+// 16 l: row RPI*q + l/LPR, slot l%LPR.  The lane reads the column that slot must
+// hold in the XOR-swizzled layout, (l%LPR) ^ (row%LPR); address = wave-uniform row
+// base + a 32-bit lane offset.  RAGGED (the tile reaches past the vocabulary or
+// past row R): rows past the end are clamped to the last one (their results are
+// discarded).
 template <bool RAGGED>
 struct Stream {
     const char *wbase, *hbase;
@@ -99,7 +116,7 @@ struct Stream {
                                          int tile0) {
         const int lane = threadIdx.x % kWaveSize, wave = threadIdx.x / kWaveSize;
         r = lane / LPR;
-        col16 = lane % LPR;
+        col16 = (lane % LPR) ^ (r % LPR);  // the slot's column (slab rows start at multiples of LPR)
         rowbytes = (uint32_t)d * 2;
         nch = (int)((rowbytes + CB - 1) / CB);
         const int ws0 = tile0 + SLAB * wave, hs0 = row0 + SLAB * wave;  // slab first rows
@@ -112,47 +129,66 @@ struct Stream {
         hlast = R - 1 - hb;
     }
 
-    // In the K tail a weight lane past the row end re-reads the row's last 16
-    // bytes (finite values) and the hidden-state columns there are zero.
-    __device__ __forceinline__ void issue(int c, Batch &b) const {
+    // Requests chunk c into LDS stage `st`.  In the K tail a lane past the row end
+    // re-reads the row's last 16 bytes (finite values); the hidden-state slots there
+    // are zeroed after arrival (zero_tail).
+    __device__ __forceinline__ void dma(int c, char *st) const {
+        const int wave = threadIdx.x / kWaveSize;
         const uint32_t col = (uint32_t)c * CB + col16 * 16;
-        const uint32_t wcol = col < rowbytes ? col : rowbytes - 16;
-        b.hok = col < rowbytes;
-        const uint32_t hcol = b.hok ? col : 0u;
+        const uint32_t kcol = col < rowbytes ? col : rowbytes - 16;
+        char *wdst = st + SLAB * wave * CB, *hdst = st + OPB + SLAB * wave * CB;
 #pragma unroll
         for (int q = 0; q < LOADS; ++q) {
-            if constexpr (RAGGED)
-                b.w[q] = ld16(wbase + (uint32_t)(min(wskip + RPI * q + r, wlast) * rowbytes + wcol));
-            else
-                b.w[q] = ld16(wbase + (size_t)q * RPI * rowbytes + (uint32_t)(r * rowbytes + wcol));
+            const char *src = RAGGED ? wbase + (uint32_t)(min(wskip + RPI * q + r, wlast) * rowbytes + kcol)
+                                     : wbase + (size_t)q * RPI * rowbytes + (uint32_t)(r * rowbytes + kcol);
+            __builtin_amdgcn_global_load_lds(src, (lds_ptr)(wdst + q * RPI * CB), 16, 0, 0);
         }
 #pragma unroll
         for (int q = 0; q < LOADS; ++q) {
-            if constexpr (RAGGED)
-                b.h[q] = ld16(hbase + (uint32_t)(min(hskip + RPI * q + r, hlast) * rowbytes + hcol));
-            else
-                b.h[q] = ld16(hbase + (size_t)q * RPI * rowbytes + (uint32_t)(r * rowbytes + hcol));
+            const char *src = RAGGED ? hbase + (uint32_t)(min(hskip + RPI * q + r, hlast) * rowbytes + kcol)
+                                     : hbase + (size_t)q * RPI * rowbytes + (uint32_t)(r * rowbytes + kcol);
+            __builtin_amdgcn_global_load_lds(src, (lds_ptr)(hdst + q * RPI * CB), 16, 0, 0);
         }
+    }
+
+    // Warms L2 with chunk c: one 4-byte load per row of the wave's slabs (a 128-byte
+    // chunk of a row is one cache line), two instructions, written to the wave's
+    // 512 bytes of `sink`, which nothing reads.  Past the last chunk it re-reads the
+    // last one.
+    __device__ __forceinline__ void prefetch(int c, char *sink) const {
+        const int lane = threadIdx.x % kWaveSize, wave = threadIdx.x / kWaveSize;
+        const uint32_t col = min((uint32_t)c * CB, rowbytes - 16);
+        const char *ws = RAGGED ? wbase + (uint32_t)(min(wskip + lane, wlast) * rowbytes + col)
+                                : wbase + (uint32_t)(lane * rowbytes + col);
+        const char *hs = RAGGED ? hbase + (uint32_t)(min(hskip + lane, hlast) * rowbytes + col)
+                                : hbase + (uint32_t)(lane * rowbytes + col);
+        static_assert(SLAB == kWaveSize, "one slab row per lane");
+        __builtin_amdgcn_global_load_lds(ws, (lds_ptr)(sink + wave * 512), 4, 0, 0);
+        __builtin_amdgcn_global_load_lds(hs, (lds_ptr)(sink + wave * 512 + 256), 4, 0, 0);
+    }
+
+    // After chunk c (the last, when rows end inside it) has landed in `st`: the
+    // wave's hidden-state slots past the row end become zero, so the re-read
+    // weights there multiply zeros.
+    __device__ __forceinline__ void zero_tail(int c, char *st) const {
+        if ((uint32_t)(c + 1) * CB <= rowbytes) return;  // workgroup-uniform
+        const int lane = threadIdx.x % kWaveSize, wave = threadIdx.x / kWaveSize;
+        if ((uint32_t)c * CB + col16 * 16 < rowbytes) return;
+        char *hdst = st + OPB + SLAB * wave * CB + lane * 16;
+#pragma unroll
+        for (int q = 0; q < LOADS; ++q) st_lds(hdst + q * RPI * CB, u32x4{0u, 0u, 0u, 0u});
     }
 };
 
 // 16-byte column c of row m of a swizzled [256][CB] operand tile
 __device__ __forceinline__ int swz(int m, int c) { return m * CB + ((c ^ (m % LPR)) << 4); }
 
-// arrived batch -> stage `st` (weights, then hidden states; zero in the K tail)
-__device__ __forceinline__ void stage(const Batch &b, char *st) {
-    const int lane = threadIdx.x % kWaveSize, wave = threadIdx.x / kWaveSize;
-    const int off = swz(SLAB * wave + lane / LPR, lane % LPR);
-#pragma unroll
-    for (int q = 0; q < LOADS; ++q) st_lds(st + off + q * RPI * CB, b.w[q]);
-#pragma unroll
-    for (int q = 0; q < LOADS; ++q)
-        st_lds(st + OPB + off + q * RPI * CB, b.hok ? b.h[q] : u32x4{0u, 0u, 0u, 0u});
-}
-
 // The wave's 128 x 128 block over one staged chunk.  A = weights (tokens as M),
 // B = hidden states (rows as N); lane l supplies row l%16 of a block and K columns
-// 8*(l/16).. of the k-step.
+// 8*(l/16).. of the k-step.  All 16 fragments of a k-step are read first, into
+// registers of their own: the MFMAs of one token block then never wait behind the
+// reads of the next (with registers reused, each block's reads could only start
+// once the previous block's MFMAs had taken their operands).
 __device__ __forceinline__ void compute(const char *st, int wt, int wr, f32x4 (&acc)[BV][BR]) {
     const int lane = threadIdx.x % kWaveSize, n = lane % 16, g = lane / 16;
     const char *wb = st + (wt * WT + n) * CB, *hb = st + OPB + (wr * WR + n) * CB;
@@ -161,48 +197,55 @@ __device__ __forceinline__ void compute(const char *st, int wt, int wr, f32x4 (&
 #pragma unroll 1
     for (int s = 0; s < KS; ++s) {
         const int col = ((4 * s + g) ^ (n % LPR)) << 4;
-        u32x4 bfr[BR];
+        u32x4 afr[BV], bfr[BR];
 #pragma unroll
         for (int rb = 0; rb < BR; ++rb) bfr[rb] = ld_lds(hb + 16 * rb * CB + col);
 #pragma unroll
-        for (int vb = 0; vb < BV; ++vb) {
-            const bf16x8 a = __builtin_bit_cast(bf16x8, ld_lds(wb + 16 * vb * CB + col));
+        for (int vb = 0; vb < BV; ++vb) afr[vb] = ld_lds(wb + 16 * vb * CB + col);
+        __builtin_amdgcn_sched_barrier(0);  // keep every read ahead of the MFMAs
+#pragma unroll
+        for (int vb = 0; vb < BV; ++vb)
 #pragma unroll
             for (int rb = 0; rb < BR; ++rb)
-                acc[vb][rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, __builtin_bit_cast(bf16x8, bfr[rb]),
+                acc[vb][rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, afr[vb]),
+                                                                      __builtin_bit_cast(bf16x8, bfr[rb]),
                                                                       acc[vb][rb], 0, 0, 0);
-        }
     }
 }
 
-// One pass over a model's K chunks, one batch in flight: stage chunk c into stage
-// c % 2, request chunk c+1, compute chunk c.  One barrier per chunk suffices: the
-// stage chunk c+1 goes to was last read by chunk c-1, which every wave finished
-// before passing chunk c's barrier.  Batch b holds chunk 0 on entry; if `next` is
-// given its chunk 0 is requested after the last chunk was staged.
+// One pass over a model's K chunks: chunk c is multiplied from stage `first` (c
+// even) or `second` (c odd) while chunk c+1 loads into the other and chunk c+2 is
+// pulled into L2 (so that its own loads, one chunk later, hit L2: with only two
+// stages the loads of one chunk must land within one chunk's MFMAs).  One barrier
+// per chunk: before it every wave has waited for its own loads of chunk c (so the
+// stage is complete) and finished multiplying chunk c-1 (so the other stage is
+// free for chunk c+1).  The caller requested chunk 0 into `first` and prefetched
+// chunk 1, the two last loads it issued before any other; no load into a stage is
+// in flight on return and every wave is done with both stages.
 template <bool RAGGED>
-__device__ __forceinline__ void run_pass(const Stream<RAGGED> &st, const Stream<RAGGED> *next, Batch &b,
-                                         char *lds, int wt, int wr, f32x4 (&acc)[BV][BR]) {
+__device__ __forceinline__ void run_pass(const Stream<RAGGED> &st, char *first, char *second, char *sink,
+                                         int wt, int wr, f32x4 (&acc)[BV][BR]) {
 #pragma unroll
     for (int vb = 0; vb < BV; ++vb)
 #pragma unroll
         for (int rb = 0; rb < BR; ++rb) acc[vb][rb] = f32x4{0.f, 0.f, 0.f, 0.f};
-    int c = 0;
-    for (; c + 1 < st.nch; ++c) {
-        char *sg = lds + (c & 1) * kStageBytes;
-        stage(b, sg);
-        st.issue(c + 1, b);
-        __builtin_amdgcn_sched_barrier(0);
-        __syncthreads();
-        compute(sg, wt, wr, acc);
+    for (int c = 0;;) {
+        wait_chunk();
+        st.zero_tail(c, first);
+        lds_barrier();
+        if (c + 1 < st.nch) st.dma(c + 1, second);  // workgroup-uniform
+        st.prefetch(c + 2, sink);
+        compute(first, wt, wr, acc);
+        if (++c >= st.nch) break;
+        wait_chunk();
+        st.zero_tail(c, second);
+        lds_barrier();
+        if (c + 1 < st.nch) st.dma(c + 1, first);
+        st.prefetch(c + 2, sink);
+        compute(second, wt, wr, acc);
+        if (++c >= st.nch) break;
     }
-    char *sg = lds + (c & 1) * kStageBytes;
-    stage(b, sg);
-    if (next) next->issue(0, b);
-    __builtin_amdgcn_sched_barrier(0);
-    __syncthreads();
-    compute(sg, wt, wr, acc);
-    __syncthreads();  // the stages are reused by the epilogue
+    lds_barrier();
 }
 
 // Logits of row block rb for this lane (token 16vb + 4g + j of the wave's half,
@@ -268,7 +311,8 @@ __device__ __forceinline__ void tile_softmax(const f32x4 (&acc)[BV][BR], const f
 }
 
 template <bool RAGGED>
-__device__ __forceinline__ void wide_tile(const Plan &P, const Inputs &in, int tile, int row0, char *lds) {
+__device__ __forceinline__ void wide_tile(const Plan &P, const Inputs &in, int tile, int row0, char *s0,
+                                          char *s1, float *misc, char *sink) {
     const int tid = threadIdx.x, lane = tid % kWaveSize;
     const int wave = __builtin_amdgcn_readfirstlane(tid / kWaveSize);
     const int wt = wave & 1, wr = wave >> 1;
@@ -276,7 +320,8 @@ __device__ __forceinline__ void wide_tile(const Plan &P, const Inputs &in, int t
     const int tile0 = tile * TT;
     const int tok0 = tile0 + wt * WT;  // first token of the wave's half
 
-    float *bias_p = reinterpret_cast<float *>(lds + 2 * kStageBytes);  // [TT]
+    char *lds = s0;                                                   // epilogue scratch
+    float *bias_p = misc;                                             // [TT]
     float *bias_q = bias_p + TT;                                      // [TT]
     float *stash = bias_q + TT + wave * kStash * kWaveSize;           // [BR][64]
     float2 *pairs = reinterpret_cast<float2 *>(lds);                  // [2][TR]
@@ -297,11 +342,14 @@ __device__ __forceinline__ void wide_tile(const Plan &P, const Inputs &in, int t
     f32x4 acc[BV][BR];
     float pmax[BR], psum[BR], qmax[BR], qsum[BR];
     uint32_t flags[BR];  // bit vb*4 + j: tile-local candidate
-    Batch b;
 
-    // ---- expert head
-    sp.issue(0, b);
-    run_pass<RAGGED>(sp, nullptr, b, lds, wt, wr, acc);
+    // ---- expert head (chunks from stage 0, 1, 0, ...); the amateur head's first
+    // chunk then loads into stage 1 while the expert epilogue uses stage 0
+    sp.dma(0, s0);
+    sp.prefetch(1, sink);
+    run_pass<RAGGED>(sp, s0, s1, sink, wt, wr, acc);
+    sq.dma(0, s1);
+    sq.prefetch(1, sink);
     const float *bias = bias_p + wt * WT;  // this wave's half of the tile (then bias_q's)
     tile_softmax<RAGGED>(acc, bias, P.inv_T, tok0, P.V, wt, wr, pairs, pmax, psum);
     // tile-local candidates; the lane's first of each row block waits in its LDS
@@ -341,11 +389,9 @@ __device__ __forceinline__ void wide_tile(const Plan &P, const Inputs &in, int t
         if (wt == 0 && g == 0 && row < P.R) atomicMax(&P.bound[row], ordered_key(pmax[rb]));
     }
 
-    // ---- amateur head (its first staging overwrites the logit buffers of waves
-    // that may still be in the loop above)
-    sq.issue(0, b);
-    __syncthreads();
-    run_pass<RAGGED>(sq, nullptr, b, lds, wt, wr, acc);
+    // ---- amateur head (chunks from stage 1, 0, 1, ...: its second chunk loads into
+    // stage 0 only after the barrier that follows every wave's expert epilogue)
+    run_pass<RAGGED>(sq, s1, s0, sink, wt, wr, acc);
     float bnd[BR];
 #pragma unroll
     for (int rb = 0; rb < BR; ++rb) {
@@ -404,7 +450,10 @@ __device__ __forceinline__ void wide_tile(const Plan &P, const Inputs &in, int t
 }
 
 __global__ __launch_bounds__(NT, 1) void lmhead_wide_kernel(Plan P, Inputs in) {
-    extern __shared__ __align__(16) char lds[];
+    __shared__ __align__(16) char stage0[kStageBytes];
+    __shared__ __align__(16) char stage1[kStageBytes];
+    __shared__ __align__(16) float misc[kMiscFloats];
+    __shared__ __align__(16) char sink[4 * 512];  // L2 prefetches land here, unread
     // workgroup -> (vocabulary tile, row tile); the row tiles of one vocabulary tile
     // are dispatched back to back on the same XCD (workgroup id modulo 8), so the
     // tile's weights are read from HBM once and from that XCD's L2 otherwise
@@ -414,9 +463,9 @@ __global__ __launch_bounds__(NT, 1) void lmhead_wide_kernel(Plan P, Inputs in) {
     if (tile >= P.ntiles) return;
     const int row0 = (local % nrt) * TR;
     if ((tile + 1) * TT > P.V || row0 + TR > P.R)  // workgroup-uniform
-        wide_tile<true>(P, in, tile, row0, lds);
+        wide_tile<true>(P, in, tile, row0, stage0, stage1, misc, sink);
     else
-        wide_tile<false>(P, in, tile, row0, lds);
+        wide_tile<false>(P, in, tile, row0, stage0, stage1, misc, sink);
 }
 
 }  // namespace
@@ -424,13 +473,9 @@ __global__ __launch_bounds__(NT, 1) void lmhead_wide_kernel(Plan P, Inputs in) {
 bool use_wide_lmhead(const Plan &p) { return p.dtype == kBF16 && !p.full && p.R >= kWideMinRows; }
 
 hipError_t launch_lmhead_wide(const Plan &p, const Inputs &in, hipStream_t st) {
-    static const hipError_t attr = hipFuncSetAttribute((const void *)lmhead_wide_kernel,
-                                                       hipFuncAttributeMaxDynamicSharedMemorySize,
-                                                       (int)kLdsBytes);
-    if (attr != hipSuccess) return attr;
     const int nrt = (p.R + TR - 1) / TR;
     const int groups = ((p.ntiles + 7) / 8) * 8 * nrt;
-    hipLaunchKernelGGL(lmhead_wide_kernel, dim3(groups), dim3(NT), kLdsBytes, st, p, in);
+    hipLaunchKernelGGL(lmhead_wide_kernel, dim3(groups), dim3(NT), 0, st, p, in);
     return hipGetLastError();
 }
 

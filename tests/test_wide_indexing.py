@@ -30,7 +30,8 @@ def _check(R, V, d):
     rowbytes = d * 2
     nch = (rowbytes + CB - 1) // CB
     lane = np.arange(64)
-    r, col16 = lane // LPR, lane % LPR
+    r = lane // LPR
+    col16 = (lane % LPR) ^ (r % LPR)  # the swizzled slot each lane fills
     q = np.arange(LOADS)[:, None]
     checked = 0
     for tile0, row0 in _ragged_groups(R, V):
