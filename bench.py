@@ -6,7 +6,14 @@ statistics, tree walk) over one Llama-3-8B/1B-shaped 64-node draft tree with
 every input resident in HBM.  Prints one JSON line.
 
   python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload b8_tree64]
-                  [--theta T] [--no-cpu-baseline] [--calibrate-copy BYTES]
+                  [--theta T] [--mode greedy|sample|propose] [--final-norm]
+                  [--no-cpu-baseline] [--no-probes] [--calibrate-copy BYTES]
+
+The default is the greedy verification of the workload.  --mode sample times
+dcd_verify_sample on the workload's tree (chains or trees; proposals from the
+expert's parent-row logits plus noise, as the tests draw them), --mode propose
+times dcd_propose on the workload's two heads, and --final-norm makes every call
+start with the models' final RMS normalisation.
 """
 from __future__ import annotations
 
@@ -51,6 +58,10 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--theta", type=float, default=None,
                     help="override the workload's plausibility cutoff (0 = untruncated target)")
+    ap.add_argument("--mode", choices=("greedy", "sample", "propose"), default=None,
+                    help="what to time (default: the workload's own mode)")
+    ap.add_argument("--final-norm", action="store_true",
+                    help="start every call with the models' final RMS normalisation")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-probes", action="store_true",
                     help="skip the measured read-bandwidth and MFMA-rate ceilings")
@@ -74,7 +85,7 @@ def main():
         print(json.dumps({"calibrate_copy_bytes": src.numel() * 4, "copies": 10}), flush=True)
         return
 
-    from paper_2608_12913_amd import synth
+    from paper_2608_12913_amd import dcd, synth
     from paper_2608_12913_amd.runner import DeviceProblem
 
     def log(msg):
@@ -82,44 +93,79 @@ def main():
 
     over = {} if args.theta is None else {"theta": args.theta}
     case = synth.make_case(args.workload, args.seed, **over)
-    mode = case.mode
-    if mode != "greedy":
-        raise SystemExit("bench.py times the greedy workloads")
-    log(f"{args.workload}: B={case.B} N={case.N} V={case.V} dp={case.dp} dq={case.dq}")
-
-    # draft tokens: half copy the target argmax of the parent row (taken from a first
-    # verification call on the GPU), half are uniform
-    dev = DeviceProblem.from_case(case, np.zeros((case.B, case.N), np.int32))
-    first = dev.run("greedy")
-    tokens = synth.greedy_tokens(case, first["row_argmax"])
-    dev.set_tokens(tokens)
+    mode = args.mode or case.mode
+    own_mode = mode == case.mode
+    if mode == "sample" and case.mode != "sample":  # the drafter's noise and draws
+        case = synth.make_case(args.workload, args.seed, mode="sample", **over)
+    log(f"{args.workload}: B={case.B} N={case.N} V={case.V} dp={case.dp} dq={case.dq} "
+        f"mode={mode} final_norm={args.final_norm}")
+    norm = {}
+    if args.final_norm:
+        # the synthetic rows taken as the models' last states before their final norm
+        rng = np.random.default_rng(args.seed + 1)
+        for key, d in (("norm_p", case.dp), ("norm_q", case.dq)):
+            norm[key] = synth.bf16_bits((1 + 0.1 * rng.standard_normal(d)).astype(np.float32)) \
+                if case.dtype == "bf16" else (1 + 0.1 * rng.standard_normal(d)).astype(np.float32)
+        norm["norm_eps"] = 1e-5
 
     stream = torch.cuda.current_stream()
+    probs = None
+    if mode == "sample":
+        # proposals of node i: softmax(z_p of its parent row + N(0,1)), its token drawn from it
+        dev0 = DeviceProblem.from_case(case, np.zeros((case.B, case.N), np.int32), row_outputs=False)
+        hp = dev0.hp.float()
+        z = (hp @ dev0.wp.float().T + dev0.bias_p).double().cpu().numpy()
+        del hp, dev0
+        parents = case.parents.reshape(-1) + np.repeat(np.arange(case.B) * case.N, case.N)
+        parent_logits = z[np.maximum(parents, 0)]
+        probs, tokens = synth.sampled_draft(case, parent_logits)
+        dev = DeviceProblem.from_case(case, tokens, draft_probs=probs, **norm)
+    else:
+        # draft tokens: half copy the target argmax of the parent row (taken from a first
+        # verification call on the GPU), half are uniform
+        dev = DeviceProblem.from_case(case, np.zeros((case.B, case.N), np.int32), **norm)
+        first = dev.run("greedy")
+        tokens = synth.greedy_tokens(case, first["row_argmax"])
+        dev.set_tokens(tokens)
+    if mode == "propose":
+        u = torch.from_numpy(case.u_res.astype(np.float32)).to(dev.device)
+        ptoks = torch.empty(case.R, dtype=torch.int32, device=dev.device)
+        pargmax = torch.empty(case.R, dtype=torch.int32, device=dev.device)
+        pprobs = torch.empty(case.R, case.V, dtype=torch.float32, device=dev.device)
+
+        def step():
+            dcd.propose(dev.problem, dev.inputs, u, ptoks, pprobs, pargmax, dev.workspace,
+                        dev.ws_bytes, stream)
+    else:
+        def step():
+            dev.launch(mode, stream)
+
     for _ in range(args.warmup):
-        dev.launch(mode, stream)
+        step()
     torch.cuda.synchronize()
 
-    # timed region: K full verification steps
+    # timed region: K full steps
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     ev0.record(stream)
     for _ in range(args.steps):
-        dev.launch(mode, stream)
+        step()
     ev1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms_step = ev0.elapsed_time(ev1) / args.steps
-    out = dev.run("greedy")
+    out = dev.run("greedy" if mode == "propose" else mode)
 
     # the dominant kernel alone (LM heads + partials), same stream, HIP events
+    lm_mode = "greedy" if mode == "greedy" else "sample"
     for _ in range(5):
-        dev.launch_lmhead(mode, stream)
+        dev.launch_lmhead(lm_mode, stream)
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record(stream)
     for _ in range(args.steps):
-        dev.launch_lmhead(mode, stream)
+        dev.launch_lmhead(lm_mode, stream)
     e1.record(stream)
     torch.cuda.synchronize()
     ms_lmhead = e0.elapsed_time(e1) / args.steps
@@ -135,7 +181,8 @@ def main():
               else "lmhead_kernel")
     ridge = MFMA_BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9)
     # the committed counters cover the default workloads of each kernel only
-    traffic, traffic_src = (counted_traffic(kernel, args.workload) if not over
+    traffic, traffic_src = (counted_traffic(kernel, args.workload)
+                            if not over and own_mode and not args.final_norm
                             else (None, "no counters for this workload"))
     if case.dtype == "bf16" and flops / kbytes > ridge:
         achieved = flops / (ms_lmhead * 1e-3) / 1e12
@@ -154,12 +201,14 @@ def main():
         roofline["frac_of_measured"] = round(roofline["achieved"] / measured[key], 4)
 
     cpu = None
-    if not args.no_cpu_baseline:
+    if mode != "greedy" or args.final_norm:
+        log("cpu baseline: only for the greedy verification of the workload's own rows")
+    elif not args.no_cpu_baseline:
         cpu = cpu_baseline(case, tokens, log)
 
     step_bytes = algorithmic_bytes(case)
     line = {
-        "metric": METRIC,
+        "metric": METRIC if mode != "propose" else "proposal rows/sec (recombined heads)",
         "value": round(nodes_per_s, 1),
         "unit": "nodes/s",
         "n_gpus": 1,
@@ -173,7 +222,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": args.workload, "batch": case.B, "nodes": case.N, "vocab": case.V,
                    "d_expert": case.dp, "d_amateur": case.dq, "plaus_thresh": case.theta,
-                   "cd_strength": case.s, "rows": R, "seed": args.seed},
+                   "cd_strength": case.s, "rows": R, "seed": args.seed, "mode": mode,
+                   "final_norm": bool(args.final_norm)},
         "hbm_frac_step": round(step_bytes / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
         "roofline": roofline,
         "cpu_baseline": cpu,

@@ -87,6 +87,16 @@ __device__ __forceinline__ f32x4 mma(u32x4 a, u32x4 b, f32x4 c) {
 __device__ __forceinline__ u32x4 ld16_stream(const char *p) {
     return __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(p));
 }
+// Weight loads: non-temporal when a tile has one row block (the weights are read
+// once), ordinary cached loads when several row blocks of a tile read the same
+// weights (they run back to back on one XCD and share them through its L2).
+template <bool STREAM>
+__device__ __forceinline__ u32x4 ld16_weights(const char *p) {
+    if constexpr (STREAM)
+        return ld16_stream(p);
+    else
+        return *reinterpret_cast<const u32x4 *>(p);
+}
 __device__ __forceinline__ u32x4 ld16(const char *p) { return *reinterpret_cast<const u32x4 *>(p); }
 __device__ __forceinline__ void st_lds(char *p, u32x4 v) { *reinterpret_cast<u32x4 *>(p) = v; }
 __device__ __forceinline__ u32x4 ld_lds(const char *p) { return *reinterpret_cast<const u32x4 *>(p); }
@@ -107,7 +117,7 @@ struct Batch {
 // Per-thread load addresses of one model's weight and hidden-state streams.
 // RAGGED: the tile reaches past the vocabulary; weight rows are clamped to the
 // last row (their results are discarded).
-template <bool RAGGED>
+template <bool RAGGED, bool STREAM>
 struct Stream {
     const char *wbase, *hbase;
     uint32_t rowbytes, wlane;
@@ -152,9 +162,9 @@ struct Stream {
 #pragma unroll
         for (int q = 0; q < WLOADS; ++q) {
             if constexpr (RAGGED)
-                b.w[q] = ld16_stream(wbase + (woff[q] + wcol));
+                b.w[q] = ld16_weights<STREAM>(wbase + (woff[q] + wcol));
             else
-                b.w[q] = ld16_stream(wbase + (size_t)q * RPI * rowbytes + (wlane + wcol));
+                b.w[q] = ld16_weights<STREAM>(wbase + (size_t)q * RPI * rowbytes + (wlane + wcol));
         }
         const uint32_t hcol = (uint32_t)c * CB + hc * 16;
         b.hok = hcol < rowbytes;
@@ -222,8 +232,8 @@ __device__ __forceinline__ void compute(const char *hb, const char *wbuf, const 
 // starts before this pass's epilogue.  The scheduling barriers pin each prefetch
 // ahead of the compute (left free, the scheduler may sink the loads, and the
 // next stage would then wait for them too).
-template <int DT, bool RAGGED>
-__device__ __forceinline__ void run_pass(const Stream<RAGGED> &st, const Stream<RAGGED> *next,
+template <int DT, bool RAGGED, bool STREAM>
+__device__ __forceinline__ void run_pass(const Stream<RAGGED, STREAM> &st, const Stream<RAGGED, STREAM> *next,
                                          Batch &b, char *hbuf, char *wbuf, const LdsAddr &a,
                                          f32x4 (&acc)[VB][RB]) {
 #pragma unroll
@@ -339,7 +349,7 @@ constexpr int kStash = RB;
 constexpr size_t kLdsBytes = kHTiles * HTILE + NW * WTILE + 2 * TS * sizeof(float) +
                              NW * kStash * kWaveSize * sizeof(float);
 
-template <int DT, bool RAGGED, bool FULL>
+template <int DT, bool RAGGED, bool FULL, bool STREAM>
 __device__ __forceinline__ void tile_body(const Plan &P, const Inputs &in, int tile, int row0,
                                           char *lds) {
     constexpr int ESZ = DT == kBF16 ? 2 : 4;
@@ -367,7 +377,7 @@ __device__ __forceinline__ void tile_body(const Plan &P, const Inputs &in, int t
         bias_q[tid] = (t < P.V && in.bq) ? in.bq[t] * P.inv_T : 0.f;
     }
 
-    Stream<RAGGED> sp, sq;
+    Stream<RAGGED, STREAM> sp, sq;
     sp.init(in.hp, in.wp, P.dp, ESZ, P.R, P.V, row0, tok0);
     sq.init(in.hq, in.wq, P.dq, ESZ, P.R, P.V, row0, tok0);
     LdsAddr a;
@@ -381,7 +391,7 @@ __device__ __forceinline__ void tile_body(const Plan &P, const Inputs &in, int t
 
     // ---- expert head (the amateur stream starts before its epilogue)
     sp.issue(0, b);
-    run_pass<DT, RAGGED>(sp, &sq, b, hbuf, wbuf, a, acc);
+    run_pass<DT, RAGGED, STREAM>(sp, &sq, b, hbuf, wbuf, a, acc);
     tile_softmax<RAGGED>(acc, bias_p, P.V, tok0, wtok0, P.inv_T, pairs, z, pmax, psum);
     if constexpr (FULL) {
         // untruncated target: the expert logits go to the dense array for the
@@ -442,7 +452,7 @@ __device__ __forceinline__ void tile_body(const Plan &P, const Inputs &in, int t
     }
 
     // ---- amateur head
-    run_pass<DT, RAGGED>(sq, nullptr, b, hbuf, wbuf, a, acc);
+    run_pass<DT, RAGGED, STREAM>(sq, nullptr, b, hbuf, wbuf, a, acc);
     if constexpr (FULL) {
         tile_softmax<RAGGED>(acc, bias_q, P.V, tok0, wtok0, P.inv_T, pairs, z, qmax, qsum);
         // the lane's expert logits back from the dense array
@@ -596,7 +606,7 @@ __device__ __forceinline__ void tile_body(const Plan &P, const Inputs &in, int t
     }
 }
 
-template <int DT, bool FULL>
+template <int DT, bool FULL, bool STREAM>
 __global__ __launch_bounds__(NT, DCD_LMHEAD_MIN_BLOCKS) void lmhead_kernel(Plan P, Inputs in) {
     extern __shared__ __align__(16) char lds[];
     // workgroup -> (vocabulary tile, row block); the row blocks of one tile are
@@ -608,9 +618,9 @@ __global__ __launch_bounds__(NT, DCD_LMHEAD_MIN_BLOCKS) void lmhead_kernel(Plan 
     if (tile >= P.ntiles) return;
     const int row0 = rblk * ROWS;
     if ((tile + 1) * TS > P.V)  // workgroup-uniform: only the last tile is ragged
-        tile_body<DT, true, FULL>(P, in, tile, row0, lds);
+        tile_body<DT, true, FULL, STREAM>(P, in, tile, row0, lds);
     else
-        tile_body<DT, false, FULL>(P, in, tile, row0, lds);
+        tile_body<DT, false, FULL, STREAM>(P, in, tile, row0, lds);
 }
 
 // Row bounds start at -inf and the per-sequence row counters of the finishing
@@ -623,37 +633,31 @@ __global__ void init_kernel(int *bound, int R, int *seqdone, int B) {
 
 }  // namespace
 
-hipError_t launch_lmhead(const Plan &p, const Inputs &in, hipStream_t st) {
+template <int DT, bool FULL, bool STREAM>
+hipError_t launch_variant(const Plan &p, const Inputs &in, hipStream_t st) {
     // the tile may need more than 64 KB of LDS (gfx950 has 160 KB per CU)
-    static const hipError_t attr = [] {
-        const void *k[4] = {(const void *)lmhead_kernel<kBF16, false>, (const void *)lmhead_kernel<kBF16, true>,
-                            (const void *)lmhead_kernel<kF32, false>, (const void *)lmhead_kernel<kF32, true>};
-        for (const void *f : k) {
-            const hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsBytes);
-            if (e != hipSuccess) return e;
-        }
-        return hipSuccess;
-    }();
+    static const hipError_t attr = hipFuncSetAttribute((const void *)lmhead_kernel<DT, FULL, STREAM>,
+                                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsBytes);
     if (attr != hipSuccess) return attr;
     const int groups = ((p.ntiles + 7) / 8) * 8 * p.nrb;
+    hipLaunchKernelGGL((lmhead_kernel<DT, FULL, STREAM>), dim3(groups), dim3(NT), kLdsBytes, st, p, in);
+    return hipGetLastError();
+}
+
+template <int DT, bool FULL>
+hipError_t launch_dt_full(const Plan &p, const Inputs &in, hipStream_t st) {
+    return p.nrb == 1 ? launch_variant<DT, FULL, true>(p, in, st) : launch_variant<DT, FULL, false>(p, in, st);
+}
+
+hipError_t launch_lmhead(const Plan &p, const Inputs &in, hipStream_t st) {
     const int ninit = p.R > p.B ? p.R : p.B;
     hipLaunchKernelGGL(init_kernel, dim3((ninit + 255) / 256), dim3(256), 0, st, p.bound, p.R, p.seqdone,
                        p.B);
     if (use_wide_lmhead(p)) return launch_lmhead_wide(p, in, st);
     // the untruncated target (plaus_thresh = 0) has its own kernels: dense logits, no candidates
-    const dim3 grid(groups), block(NT);
-    if (p.dtype == kBF16) {
-        if (p.full)
-            hipLaunchKernelGGL((lmhead_kernel<kBF16, true>), grid, block, kLdsBytes, st, p, in);
-        else
-            hipLaunchKernelGGL((lmhead_kernel<kBF16, false>), grid, block, kLdsBytes, st, p, in);
-    } else {
-        if (p.full)
-            hipLaunchKernelGGL((lmhead_kernel<kF32, true>), grid, block, kLdsBytes, st, p, in);
-        else
-            hipLaunchKernelGGL((lmhead_kernel<kF32, false>), grid, block, kLdsBytes, st, p, in);
-    }
-    return hipGetLastError();
+    if (p.dtype == kBF16)
+        return p.full ? launch_dt_full<kBF16, true>(p, in, st) : launch_dt_full<kBF16, false>(p, in, st);
+    return p.full ? launch_dt_full<kF32, true>(p, in, st) : launch_dt_full<kF32, false>(p, in, st);
 }
 
 }  // namespace dcd

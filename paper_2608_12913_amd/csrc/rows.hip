@@ -201,7 +201,7 @@ struct Smem {
     int wave_tot[NT / kWaveSize];
     int flag[4];
     int ints[4];
-    double dbl;
+    double dbl, dbl2;
 };
 
 // Writes a row's results: rowinfo (for the sequence phase) and the optional outputs.
@@ -668,58 +668,165 @@ __device__ int masked_scan(const Plan &P, size_t jrow, const Residual &res, bool
 }
 
 // Untruncated target: the same over the whole vocabulary of row jrow, from the
-// dense logits.  Each thread sums a contiguous token range; thread 0 scans the
-// partial sums in order; the thread whose range holds the target walks it.
+// dense logits.  The vocabulary is cut into at most kList blocks of bt consecutive
+// tokens (lane l holding the k = bt/64 tokens l*k .. l*k+k-1 of a block, k a
+// multiple of 4 so that every load is 16 bytes); wave w takes blocks w, w+4, ...,
+// kUnroll at a time, so that a lane has several blocks' loads in flight.  Block
+// sums (a fixed shuffle tree) go to LDS; thread 0 adds them in token order; for a
+// draw it finds the block holding u times the total, and wave 0 scans that
+// block's lanes in order to find the token.  With `reuse` the block sums and the
+// total of the previous call (the same row and weights) are still in LDS and only
+// the draw is done.
 __device__ int full_scan(const Plan &P, size_t jrow, const Residual &res, bool draw, float u,
-                         double *total_out, int tid, Smem &sm) {
+                         double *total_out, int tid, Smem &sm, bool reuse = false) {
+    constexpr int kUnroll = 4;
     const float *rj = P.rowinfo + jrow * kRowInfo;
     const float lse_p = rj[RI_LSEP], lse_q = rj[RI_LSEQ], logZ = rj[RI_LOGZ];
     const float *zp = P.zp_full + jrow * P.zstride, *zq = P.zq_full + jrow * P.zstride;
-    const int t0 = (int)((long long)tid * P.V / NT), t1 = (int)((long long)(tid + 1) * P.V / NT);
-    auto weight = [&](int t) -> double {
-        return res(__expf((1.f + P.s) * (zp[t] - lse_p) - P.s * (zq[t] - lse_q) - logZ), t);
-    };
-    double *local = sm.wts, *prefix = sm.wts + NT;  // [NT], [NT + 1]
-    double acc = 0.0;
-    for (int t = t0; t < t1; ++t) acc += weight(t);
-    local[tid] = acc;
-    __syncthreads();
-    if (tid == 0) {
-        double run = 0.0;
-        for (int i = 0; i < NT; ++i) {
-            prefix[i] = run;
-            run += local[i];
+    const int lane = tid % kWaveSize, wave = tid / kWaveSize;
+    constexpr int NW = NT / kWaveSize;
+    const int k = 4 * max(1, (P.V + 4 * kList * kWaveSize - 1) / (4 * kList * kWaveSize));
+    const int bt = k * kWaveSize;
+    const int nblk = (P.V + bt - 1) / bt;
+    const bool q4 = P.V % 4 == 0;  // draft_probs rows are 16-byte aligned
+    // weights of tokens t .. t+3 (zero past the vocabulary); the dense logit rows are
+    // padded to whole tiles, so their 16-byte loads stay inside the row
+    auto weight4 = [&](int t, double (&w)[4]) {
+        if (t >= P.V) {  // (t is a multiple of 4 and the rows are padded to 256 tokens)
+            w[0] = w[1] = w[2] = w[3] = 0.0;
+            return;
         }
-        prefix[NT] = run;
+        const float4 p4 = *reinterpret_cast<const float4 *>(zp + t);
+        const float4 q4v = *reinterpret_cast<const float4 *>(zq + t);
+        const float zpv[4] = {p4.x, p4.y, p4.z, p4.w}, zqv[4] = {q4v.x, q4v.y, q4v.z, q4v.w};
+        float qn[4] = {0.f, 0.f, 0.f, 0.f};
+        if (res.qnext) {
+            if (q4 && t + 3 < P.V) {
+                const float4 v = *reinterpret_cast<const float4 *>(res.qnext + t);
+                qn[0] = v.x; qn[1] = v.y; qn[2] = v.z; qn[3] = v.w;
+            } else {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) qn[i] = t + i < P.V ? res.qnext[t + i] : 0.f;
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            if (t + i >= P.V) {
+                w[i] = 0.0;
+                continue;
+            }
+            double v = (double)__expf((1.f + P.s) * (zpv[i] - lse_p) - P.s * (zqv[i] - lse_q) - logZ);
+            for (int m = 0; m < res.nrej; ++m)
+                if (res.invz[m] > 0.0)
+                    v = fmax(0.0, v - (double)res.dprobs[(size_t)res.rej[m] * P.V + t + i]) * res.invz[m];
+            if (res.qnext) v = fmax(0.0, v - (double)qn[i]);
+            w[i] = v;
+        }
+    };
+    auto lane_sum = [&](int b) {  // this lane's tokens of block b, in order
+        const int t0 = b * bt + lane * k;
+        double s = 0.0;
+        for (int j = 0; j < k; j += 4) {
+            double w[4];
+            weight4(t0 + j, w);
+            s += w[0];
+            s += w[1];
+            s += w[2];
+            s += w[3];
+        }
+        return s;
+    };
+    auto wave_total = [&](double x) {
+#pragma unroll
+        for (int o = kWaveSize / 2; o > 0; o >>= 1) x += __shfl_xor(x, o);
+        return x;
+    };
+    if (!reuse) {
+        // pass 1: block sums
+        for (int b0 = wave; b0 < nblk; b0 += kUnroll * NW) {
+            double ls[kUnroll];
+#pragma unroll
+            for (int i = 0; i < kUnroll; ++i) ls[i] = b0 + i * NW < nblk ? lane_sum(b0 + i * NW) : 0.0;
+#pragma unroll
+            for (int i = 0; i < kUnroll; ++i) {
+                const double bs = wave_total(ls[i]);
+                if (lane == 0 && b0 + i * NW < nblk) sm.wts[b0 + i * NW] = bs;
+            }
+        }
+        __syncthreads();
+        if (tid == 0) {
+            double run = 0.0;
+            for (int b = 0; b < nblk; ++b) run += sm.wts[b];
+            sm.dbl = run;
+        }
+        __syncthreads();
     }
-    __syncthreads();
-    *total_out = prefix[NT];
+    const double total = sm.dbl;
+    *total_out = total;
     if (!draw) {
         __syncthreads();
         return -1;
     }
-    const double target = (double)u * prefix[NT];
-    if (tid == 0) sm.ints[1] = -1;
-    __syncthreads();
-    const double mine = local[tid], start = prefix[tid];
-    if (mine > 0.0 && start <= target && target < start + mine) {
-        double run = 0.0;
-        int found = -1, last = -1;
-        for (int t = t0; t < t1; ++t) {
-            const double wt = weight(t);
-            run += wt;
-            if (wt > 0.0) {
-                last = t;
-                if (start + run > target) {
-                    found = t;
+    if (tid == 0) {  // the block holding u * total (the last block of positive weight if rounding leaves none)
+        const double target = (double)u * total;
+        double before = 0.0, last_before = 0.0;
+        int hit = -1, last = -1;
+        for (int b = 0; b < nblk; ++b) {
+            const double w = sm.wts[b];
+            if (w > 0.0) {
+                last = b;
+                last_before = before;
+                if (before + w > target) {
+                    hit = b;
                     break;
                 }
             }
+            before += w;
         }
-        sm.ints[1] = found >= 0 ? found : last;
+        sm.ints[1] = hit >= 0 ? hit : last;
+        sm.dbl2 = hit >= 0 ? before : last_before;  // running sum before that block
     }
     __syncthreads();
-    const int got = sm.ints[1];
+    const int blk = sm.ints[1];
+    const double before_blk = sm.dbl2;
+    __syncthreads();
+    if (blk < 0) return -1;  // empty support
+    if (wave == 0) {
+        const double target = (double)u * total;
+        const double ls = lane_sum(blk);
+        double incl = ls;
+#pragma unroll
+        for (int o = 1; o < kWaveSize; o <<= 1) {
+            const double v = __shfl_up(incl, o);
+            if (lane >= o) incl += v;
+        }
+        const double start = before_blk + incl - ls;  // running sum before this lane's tokens
+        const unsigned long long cross = __ballot(ls > 0.0 && start + ls > target);
+        const unsigned long long pos = __ballot(ls > 0.0);
+        // the first lane whose tokens cross the target, else the last lane of positive weight
+        const int pick = cross ? __builtin_ctzll(cross) : (pos ? 63 - __builtin_clzll(pos) : -1);
+        if (lane == pick) {
+            double run = start;
+            int found = -1, lastpos = -1;
+            const int t0 = blk * bt + lane * k;
+            for (int j = 0; j < k && found < 0; j += 4) {
+                double w[4];
+                weight4(t0 + j, w);
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    run += w[i];
+                    if (w[i] > 0.0 && found < 0) {
+                        lastpos = t0 + j + i;
+                        if (run > target) found = t0 + j + i;
+                    }
+                }
+            }
+            sm.ints[2] = found >= 0 ? found : lastpos;
+        }
+        if (pick < 0 && lane == 0) sm.ints[2] = -1;
+    }
+    __syncthreads();
+    const int got = sm.ints[2];
     __syncthreads();
     return got;
 }
@@ -861,8 +968,19 @@ __device__ void verify_sequence(const Plan &P, const Inputs &in, const Outputs &
         ++res.nrej;
     }
     const float u = smp.u_res[r0 + cur];
-    const int next = P.full ? full_scan(P, r0 + cur, res, true, u, &total, tid, sm)
-                            : masked_scan(P, r0 + cur, res, true, u, &total, tid, sm);
+    int next;
+    if (P.full && res.nrej > 0 && s_invz[res.nrej - 1] > 0.0) {
+        // the residual left by the last rejection is proportional to the weights of
+        // its normaliser pass, whose block sums are still in LDS: draw from those
+        // (a rejection whose residual summed to zero left nothing to reuse)
+        Residual last = res;
+        --last.nrej;
+        last.qnext = smp.draft_probs + (r0 + s_rej[last.nrej]) * V;
+        next = full_scan(P, r0 + cur, last, true, u, &total, tid, sm, true);
+    } else {
+        next = P.full ? full_scan(P, r0 + cur, res, true, u, &total, tid, sm)
+                      : masked_scan(P, r0 + cur, res, true, u, &total, tid, sm);
+    }
     for (int i = len + 1 + tid; i < N; i += NT) out.accept_path[r0 + i] = -1;
     if (tid == 0) {
         out.accept_path[r0] = 0;
