@@ -230,7 +230,7 @@ __device__ __forceinline__ void write_row(const Plan &P, int row, const float (&
 // its max) and D_KL(pi_p || pi_q) = sum_x pi_p (z_p - z_q) - lse_p + lse_q, whose sum
 // is merged like the expert's sum of exp (per tile: sum exp(z_p - tile max)(z_p - z_q));
 // D_KL(pi_p || pi_CD) = log Z - s D_KL(pi_p || pi_q) by the KL-decomposition lemma.
-__device__ void row_stats_full(const Plan &P, int row, int lane, const Outputs &out) {
+__device__ __forceinline__ void row_stats_full(const Plan &P, int row, int lane, const Outputs &out) {
     const float4 *pr = P.partials + (size_t)row * P.ntiles;
     const float4 *yp = P.ypart + (size_t)row * P.ntiles * 2;
     LseW lp{-INFINITY, 0.f, 0.f};
@@ -289,7 +289,7 @@ __device__ void row_stats_full(const Plan &P, int row, int lane, const Outputs &
 // ---------------------------------------------------------------------------
 // Row phase.  wave 0: the row's statistics; wave 1: the row as a draft node.
 template <int DT>
-__device__ void combine_row(const Plan &P, const Inputs &in, const Outputs &out, int row, int lane,
+__device__ __forceinline__ void combine_row(const Plan &P, const Inputs &in, const Outputs &out, int row, int lane,
                             int wave, int *list) {
     const bool want_node_logits = out.node_stats != nullptr;
     if (wave == 1) {
@@ -566,7 +566,7 @@ struct Residual {
 // that sum (the smallest token whose cumulative weight exceeds it; the last token
 // of positive weight if rounding leaves none).  Called by the whole group; returns
 // the drawn token (-1 without `draw` or with an empty support), *total the sum.
-__device__ int masked_scan(const Plan &P, size_t jrow, const Residual &res, bool draw, float u,
+__device__ __forceinline__ int masked_scan(const Plan &P, size_t jrow, const Residual &res, bool draw, float u,
                            double *total_out, int tid, Smem &sm) {
     const float *rj = P.rowinfo + jrow * kRowInfo;
     const float thr = rj[RI_THRESH], lse_p = rj[RI_LSEP], lse_q = rj[RI_LSEQ], logZ = rj[RI_LOGZ];
@@ -677,7 +677,7 @@ __device__ int masked_scan(const Plan &P, size_t jrow, const Residual &res, bool
 // block's lanes in order to find the token.  With `reuse` the block sums and the
 // total of the previous call (the same row and weights) are still in LDS and only
 // the draw is done.
-__device__ int full_scan(const Plan &P, size_t jrow, const Residual &res, bool draw, float u,
+__device__ __forceinline__ int full_scan(const Plan &P, size_t jrow, const Residual &res, bool draw, float u,
                          double *total_out, int tid, Smem &sm, bool reuse = false) {
     constexpr int kUnroll = 4;
     const float *rj = P.rowinfo + jrow * kRowInfo;
@@ -754,39 +754,59 @@ __device__ int full_scan(const Plan &P, size_t jrow, const Residual &res, bool d
             }
         }
         __syncthreads();
-        if (tid == 0) {
-            double run = 0.0;
-            for (int b = 0; b < nblk; ++b) run += sm.wts[b];
-            sm.dbl = run;
-        }
-        __syncthreads();
     }
+    // wave 0 takes the block sums in token order: lane l adds its cb consecutive
+    // blocks, an inclusive scan over the lanes gives the running sums; the total is
+    // the last lane's (the same order every time, so the draw that reuses a pass
+    // sees the same total)
+    const int cb = (nblk + kWaveSize - 1) / kWaveSize;
+    if (wave == 0) {
+        const int b0 = lane * cb;
+        double part = 0.0;
+        for (int b = b0; b < min(b0 + cb, nblk); ++b) part += sm.wts[b];
+        double incl = part;
+#pragma unroll
+        for (int o = 1; o < kWaveSize; o <<= 1) {
+            const double v = __shfl_up(incl, o);
+            if (lane >= o) incl += v;
+        }
+        const double tot = __shfl(incl, kWaveSize - 1);
+        if (lane == 0) sm.dbl = tot;
+        if (draw) {
+            // the block holding u * total: the first lane whose blocks cross it walks
+            // them (the last block of positive weight if rounding leaves none)
+            const double target = (double)u * tot, start = incl - part;
+            const unsigned long long cross = __ballot(part > 0.0 && start + part > target);
+            const unsigned long long pos = __ballot(part > 0.0);
+            const int pick = cross ? __builtin_ctzll(cross) : (pos ? 63 - __builtin_clzll(pos) : -1);
+            if (lane == pick) {
+                double before = start, last_before = start;
+                int hit = -1, last = -1;
+                for (int b = b0; b < min(b0 + cb, nblk); ++b) {
+                    const double w = sm.wts[b];
+                    if (w > 0.0) {
+                        last = b;
+                        last_before = before;
+                        if (before + w > target) {
+                            hit = b;
+                            break;
+                        }
+                    }
+                    before += w;
+                }
+                sm.ints[1] = hit >= 0 ? hit : last;
+                sm.dbl2 = hit >= 0 ? before : last_before;  // running sum before that block
+            }
+            if (pick < 0 && lane == 0) sm.ints[1] = -1;
+        }
+    }
+    __syncthreads();
     const double total = sm.dbl;
     *total_out = total;
     if (!draw) {
         __syncthreads();
         return -1;
     }
-    if (tid == 0) {  // the block holding u * total (the last block of positive weight if rounding leaves none)
-        const double target = (double)u * total;
-        double before = 0.0, last_before = 0.0;
-        int hit = -1, last = -1;
-        for (int b = 0; b < nblk; ++b) {
-            const double w = sm.wts[b];
-            if (w > 0.0) {
-                last = b;
-                last_before = before;
-                if (before + w > target) {
-                    hit = b;
-                    break;
-                }
-            }
-            before += w;
-        }
-        sm.ints[1] = hit >= 0 ? hit : last;
-        sm.dbl2 = hit >= 0 ? before : last_before;  // running sum before that block
-    }
-    __syncthreads();
     const int blk = sm.ints[1];
     const double before_blk = sm.dbl2;
     __syncthreads();
@@ -832,7 +852,7 @@ __device__ int full_scan(const Plan &P, size_t jrow, const Residual &res, bool d
 }
 
 template <int DT, bool SAMPLE>
-__device__ void verify_sequence(const Plan &P, const Inputs &in, const Outputs &out,
+__device__ __forceinline__ void verify_sequence(const Plan &P, const Inputs &in, const Outputs &out,
                                 const SampleInputs &smp, int b, int tid, Smem &sm, int *dyn) {
     const int N = P.N, V = P.V;
     const size_t r0 = (size_t)b * N;
