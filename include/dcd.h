@@ -167,7 +167,8 @@ typedef struct {                 /* device pointers, written by the call        
  * elements).
  * The workspace holds per-tile softmax partials, the candidate logits that may
  * fall inside the plausibility mask (theta > 0) or both models' dense logits
- * (theta = 0, where every token is in the support), and per-row results; it is
+ * (theta = 0, where every token is in the support, plus two rows of V doubles per
+ * sequence for the residuals of sampled verification), and per-row results; it is
  * O(B*N*V) bytes (about 8.1 bytes per row and vocabulary entry).  The size depends
  * on the problem, so a workspace sized for one problem may be too small for
  * another.

@@ -186,6 +186,7 @@ size_t workspace_layout(Plan &p, char *base) {
         p.zp_full = (float *)take(R * (size_t)p.zstride * sizeof(float));
         p.zq_full = (float *)take(R * (size_t)p.zstride * sizeof(float));
         p.ypart = (float4 *)take(R * p.ntiles * 2 * sizeof(float4));
+        p.resbuf = (double *)take((size_t)p.B * 2 * p.zstride * sizeof(double));
     } else {  // candidates of the mask
         p.cand = (float2 *)take(R * (size_t)p.V * sizeof(float2));
         p.bits = (uint32_t *)take(R * (size_t)p.wstride * sizeof(uint32_t));

@@ -57,6 +57,8 @@ struct Plan {
     // untruncated target (full = 1)
     float *zp_full;    // [R][zstride]  expert logits (divided by T)
     float *zq_full;    // [R][zstride]  amateur logits (divided by T)
+    double *resbuf;    // [B][2][zstride] sampled verification: the residual after the
+                       //   last applied rejection of the walk's current node (two rows)
     float4 *ypart;     // [R][ntiles][2] per tile, over y = (1+s) z_p - s z_q:
                        //   (max y, sum exp(y - max y), second-best y, sum exp(z_p - max_p)(z_p - z_q))
                        //   (argmax bits, z_p and z_q at the argmax, bits of the lowest

@@ -545,6 +545,13 @@ __device__ int group_exclusive_scan(int x, int tid, int *total, Smem &sm) {
 // (proposal q_j, normaliser 1/Z_j; 0 when that residual summed to zero and was not
 // applied) maps w -> max(0, w - q_j(t)) / Z_j.  With `qnext`, the unnormalised
 // residual of one more rejection, max(0, w - qnext(t)), whose sum is the next Z.
+//
+// The untruncated target's scans (full_scan) take the chain from a stored row
+// instead: `x` holds max(0, w - q_j(t)) of the last applied rejection, so that
+// w = x[t] * xs with xs its 1/Z (x = null: w = p0), and with `xout` a rejection
+// pass stores its own max(0, w - qnext(t)) there.  Both give the same doubles as
+// the chain; the stored row makes a pass read two rows instead of one per
+// rejection.
 struct Residual {
     const float *dprobs;  // draft_probs rows of the sequence (row i = pi_e^(i))
     const int *rej;       // rejected siblings in order (LDS)
@@ -552,6 +559,9 @@ struct Residual {
     int nrej;
     const float *qnext;
     int V;
+    const double *x = nullptr;  // full_scan: the stored residual row, or null
+    double xs = 0.0;
+    double *xout = nullptr;     // full_scan with qnext: where the new residual goes
     __device__ double operator()(float p0, int t) const {
         double w = (double)p0;
         for (int m = 0; m < nrej; ++m)
@@ -668,18 +678,20 @@ __device__ __forceinline__ int masked_scan(const Plan &P, size_t jrow, const Res
 }
 
 // Untruncated target: the same over the whole vocabulary of row jrow, from the
-// dense logits.  The vocabulary is cut into at most kList blocks of bt consecutive
-// tokens (lane l holding the k = bt/64 tokens l*k .. l*k+k-1 of a block, k a
-// multiple of 4 so that every load is 16 bytes); wave w takes blocks w, w+4, ...,
-// kUnroll at a time, so that a lane has several blocks' loads in flight.  Block
-// sums (a fixed shuffle tree) go to LDS; thread 0 adds them in token order; for a
-// draw it finds the block holding u times the total, and wave 0 scans that
-// block's lanes in order to find the token.  With `reuse` the block sums and the
-// total of the previous call (the same row and weights) are still in LDS and only
-// the draw is done.
+// dense logits or the stored residual row (res.x; res.nrej must be 0).  The
+// vocabulary is cut into at most kList blocks of bt consecutive tokens (lane l
+// holding the k = bt/64 tokens l*k .. l*k+k-1 of a block, k a multiple of 4 so that
+// every load is 16 bytes); wave w takes blocks w, w+4, ..., kUnroll at a time, and
+// issues the loads of all of them before it weighs any, so that a lane has
+// several blocks' loads in flight.  Block sums (a fixed shuffle tree) go to LDS;
+// wave 0 adds them in token order; for a draw it finds the block holding u times
+// the total, and wave 0 scans that block's lanes in order to find the token.  With
+// `reuse` the block sums and the total of the previous call (the same row and
+// weights) are still in LDS and only the draw is done.  A rejection pass with
+// res.xout stores its weights there.
 __device__ __forceinline__ int full_scan(const Plan &P, size_t jrow, const Residual &res, bool draw, float u,
                          double *total_out, int tid, Smem &sm, bool reuse = false) {
-    constexpr int kUnroll = 4;
+    constexpr int kUnroll = 8;
     const float *rj = P.rowinfo + jrow * kRowInfo;
     const float lse_p = rj[RI_LSEP], lse_q = rj[RI_LSEQ], logZ = rj[RI_LOGZ];
     const float *zp = P.zp_full + jrow * P.zstride, *zq = P.zq_full + jrow * P.zstride;
@@ -689,39 +701,54 @@ __device__ __forceinline__ int full_scan(const Plan &P, size_t jrow, const Resid
     const int bt = k * kWaveSize;
     const int nblk = (P.V + bt - 1) / bt;
     const bool q4 = P.V % 4 == 0;  // draft_probs rows are 16-byte aligned
-    // weights of tokens t .. t+3 (zero past the vocabulary); the dense logit rows are
-    // padded to whole tiles, so their 16-byte loads stay inside the row
-    auto weight4 = [&](int t, double (&w)[4]) {
-        if (t >= P.V) {  // (t is a multiple of 4 and the rows are padded to 256 tokens)
-            w[0] = w[1] = w[2] = w[3] = 0.0;
-            return;
+    // the raw inputs of tokens t .. t+3: loads clamped into the rows (the dense and
+    // stored rows have zstride entries, the proposal rows V), values past the
+    // vocabulary discarded by weigh4
+    // (lo, hi: z_p and z_q of the 4 tokens, or their 4 stored doubles)
+    struct Raw4 {
+        uint4 lo, hi;
+        float4 qn;
+    };
+    auto load4 = [&](int t, Raw4 &r) {
+        const int tl = min(t, P.zstride - 4);
+        if (res.x) {
+            r.lo = *reinterpret_cast<const uint4 *>(res.x + tl);
+            r.hi = *reinterpret_cast<const uint4 *>(res.x + tl + 2);
+        } else {
+            r.lo = *reinterpret_cast<const uint4 *>(zp + tl);
+            r.hi = *reinterpret_cast<const uint4 *>(zq + tl);
         }
-        const float4 p4 = *reinterpret_cast<const float4 *>(zp + t);
-        const float4 q4v = *reinterpret_cast<const float4 *>(zq + t);
-        const float zpv[4] = {p4.x, p4.y, p4.z, p4.w}, zqv[4] = {q4v.x, q4v.y, q4v.z, q4v.w};
-        float qn[4] = {0.f, 0.f, 0.f, 0.f};
         if (res.qnext) {
-            if (q4 && t + 3 < P.V) {
-                const float4 v = *reinterpret_cast<const float4 *>(res.qnext + t);
-                qn[0] = v.x; qn[1] = v.y; qn[2] = v.z; qn[3] = v.w;
+            if (q4) {
+                r.qn = *reinterpret_cast<const float4 *>(res.qnext + min(t, P.V - 4));
             } else {
-#pragma unroll
-                for (int i = 0; i < 4; ++i) qn[i] = t + i < P.V ? res.qnext[t + i] : 0.f;
+                r.qn.x = t < P.V ? res.qnext[t] : 0.f;
+                r.qn.y = t + 1 < P.V ? res.qnext[t + 1] : 0.f;
+                r.qn.z = t + 2 < P.V ? res.qnext[t + 2] : 0.f;
+                r.qn.w = t + 3 < P.V ? res.qnext[t + 3] : 0.f;
             }
         }
+    };
+    auto weigh4 = [&](int t, const Raw4 &r, double (&w)[4]) {
+        const float zpv[4] = {__uint_as_float(r.lo.x), __uint_as_float(r.lo.y), __uint_as_float(r.lo.z),
+                              __uint_as_float(r.lo.w)};
+        const float zqv[4] = {__uint_as_float(r.hi.x), __uint_as_float(r.hi.y), __uint_as_float(r.hi.z),
+                              __uint_as_float(r.hi.w)};
+        const float qn[4] = {r.qn.x, r.qn.y, r.qn.z, r.qn.w};
+        auto dbl = [](uint32_t l, uint32_t h) { return __hiloint2double((int)h, (int)l); };
+        const double xv[4] = {dbl(r.lo.x, r.lo.y), dbl(r.lo.z, r.lo.w), dbl(r.hi.x, r.hi.y), dbl(r.hi.z, r.hi.w)};
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            if (t + i >= P.V) {
-                w[i] = 0.0;
-                continue;
-            }
-            double v = (double)__expf((1.f + P.s) * (zpv[i] - lse_p) - P.s * (zqv[i] - lse_q) - logZ);
-            for (int m = 0; m < res.nrej; ++m)
-                if (res.invz[m] > 0.0)
-                    v = fmax(0.0, v - (double)res.dprobs[(size_t)res.rej[m] * P.V + t + i]) * res.invz[m];
+            double v = res.x ? xv[i] * res.xs
+                             : (double)__expf((1.f + P.s) * (zpv[i] - lse_p) - P.s * (zqv[i] - lse_q) - logZ);
             if (res.qnext) v = fmax(0.0, v - (double)qn[i]);
-            w[i] = v;
+            w[i] = t + i < P.V ? v : 0.0;
         }
+    };
+    auto weight4 = [&](int t, double (&w)[4]) {
+        Raw4 r;
+        load4(t, r);
+        weigh4(t, r, w);
     };
     auto lane_sum = [&](int b) {  // this lane's tokens of block b, in order
         const int t0 = b * bt + lane * k;
@@ -742,11 +769,32 @@ __device__ __forceinline__ int full_scan(const Plan &P, size_t jrow, const Resid
         return x;
     };
     if (!reuse) {
-        // pass 1: block sums
+        // pass 1: block sums (and the stored residual of a rejection pass); the
+        // loads of all kUnroll blocks first (blocks past the end re-read the last)
         for (int b0 = wave; b0 < nblk; b0 += kUnroll * NW) {
             double ls[kUnroll];
 #pragma unroll
-            for (int i = 0; i < kUnroll; ++i) ls[i] = b0 + i * NW < nblk ? lane_sum(b0 + i * NW) : 0.0;
+            for (int i = 0; i < kUnroll; ++i) ls[i] = 0.0;
+            for (int j = 0; j < k; j += 4) {
+                Raw4 r[kUnroll];
+#pragma unroll
+                for (int i = 0; i < kUnroll; ++i) load4(min(b0 + i * NW, nblk - 1) * bt + lane * k + j, r[i]);
+#pragma unroll
+                for (int i = 0; i < kUnroll; ++i) {
+                    const int t = (b0 + i * NW) * bt + lane * k + j;
+                    if (b0 + i * NW >= nblk) continue;
+                    double w[4];
+                    weigh4(t, r[i], w);
+                    ls[i] += w[0];
+                    ls[i] += w[1];
+                    ls[i] += w[2];
+                    ls[i] += w[3];
+                    if (res.xout && t < P.V) {  // the stored row has zstride >= t + 4 entries
+                        *reinterpret_cast<double2 *>(res.xout + t) = double2{w[0], w[1]};
+                        *reinterpret_cast<double2 *>(res.xout + t + 2) = double2{w[2], w[3]};
+                    }
+                }
+            }
 #pragma unroll
             for (int i = 0; i < kUnroll; ++i) {
                 const double bs = wave_total(ls[i]);
@@ -954,6 +1002,13 @@ __device__ __forceinline__ void verify_sequence(const Plan &P, const Inputs &in,
     // there is none) the emitted token is drawn from what is left.  Every thread
     // follows the walk; thread 0 takes the accept decisions.
     Residual res{smp.draft_probs + r0 * V, s_rej, s_invz, 0, nullptr, V};
+    // untruncated target: the residual after the last applied rejection at the
+    // current node is kept as a stored row (null: none yet) and its 1/Z; the next
+    // rejection pass writes the other of the sequence's two rows
+    double *const xrow0 = P.full ? P.resbuf + (size_t)b * 2 * P.zstride : nullptr;
+    double *const xrow1 = P.full ? xrow0 + P.zstride : nullptr;
+    const double *xcur = nullptr;
+    double xs = 0.0;
     double total;
     int cur = 0, len = 0;
     for (int c = 1; c < N; ++c) {
@@ -971,14 +1026,21 @@ __device__ __forceinline__ void verify_sequence(const Plan &P, const Inputs &in,
             if (tid == 0) out.accept_path[r0 + len] = c;
             cur = c;  // its children have larger indices
             res.nrej = 0;
+            xcur = nullptr;
             continue;
         }
         // rejected: the normaliser of the residual it leaves
         res.qnext = smp.draft_probs + (r0 + c) * V;
-        if (P.full)
-            full_scan(P, r0 + cur, res, false, 0.f, &total, tid, sm);
-        else
+        if (P.full) {
+            Residual fr{res.dprobs, s_rej, s_invz, 0, res.qnext, V, xcur, xs, xcur == xrow0 ? xrow1 : xrow0};
+            full_scan(P, r0 + cur, fr, false, 0.f, &total, tid, sm);
+            if (total > 0.0) {  // applied: the stored row becomes the current residual
+                xcur = fr.xout;
+                xs = 1.0 / total;
+            }
+        } else {
             masked_scan(P, r0 + cur, res, false, 0.f, &total, tid, sm);
+        }
         res.qnext = nullptr;
         if (tid == 0) {
             s_rej[res.nrej] = c;
@@ -991,15 +1053,16 @@ __device__ __forceinline__ void verify_sequence(const Plan &P, const Inputs &in,
     int next;
     if (P.full && res.nrej > 0 && s_invz[res.nrej - 1] > 0.0) {
         // the residual left by the last rejection is proportional to the weights of
-        // its normaliser pass, whose block sums are still in LDS: draw from those
-        // (a rejection whose residual summed to zero left nothing to reuse)
-        Residual last = res;
-        --last.nrej;
-        last.qnext = smp.draft_probs + (r0 + s_rej[last.nrej]) * V;
+        // its normaliser pass, stored in xcur, whose block sums are still in LDS:
+        // draw from those (a rejection whose residual summed to zero left nothing
+        // to reuse)
+        const Residual last{res.dprobs, s_rej, s_invz, 0, nullptr, V, xcur, 1.0};
         next = full_scan(P, r0 + cur, last, true, u, &total, tid, sm, true);
+    } else if (P.full) {
+        const Residual fin{res.dprobs, s_rej, s_invz, 0, nullptr, V, xcur, xs};
+        next = full_scan(P, r0 + cur, fin, true, u, &total, tid, sm);
     } else {
-        next = P.full ? full_scan(P, r0 + cur, res, true, u, &total, tid, sm)
-                      : masked_scan(P, r0 + cur, res, true, u, &total, tid, sm);
+        next = masked_scan(P, r0 + cur, res, true, u, &total, tid, sm);
     }
     for (int i = len + 1 + tid; i < N; i += NT) out.accept_path[r0 + i] = -1;
     if (tid == 0) {
@@ -1036,7 +1099,8 @@ __global__ __launch_bounds__(NT) void finish_kernel(Plan P, Inputs in, Outputs o
 
 // Proposals from the recombined heads: one workgroup per row.  The row phase
 // (wave 0) gives the row's normalisers and argmax; then the whole group draws a
-// token from the row's target and/or writes the target densely (0 off the mask).
+// token from the row's target.  The dense target rows are written afterwards by
+// propose_probs_kernel, which spreads them over many workgroups.
 template <int DT>
 __global__ __launch_bounds__(NT) void propose_kernel(Plan P, Inputs in, ProposeOutputs po) {
     __shared__ Smem sm;
@@ -1052,28 +1116,51 @@ __global__ __launch_bounds__(NT) void propose_kernel(Plan P, Inputs in, ProposeO
                              : masked_scan(P, row, target, true, po.u[row], &total, tid, sm);
         if (tid == 0) po.tokens[row] = t;
     }
-    if (po.probs) {
-        const float *rj = P.rowinfo + (size_t)row * kRowInfo;
-        const float thr = rj[RI_THRESH], lse_p = rj[RI_LSEP], lse_q = rj[RI_LSEQ], logZ = rj[RI_LOGZ];
-        float *dst = po.probs + (size_t)row * P.V;
-        if (P.full) {
-            const float *zp = P.zp_full + (size_t)row * P.zstride, *zq = P.zq_full + (size_t)row * P.zstride;
-            for (int t = tid; t < P.V; t += NT)
-                dst[t] = __expf((1.f + P.s) * (zp[t] - lse_p) - P.s * (zq[t] - lse_q) - logZ);
-        } else {
-            const int *tc = P.tcount + (size_t)row * P.ntiles;
-            const uint32_t *bits = P.bits + (size_t)row * P.wstride;
-            const float2 *cz = P.cand + (size_t)row * P.V;
-            for (int t = tid; t < P.V; t += NT) {
-                float v = 0.f;
-                // bitmap words are valid only in tiles that kept candidates
-                if (tc[t / kTileTokens] > 0 && (bits[t >> 5] >> (t & 31) & 1u)) {
-                    const float2 c = cz[t];
-                    if (c.x >= thr) v = __expf((1.f + P.s) * (c.x - lse_p) - P.s * (c.y - lse_q) - logZ);
-                }
-                dst[t] = v;
+}
+
+constexpr int kProbTokens = NT * 4;  // tokens of a row per workgroup of propose_probs_kernel
+
+// The proposal rows written densely: pi_hat(t) of row blockIdx.x for the
+// kProbTokens tokens of slice blockIdx.y, 0 off the mask.  A thread takes 4
+// consecutive tokens (one 16-byte store when the rows are 16-byte aligned); the
+// values are computed exactly as in the row phase's target.
+template <bool FULL>
+__global__ __launch_bounds__(NT) void propose_probs_kernel(Plan P, float *probs, bool aligned) {
+    const int row = blockIdx.x;
+    const int t0 = blockIdx.y * kProbTokens + threadIdx.x * 4;
+    if (t0 >= P.V) return;
+    const float *rj = P.rowinfo + (size_t)row * kRowInfo;
+    const float thr = rj[RI_THRESH], lse_p = rj[RI_LSEP], lse_q = rj[RI_LSEQ], logZ = rj[RI_LOGZ];
+    float v[4] = {0.f, 0.f, 0.f, 0.f};
+    if constexpr (FULL) {
+        // the dense logit rows are padded to whole tiles, so the loads stay inside the row
+        const float4 p = *reinterpret_cast<const float4 *>(P.zp_full + (size_t)row * P.zstride + t0);
+        const float4 q = *reinterpret_cast<const float4 *>(P.zq_full + (size_t)row * P.zstride + t0);
+        const float zp[4] = {p.x, p.y, p.z, p.w}, zq[4] = {q.x, q.y, q.z, q.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) v[i] = __expf((1.f + P.s) * (zp[i] - lse_p) - P.s * (zq[i] - lse_q) - logZ);
+    } else {
+        // bitmap words are valid only in tiles that kept candidates; the 4 tokens
+        // share a tile and a word (t0 is a multiple of 4)
+        const uint32_t word = P.tcount[(size_t)row * P.ntiles + t0 / kTileTokens] > 0
+                                  ? P.bits[(size_t)row * P.wstride + (t0 >> 5)] >> (t0 & 31)
+                                  : 0u;
+        const float2 *cz = P.cand + (size_t)row * P.V;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            if ((word >> i & 1u) && t0 + i < P.V) {
+                const float2 c = cz[t0 + i];
+                if (c.x >= thr) v[i] = __expf((1.f + P.s) * (c.x - lse_p) - P.s * (c.y - lse_q) - logZ);
             }
         }
+    }
+    float *dst = probs + (size_t)row * P.V + t0;
+    if (aligned && t0 + 3 < P.V) {
+        *reinterpret_cast<float4 *>(dst) = float4{v[0], v[1], v[2], v[3]};
+    } else {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            if (t0 + i < P.V) dst[i] = v[i];
     }
 }
 
@@ -1084,6 +1171,14 @@ hipError_t launch_propose(const Plan &p, const Inputs &in, const ProposeOutputs 
         hipLaunchKernelGGL((propose_kernel<kBF16>), dim3(p.R), dim3(NT), 0, st, p, in, out);
     else
         hipLaunchKernelGGL((propose_kernel<kF32>), dim3(p.R), dim3(NT), 0, st, p, in, out);
+    if (out.probs) {
+        const dim3 grid(p.R, (p.V + kProbTokens - 1) / kProbTokens);
+        const bool aligned = p.V % 4 == 0 && reinterpret_cast<uintptr_t>(out.probs) % 16 == 0;
+        if (p.full)
+            hipLaunchKernelGGL(propose_probs_kernel<true>, grid, dim3(NT), 0, st, p, out.probs, aligned);
+        else
+            hipLaunchKernelGGL(propose_probs_kernel<false>, grid, dim3(NT), 0, st, p, out.probs, aligned);
+    }
     return hipGetLastError();
 }
 
