@@ -7,19 +7,13 @@
 
 namespace dcd {
 
-// LM-head tile geometry (gfx950: 64-lane waves, 16x16 MFMA blocks).
+// LM-head tile geometry (gfx950: 64-lane waves, 16x16 MFMA blocks).  Every LM-head
+// kernel reduces its logits per vocabulary tile of kTileTokens tokens; the
+// streaming kernel has two row shapes, 64 and 128 rows per workgroup.
 constexpr int kWaveSize = 64;
-#ifndef DCD_TILE_WAVES
-#define DCD_TILE_WAVES 4
-#endif
-#ifndef DCD_TILE_VBLOCKS
-#define DCD_TILE_VBLOCKS 4
-#endif
-constexpr int kTileWaves = DCD_TILE_WAVES;           // waves per workgroup
-constexpr int kTileVBlocks = DCD_TILE_VBLOCKS;       // 16-token blocks per wave
-constexpr int kTileTokens = kTileWaves * kTileVBlocks * 16;   // tokens per workgroup
-constexpr int kTileRBlocks = 4;                      // 16-row blocks per workgroup
-constexpr int kTileRows = kTileRBlocks * 16;         // 64 rows per workgroup
+constexpr int kTileTokens = 256;                     // tokens per vocabulary tile
+constexpr int kSkinnyRows = 64;                      // rows per workgroup, one sequence's tree
+constexpr int kSkinnyRowsWide = 128;                 // rows per workgroup above 64 rows
 constexpr int kWordsPerTile = kTileTokens / 32;      // candidate bit words per row and tile
 constexpr int kRowInfo = 16;                         // floats of per-row results
 constexpr int kMaxNodes = 4096;                      // nodes per sequence (staged in LDS)
@@ -38,7 +32,8 @@ enum ElemType { kF32 = 0, kBF16 = 1 };
 struct Plan {
     int B, N, R, V, dp, dq, dtype;
     int ntiles;        // ceil(V / kTileTokens)
-    int nrb;           // ceil(R / kTileRows)
+    int rows_blk;      // rows per workgroup of the streaming LM-head kernel (64 or 128)
+    int nrb;           // ceil(R / rows_blk)
     int wstride;       // candidate bit words per row (ntiles * kWordsPerTile)
     float log_theta;   // ln(plaus_thresh); -inf when the mask is off
     float s;           // cd_strength
@@ -133,6 +128,9 @@ hipError_t launch_lmhead(const Plan &p, const Inputs &in, hipStream_t st);
 // the many-row variant (bf16, masked target, R >= kWideMinRows): same outputs
 bool use_wide_lmhead(const Plan &p);
 hipError_t launch_lmhead_wide(const Plan &p, const Inputs &in, hipStream_t st);
+// the streaming LM-head kernel in its two row shapes (p.rows_blk selects)
+hipError_t launch_lmhead_rows64(const Plan &p, const Inputs &in, hipStream_t st);
+hipError_t launch_lmhead_rows128(const Plan &p, const Inputs &in, hipStream_t st);
 // proposals from the recombined heads (rows only, after launch_lmhead)
 struct ProposeOutputs {
     const float *u;

@@ -2,9 +2,9 @@
 // candidate epilogue (Alg. 1 "parallel model evaluation" followed by the
 // per-tile pieces of Eq. (1) and the plausibility mask of Sec. 2.1).
 //
-// Tiling.  One workgroup = kTileWaves waves = one tile of kTileTokens vocabulary
-// tokens x 64 rows.  Each wave owns 16*kTileVBlocks consecutive tokens and
-// accumulates z^T[tokens][64 rows] = W * H^T in 16x16 MFMA blocks
+// Tiling.  One workgroup = NW waves = one tile of kTileTokens vocabulary tokens x
+// ROWS rows.  Each wave owns 16*VB consecutive tokens and accumulates
+// z^T[tokens][ROWS rows] = W * H^T in 16x16 MFMA blocks
 // (v_mfma_f32_16x16x32_bf16, or 4 x v_mfma_f32_16x16x4_f32 for fp32).  K is
 // walked in chunks of CB bytes of every row, each tile from its own starting
 // chunk (Stream::init); the expert head first, then the amateur head, through
@@ -40,21 +40,28 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
-#ifndef DCD_CHUNK_BYTES
-#define DCD_CHUNK_BYTES 128
+// Row shape of this translation unit (lmhead128.hip includes this file with 128):
+//   64 rows:  4 waves of 64 tokens x 64 rows, 128-byte chunks (32 KB of weights in
+//             flight per workgroup), two workgroups per CU;
+//   128 rows: 8 waves of 32 tokens x 128 rows (the same 64 accumulators per wave),
+//             256-byte chunks (64 KB in flight), one workgroup per CU (its LDS).
+// Either way about 64 KB of weights is in flight per CU, and each weight byte
+// serves ROWS rows.
+#ifndef DCD_SKINNY_ROWS
+#define DCD_SKINNY_ROWS 64
 #endif
-// minimum waves per SIMD: 2 keeps two 4-wave tiles resident per CU
-#ifndef DCD_LMHEAD_MIN_BLOCKS
-#define DCD_LMHEAD_MIN_BLOCKS 2
+#if DCD_SKINNY_ROWS == 64
+constexpr int NW = 4, VB = 4, CB = 128, kMinBlocks = 2;
+#elif DCD_SKINNY_ROWS == 128
+constexpr int NW = 8, VB = 2, CB = 256, kMinBlocks = 1;
+#else
+#error "DCD_SKINNY_ROWS must be 64 or 128"
 #endif
 
-constexpr int NW = kTileWaves;
-constexpr int VB = kTileVBlocks;          // 16-token blocks per wave
 constexpr int NT = NW * kWaveSize;        // threads per workgroup
 constexpr int TS = kTileTokens;           // tokens per tile
-constexpr int RB = kTileRBlocks;          // 16-row blocks
-constexpr int ROWS = kTileRows;           // 64
-constexpr int CB = DCD_CHUNK_BYTES;       // bytes of every row per K-chunk
+constexpr int ROWS = DCD_SKINNY_ROWS;     // rows per workgroup
+constexpr int RB = ROWS / 16;             // 16-row blocks
 constexpr int LPR = CB / 16;              // lanes per row in a weight load instruction
 constexpr int RPI = kWaveSize / LPR;      // rows per weight load instruction
 constexpr int WLOADS = 16 * VB / RPI;     // weight load instructions per wave and chunk
@@ -68,6 +75,7 @@ static_assert(CB % 64 == 0 && WLOADS * RPI == 16 * VB && LPR % RPI == 0 || RPI %
               "weight chunk must tile");
 static_assert(TS == 16 * VB * NW && TS % 32 == 0 && TS <= NT, "tile = 16*VB tokens per wave");
 static_assert((NT / LPR) % LPR == 0, "hidden-state rows of one thread share a swizzle");
+static_assert(4 * VB <= 32, "a lane's candidate flags of a row block fit one word");
 
 // One 16-byte A fragment x one 16-byte B fragment, accumulated into c.
 template <int DT>
@@ -619,7 +627,7 @@ __device__ __forceinline__ void tile_body(const Plan &P, const Inputs &in, int t
 }
 
 template <int DT, bool FULL, bool STREAM>
-__global__ __launch_bounds__(NT, DCD_LMHEAD_MIN_BLOCKS) void lmhead_kernel(Plan P, Inputs in) {
+__global__ __launch_bounds__(NT, kMinBlocks) void lmhead_kernel(Plan P, Inputs in) {
     extern __shared__ __align__(16) char lds[];
     // workgroup -> (vocabulary tile, row block); the row blocks of one tile are
     // dispatched back to back on the same XCD (workgroup id modulo 8) so the
@@ -635,6 +643,7 @@ __global__ __launch_bounds__(NT, DCD_LMHEAD_MIN_BLOCKS) void lmhead_kernel(Plan 
         tile_body<DT, false, FULL, STREAM>(P, in, tile, row0, lds);
 }
 
+#if DCD_SKINNY_ROWS == 64
 // Row bounds start at -inf and the per-sequence row counters of the finishing
 // step at 0, for every call.
 __global__ void init_kernel(int *bound, int R, int *seqdone, int B) {
@@ -642,8 +651,7 @@ __global__ void init_kernel(int *bound, int R, int *seqdone, int B) {
     if (r < R) bound[r] = ordered_key(-INFINITY);
     if (r < B) seqdone[r] = 0;
 }
-
-}  // namespace
+#endif
 
 template <int DT, bool FULL, bool STREAM>
 hipError_t launch_variant(const Plan &p, const Inputs &in, hipStream_t st) {
@@ -661,15 +669,28 @@ hipError_t launch_dt_full(const Plan &p, const Inputs &in, hipStream_t st) {
     return p.nrb == 1 ? launch_variant<DT, FULL, true>(p, in, st) : launch_variant<DT, FULL, false>(p, in, st);
 }
 
+// the untruncated target (plaus_thresh = 0) has its own kernels: dense logits, no candidates
+hipError_t launch_skinny(const Plan &p, const Inputs &in, hipStream_t st) {
+    if (p.rows_blk != ROWS) return hipErrorInvalidValue;
+    if (p.dtype == kBF16)
+        return p.full ? launch_dt_full<kBF16, true>(p, in, st) : launch_dt_full<kBF16, false>(p, in, st);
+    return p.full ? launch_dt_full<kF32, true>(p, in, st) : launch_dt_full<kF32, false>(p, in, st);
+}
+
+}  // namespace
+
+#if DCD_SKINNY_ROWS == 64
+hipError_t launch_lmhead_rows64(const Plan &p, const Inputs &in, hipStream_t st) { return launch_skinny(p, in, st); }
+
 hipError_t launch_lmhead(const Plan &p, const Inputs &in, hipStream_t st) {
     const int ninit = p.R > p.B ? p.R : p.B;
     hipLaunchKernelGGL(init_kernel, dim3((ninit + 255) / 256), dim3(256), 0, st, p.bound, p.R, p.seqdone,
                        p.B);
     if (use_wide_lmhead(p)) return launch_lmhead_wide(p, in, st);
-    // the untruncated target (plaus_thresh = 0) has its own kernels: dense logits, no candidates
-    if (p.dtype == kBF16)
-        return p.full ? launch_dt_full<kBF16, true>(p, in, st) : launch_dt_full<kBF16, false>(p, in, st);
-    return p.full ? launch_dt_full<kF32, true>(p, in, st) : launch_dt_full<kF32, false>(p, in, st);
+    return p.rows_blk == kSkinnyRowsWide ? launch_lmhead_rows128(p, in, st) : launch_lmhead_rows64(p, in, st);
 }
+#else
+hipError_t launch_lmhead_rows128(const Plan &p, const Inputs &in, hipStream_t st) { return launch_skinny(p, in, st); }
+#endif
 
 }  // namespace dcd
