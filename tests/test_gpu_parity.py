@@ -113,6 +113,14 @@ def test_untruncated_target_fp32_ragged_k():
     _check_greedy(case, _greedy_tokens(case), "untruncated fp32")
 
 
+@pytest.mark.parametrize("B,theta", [(4, 0.1), (8, 0.1), (4, 0.0), (8, 0.0)])
+def test_fp32_128_row_tiles(B, theta):
+    # 100 and 200 rows go to the streaming kernel's 128-row workgroups (one row
+    # block with non-temporal weight loads, two with cached ones), fp32 with K tails
+    case = synth.make_case("tiny_chain8", 24 + B, B=B, N=25, V=777, dp=100, dq=36, theta=theta)
+    _check_greedy(case, _greedy_tokens(case), f"fp32 {case.R} rows theta={theta}")
+
+
 def test_flat_logits_every_token_in_mask():
     case = synth.make_case("tiny_chain8", 12, N=8, V=1500, dp=64, dq=32)
     case.wp[:] = 0
