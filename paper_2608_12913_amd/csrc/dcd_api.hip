@@ -57,7 +57,7 @@ int make_plan(const dcd_problem *p, bool sample, Plan &P) {
     // weight byte is streamed once for each 128 rows (10% faster at 128 rows); from
     // 512 rows the many-row kernel takes a masked bf16 problem, and the others keep
     // 64-row workgroups, two per CU (7% faster than 128 rows at 2048 untruncated rows)
-    P.rows_blk = P.R > kSkinnyRows && P.R < kWideMinRows ? kSkinnyRowsWide : kSkinnyRows;
+    P.rows_blk = P.R > kStreamRowsSmall && P.R < kWideMinRows ? kStreamRowsLarge : kStreamRowsSmall;
     P.nrb = (P.R + P.rows_blk - 1) / P.rows_blk;
     const long long groups = (long long)((P.ntiles + 7) / 8) * 8 * P.nrb;
     if (groups > 0x7fffffffLL) return DCD_ERR_SHAPE;

@@ -12,8 +12,8 @@ namespace dcd {
 // streaming kernel has two row shapes, 64 and 128 rows per workgroup.
 constexpr int kWaveSize = 64;
 constexpr int kTileTokens = 256;                     // tokens per vocabulary tile
-constexpr int kSkinnyRows = 64;                      // rows per workgroup, one sequence's tree
-constexpr int kSkinnyRowsWide = 128;                 // rows per workgroup above 64 rows
+constexpr int kStreamRowsSmall = 64;                 // rows per workgroup up to 64 rows
+constexpr int kStreamRowsLarge = 128;                // rows per workgroup from 65 to 511 rows
 constexpr int kWordsPerTile = kTileTokens / 32;      // candidate bit words per row and tile
 constexpr int kRowInfo = 16;                         // floats of per-row results
 constexpr int kMaxNodes = 4096;                      // nodes per sequence (staged in LDS)

@@ -47,20 +47,20 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 //             256-byte chunks (64 KB in flight), one workgroup per CU (its LDS).
 // Either way about 64 KB of weights is in flight per CU, and each weight byte
 // serves ROWS rows.
-#ifndef DCD_SKINNY_ROWS
-#define DCD_SKINNY_ROWS 64
+#ifndef DCD_STREAM_ROWS
+#define DCD_STREAM_ROWS 64
 #endif
-#if DCD_SKINNY_ROWS == 64
+#if DCD_STREAM_ROWS == 64
 constexpr int NW = 4, VB = 4, CB = 128, kMinBlocks = 2;
-#elif DCD_SKINNY_ROWS == 128
+#elif DCD_STREAM_ROWS == 128
 constexpr int NW = 8, VB = 2, CB = 256, kMinBlocks = 1;
 #else
-#error "DCD_SKINNY_ROWS must be 64 or 128"
+#error "DCD_STREAM_ROWS must be 64 or 128"
 #endif
 
 constexpr int NT = NW * kWaveSize;        // threads per workgroup
 constexpr int TS = kTileTokens;           // tokens per tile
-constexpr int ROWS = DCD_SKINNY_ROWS;     // rows per workgroup
+constexpr int ROWS = DCD_STREAM_ROWS;     // rows per workgroup
 constexpr int RB = ROWS / 16;             // 16-row blocks
 constexpr int LPR = CB / 16;              // lanes per row in a weight load instruction
 constexpr int RPI = kWaveSize / LPR;      // rows per weight load instruction
@@ -643,7 +643,7 @@ __global__ __launch_bounds__(NT, kMinBlocks) void lmhead_kernel(Plan P, Inputs i
         tile_body<DT, false, FULL, STREAM>(P, in, tile, row0, lds);
 }
 
-#if DCD_SKINNY_ROWS == 64
+#if DCD_STREAM_ROWS == 64
 // Row bounds start at -inf and the per-sequence row counters of the finishing
 // step at 0, for every call.
 __global__ void init_kernel(int *bound, int R, int *seqdone, int B) {
@@ -679,7 +679,7 @@ hipError_t launch_skinny(const Plan &p, const Inputs &in, hipStream_t st) {
 
 }  // namespace
 
-#if DCD_SKINNY_ROWS == 64
+#if DCD_STREAM_ROWS == 64
 hipError_t launch_lmhead_rows64(const Plan &p, const Inputs &in, hipStream_t st) { return launch_skinny(p, in, st); }
 
 hipError_t launch_lmhead(const Plan &p, const Inputs &in, hipStream_t st) {
@@ -687,7 +687,7 @@ hipError_t launch_lmhead(const Plan &p, const Inputs &in, hipStream_t st) {
     hipLaunchKernelGGL(init_kernel, dim3((ninit + 255) / 256), dim3(256), 0, st, p.bound, p.R, p.seqdone,
                        p.B);
     if (use_wide_lmhead(p)) return launch_lmhead_wide(p, in, st);
-    return p.rows_blk == kSkinnyRowsWide ? launch_lmhead_rows128(p, in, st) : launch_lmhead_rows64(p, in, st);
+    return p.rows_blk == kStreamRowsLarge ? launch_lmhead_rows128(p, in, st) : launch_lmhead_rows64(p, in, st);
 }
 #else
 hipError_t launch_lmhead_rows128(const Plan &p, const Inputs &in, hipStream_t st) { return launch_skinny(p, in, st); }

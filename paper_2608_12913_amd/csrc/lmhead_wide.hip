@@ -1,5 +1,5 @@
 // LM-head projection for many rows (the compute-bound regime), with the same
-// softmax-partials and candidate epilogue as the 64-row kernel (Alg. 1 "parallel
+// softmax-partials and candidate epilogue as the streaming kernel (Alg. 1 "parallel
 // model evaluation", the per-tile pieces of Eq. (1) and the plausibility mask of
 // Sec. 2.1).
 //
@@ -14,7 +14,7 @@
 // row tiles of a vocabulary tile are dispatched together on one XCD, so its
 // weights come from HBM once and from that XCD's L2 for the others.
 //
-// Epilogue: as in the 64-row kernel -- per (row, tile) the max and sum of exp of
+// Epilogue: as in the streaming kernel -- per (row, tile) the max and sum of exp of
 // both models, tile-local candidates (z_p within ln(theta) of the tile max)
 // pruned against the running row bound.  It works one 16-row block at a time and
 // recomputes logits from the accumulators; the block's logits also go to an LDS
