@@ -763,11 +763,6 @@ __device__ __forceinline__ int full_scan(const Plan &P, size_t jrow, const Resid
         }
         return s;
     };
-    auto wave_total = [&](double x) {
-#pragma unroll
-        for (int o = kWaveSize / 2; o > 0; o >>= 1) x += __shfl_xor(x, o);
-        return x;
-    };
     if (!reuse) {
         // pass 1: block sums (and the stored residual of a rejection pass); the
         // loads of all kUnroll blocks first (blocks past the end re-read the last)
@@ -795,11 +790,16 @@ __device__ __forceinline__ int full_scan(const Plan &P, size_t jrow, const Resid
                     }
                 }
             }
+            // the blocks' sums by a shuffle tree (xor 32, 16, ..., 1), one level for
+            // all blocks at a time, so that their independent shuffles are in
+            // flight together
 #pragma unroll
-            for (int i = 0; i < kUnroll; ++i) {
-                const double bs = wave_total(ls[i]);
-                if (lane == 0 && b0 + i * NW < nblk) sm.wts[b0 + i * NW] = bs;
-            }
+            for (int o = kWaveSize / 2; o > 0; o >>= 1)
+#pragma unroll
+                for (int i = 0; i < kUnroll; ++i) ls[i] += __shfl_xor(ls[i], o);
+#pragma unroll
+            for (int i = 0; i < kUnroll; ++i)
+                if (lane == 0 && b0 + i * NW < nblk) sm.wts[b0 + i * NW] = ls[i];
         }
         __syncthreads();
     }
