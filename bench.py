@@ -263,12 +263,29 @@ def measured_ceilings(torch, stream, log):
     return out
 
 
+def code_sha256(root, rels):
+    """SHA-256 of the code of the listed sources: comments, blank lines and the
+    indentation of lines removed, so that a change to comments alone keeps committed
+    counters valid."""
+    import hashlib
+    import re
+
+    h = hashlib.sha256()
+    for rel in rels:
+        text = open(os.path.join(root, rel), encoding="utf-8").read()
+        text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", "", text)
+        for line in text.splitlines():
+            line = line.strip()
+            if line:
+                h.update(line.encode() + b"\n")
+    return h.hexdigest()
+
+
 def counted_traffic(kernel, workload):
     """HBM bytes per LM-head launch from the committed profiler counter summary of this
     kernel and workload, or None when there is none or the kernel sources have changed
     since the counters were taken."""
-    import hashlib
-
     root = os.path.dirname(os.path.abspath(__file__))
     path = os.path.join(root, "profiles", f"{kernel}_{workload}_hbm_counters.txt")
     if not os.path.exists(path):
@@ -278,10 +295,8 @@ def counted_traffic(kernel, workload):
         if ":" in line and not line.startswith(" "):
             k, v = line.split(":", 1)
             fields[k.strip()] = v.strip()
-    h = hashlib.sha256()
-    for rel in fields.get("sources", "").split():
-        h.update(open(os.path.join(root, rel), "rb").read())
-    if not fields.get("sources") or h.hexdigest() != fields.get("sources_sha256"):
+    rels = fields.get("sources", "").split()
+    if not rels or code_sha256(root, rels) != fields.get("sources_code_sha256"):
         return None, "stale counters (kernel changed since they were taken)"
     fetch = float(fields["fetch_kib_per_dispatch"]) * float(fields["fetch_scale"])
     write = float(fields["write_kib_per_dispatch"]) * float(fields["write_scale"])

@@ -10,8 +10,9 @@
 // chunk (Stream::init); the expert head first, then the amateur head, through
 // the same registers and LDS.
 //
-// Weight stream (the HBM-bound part).  A wave reads its rows with non-temporal
-// 128-bit loads, RPI rows x CB contiguous bytes per instruction.  On MI355X this
+// Weight stream (the HBM-bound part).  A wave reads its rows with 128-bit loads
+// (non-temporal when a tile has one row block, ld16_weights), RPI rows x CB
+// contiguous bytes per instruction.  On MI355X this
 // shape (long runs per row, every tile resident at once) streams HBM3E far
 // faster than the MFMA A-fragment shape (16 rows x 64 bytes per instruction), so
 // each chunk is transposed through a wave-private LDS tile into fragment order.
