@@ -908,7 +908,7 @@ __device__ __forceinline__ void verify_sequence(const Plan &P, const Inputs &in,
     // sampled: the walk's state (see seq_lds_bytes)
     float *s_p0 = reinterpret_cast<float *>(dyn + 3 * N), *s_qx = s_p0 + N;
     int *s_rej = reinterpret_cast<int *>(s_qx + N);
-    double *s_invz = reinterpret_cast<double *>(dyn + 6 * N + (N & 1));
+    double *s_invz = reinterpret_cast<double *>(dyn + 6 * N);  // 24 N bytes in: 8-byte aligned
 
     if (tid < 4) sm.flag[tid] = 0;
     __syncthreads();
@@ -1185,9 +1185,9 @@ hipError_t launch_propose(const Plan &p, const Inputs &in, const ProposeOutputs 
 // dynamic LDS of the sequence phase: parents, tokens and row argmax (12 bytes per
 // node); sampled also the walk's state: target and proposal probability of each
 // node's token, the rejected siblings and their normalisers (20 more bytes per
-// node, the doubles 8-byte aligned)
+// node; the doubles follow 6 N 4-byte slots, so they are 8-byte aligned for any N)
 size_t seq_lds_bytes(int N, bool sampled) {
-    return sampled ? (size_t)(6 * N + (N & 1)) * sizeof(int) + (size_t)N * sizeof(double)
+    return sampled ? (size_t)6 * N * sizeof(int) + (size_t)N * sizeof(double)
                    : (size_t)3 * N * sizeof(int);
 }
 

@@ -243,6 +243,29 @@ def _check_sample(case, probs, tokens, label, seqs=None):
     return g, o
 
 
+@pytest.mark.parametrize("theta", [0.1, 0.0])
+def test_root_only_sequences(theta):
+    # N = 1, nothing drafted: greedy emits the root row's argmax, sampled verification
+    # the bonus draw from pi_CD of the root row
+    case = synth.make_case("tiny_chain8", 60, B=3, N=1, V=1000, dp=64, dq=32, theta=theta)
+    g, _, _ = _check_greedy(case, _greedy_tokens(case), f"root only theta={theta}")
+    assert np.all(g["accept_len"] == 0)
+    case = synth.make_case("s8_chain16x8", 62, B=3, N=1, V=1000, dp=64, dq=32, theta=theta)
+    probs, tokens = _sampled_setup(case)
+    g, _ = _check_sample(case, probs, tokens, f"root only sampled theta={theta}")
+    assert np.all(g["accept_len"] == 0)
+
+
+@pytest.mark.parametrize("theta", [0.5, 0.0])
+def test_vocabulary_smaller_than_a_tile(theta):
+    # 5 tokens and 8-element rows: one ragged vocabulary tile and one 16-byte K chunk
+    case = synth.make_case("b8_tree64", 61, B=2, N=3, V=5, dp=8, dq=8, theta=theta)
+    _check_greedy(case, _greedy_tokens(case), f"V=5 theta={theta}")
+    case = synth.make_case("s8_chain16x8", 63, B=2, N=3, V=5, dp=8, dq=8, theta=theta)
+    probs, tokens = _sampled_setup(case)
+    _check_sample(case, probs, tokens, f"V=5 sampled theta={theta}")
+
+
 @pytest.mark.parametrize("seed,theta,s", [(0, 0.1, 0.5), (1, 0.0, 0.5), (2, 0.3, 1.0), (3, 0.1, 0.0)])
 def test_sampled_chains_small(seed, theta, s):
     case = synth.make_case("s8_chain16x8", seed, V=3000, dp=256, dq=128, theta=theta, s=s)
@@ -322,6 +345,15 @@ def test_sampled_trees_small(seed, theta, s):
     walked = np.isfinite(o["walk_ratio"]) | np.isinf(o["walk_ratio"])
     _say(f"sampled trees seed {seed}: {int(walked.sum())} nodes tested on the walks, "
          f"accept lengths {g['accept_len'].tolist()}")
+
+
+@pytest.mark.parametrize("theta", [0.1, 0.0])
+def test_sampled_trees_odd_node_count(theta):
+    # 23 nodes per sequence: the walk's per-node LDS state at an odd count
+    case = synth.make_case("s8_chain16x8", 48, B=3, N=23, tree="tree", depth=4,
+                           max_children=5, V=2000, dp=128, dq=64, theta=theta)
+    probs, tokens = _sampled_tree_setup(case)
+    _check_sample(case, probs, tokens, f"sampled trees N=23 theta={theta}")
 
 
 def test_sampled_tree_forced_paths():
