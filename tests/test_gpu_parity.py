@@ -204,6 +204,31 @@ def test_sequence_status_codes():
     _check_greedy(case, tokens, "status codes")
 
 
+@pytest.mark.parametrize("which", ["separate", "none"])
+def test_bias_variants(which):
+    # one bias per model (the amateur's differs from the expert's), or none at all
+    # (null pointers: both models' logits unbiased)
+    case = synth.make_case("b8_tree64", 70, N=20, depth=4, max_children=4, V=1500, dp=128, dq=64)
+    zero = np.zeros(case.V, np.float32)
+    if which == "separate":
+        bp, bq = case.bias, (0.5 * case.bias - 0.25).astype(np.float32)
+    else:
+        bp = bq = None
+    op = bp if bp is not None else zero
+    oq = bq if bq is not None else zero
+    rows = oracle.eval_rows(case.hp, case.hq, case.wp, case.wq, op, oq, theta=case.theta, s=case.s)
+    tokens = synth.greedy_tokens(case, rows["argmax"])
+    _say(f"bias {which}: B={case.B} N={case.N} V={case.V}")
+    o = oracle.verify("greedy", case.B, case.N, case.hp, case.hq, case.wp, case.wq, op, oq,
+                      case.parents, tokens, theta=case.theta, s=case.s)
+    g = _runner().from_case(case, tokens, bias_p=bp, bias_q=bq).run("greedy")
+    report = {}
+    amb = parity.compare_rows(g, o, np.arange(case.R), report)
+    parity.compare_nodes(g, o, case.parents, amb, report)
+    parity.compare_greedy(g, o, case.parents, amb, report)
+    _say(f"bias {which}: ok {report}")
+
+
 def test_repeated_calls_are_bit_identical():
     case = synth.make_case("b8_tree64", 16, N=40, V=3001, dp=256, dq=128)
     tokens = _greedy_tokens(case)
@@ -241,6 +266,15 @@ def _check_sample(case, probs, tokens, label, seqs=None):
     assert np.all(np.abs(gr[fin] / orat[fin] - 1) < 1e-3)
     _say(f"{label}: ok {report}")
     return g, o
+
+
+@pytest.mark.parametrize("theta,T", [(1.0, 1.0), (0.1, 0.7), (0.0, 1.3)])
+def test_sampled_chains_mask_and_temperature(theta, T):
+    # theta = 1 (the target keeps only the tokens tied at the expert max) and
+    # temperatures other than 1 (dividing both models' logits before the mask)
+    case = synth.make_case("s8_chain16x8", 72, V=3000, dp=256, dq=128, theta=theta, T=T)
+    probs, tokens = _sampled_setup(case)
+    _check_sample(case, probs, tokens, f"sampled theta={theta} T={T}")
 
 
 @pytest.mark.parametrize("theta", [0.1, 0.0])
