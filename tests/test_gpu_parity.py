@@ -487,12 +487,15 @@ def test_full_s8_chain16x8(theta):
 
 
 @pytest.mark.slow
-def test_full_b8_batch32x64():
-    case = synth.make_case("b8_batch32x64", 0)
+@pytest.mark.parametrize("theta", [0.1, 0.0])
+def test_full_b8_batch32x64(theta):
+    # theta 0.1: the many-row kernel; theta 0: the streaming kernel's 64-row shape
+    # with 32 row blocks per tile
+    case = synth.make_case("b8_batch32x64", 0, theta=theta)
     # draft tokens copy the oracle's argmax in sequences 0 and 1; elsewhere they are random
     seqs = [0, 1]
     rows = np.concatenate([np.arange(b * 64, b * 64 + 64) for b in seqs])
-    _say("b8_batch32x64: oracle over sequences 0 and 1")
+    _say(f"b8_batch32x64 theta={theta}: oracle over sequences 0 and 1")
     o_rows = oracle.eval_rows(case.hp, case.hq, case.wp, case.wq, case.bias, case.bias,
                               theta=case.theta, s=case.s, rows=rows)
     amax = np.full(case.R, -1, np.int32)
@@ -518,7 +521,7 @@ def test_full_b8_batch32x64():
                               theta=case.theta, s=case.s, rows=spot)
     parity.compare_rows(g, o_spot, spot, report)
     parity.compare_diagnostics(g, o_spot, spot, case.theta, case.s, case.V, report)
-    _say(f"b8_batch32x64: ok {report}")
+    _say(f"b8_batch32x64 theta={theta}: ok {report}")
 
 
 # ------------------------------------------------------------------ final RMS normalisation
