@@ -59,16 +59,17 @@ __device__ __forceinline__ Best best_merge(Best x, Best y) {
     return (x.v > y.v || (x.v == y.v && (unsigned)x.id < (unsigned)y.id)) ? x : y;
 }
 
-struct Top2 {  // best value and id, runner-up value
+struct Top2 {  // best value and id, runner-up value; both models' logits at the best
     float v;
     int id;
     float v2;
+    float zp, zq;
 };
 
 __device__ __forceinline__ Top2 top2_merge(Top2 a, Top2 b) {
     const bool a_wins = b.id < 0 || (a.id >= 0 && (a.v > b.v || (a.v == b.v && a.id < b.id)));
     const Top2 w = a_wins ? a : b, l = a_wins ? b : a;
-    return Top2{w.v, w.id, fmaxf(w.v2, l.id >= 0 ? l.v : -INFINITY)};
+    return Top2{w.v, w.id, fmaxf(w.v2, l.id >= 0 ? l.v : -INFINITY), w.zp, w.zq};
 }
 
 // ---------------------------------------------------------------------------
@@ -78,14 +79,6 @@ __device__ __forceinline__ Lse wave_lse(Lse x) {
 #pragma unroll
     for (int d = kWaveSize / 2; d > 0; d >>= 1)
         x = lse_merge(x, Lse{__shfl_down(x.m, d, kWaveSize), __shfl_down(x.s, d, kWaveSize)});
-    return x;
-}
-
-__device__ __forceinline__ Top2 wave_top2(Top2 x) {
-#pragma unroll
-    for (int d = kWaveSize / 2; d > 0; d >>= 1)
-        x = top2_merge(x, Top2{__shfl_down(x.v, d, kWaveSize), __shfl_down(x.id, d, kWaveSize),
-                               __shfl_down(x.v2, d, kWaveSize)});
     return x;
 }
 
@@ -101,13 +94,6 @@ __device__ __forceinline__ Best wave_best(Best x) {
 #pragma unroll
     for (int d = kWaveSize / 2; d > 0; d >>= 1)
         x = best_merge(x, Best{__shfl_down(x.v, d, kWaveSize), __shfl_down(x.id, d, kWaveSize)});
-    return x;
-}
-
-__device__ __forceinline__ int wave_min_unsigned(int x) {
-#pragma unroll
-    for (int d = kWaveSize / 2; d > 0; d >>= 1)
-        x = (int)min((unsigned)x, (unsigned)__shfl_down(x, d, kWaveSize));
     return x;
 }
 
@@ -405,8 +391,14 @@ __device__ __forceinline__ void combine_row(const Plan &P, const Inputs &in, con
         issue_partials(base);
         mask_partials(base);
     }
-    lp = wave_lse(lp);
-    lq = wave_lse(lq);
+    // both trees one level at a time (the same merges as two separate trees)
+#pragma unroll
+    for (int d = kWaveSize / 2; d > 0; d >>= 1) {
+        const Lse op{__shfl_down(lp.m, d, kWaveSize), __shfl_down(lp.s, d, kWaveSize)};
+        const Lse oq{__shfl_down(lq.m, d, kWaveSize), __shfl_down(lq.s, d, kWaveSize)};
+        lp = lse_merge(lp, op);
+        lq = lse_merge(lq, oq);
+    }
     const float max_p = __shfl(lp.m, 0, kWaveSize);
     const float lse_p = __shfl(lp.m + __logf(lp.s), 0, kWaveSize);
     const float lse_q = __shfl(lq.m + __logf(lq.s), 0, kWaveSize);
@@ -416,7 +408,7 @@ __device__ __forceinline__ void combine_row(const Plan &P, const Inputs &in, con
     // 2. candidates of the tiles that kept any, compacted into LDS so that their
     //    logits are fetched in one round
     Lse lc{-INFINITY, 0.f};
-    Top2 best{-INFINITY, -1, -INFINITY};
+    Top2 best{-INFINITY, -1, -INFINITY, 0.f, 0.f};
     int count = 0;
     int top_p = -1;  // the expert's top-1: the lowest candidate whose z_p is max_p
     for (int base = 0; base < P.ntiles; base += kPass) {
@@ -443,24 +435,30 @@ __device__ __forceinline__ void combine_row(const Plan &P, const Inputs &in, con
                 ++count;
                 top_p = c.x == max_p ? (int)min((unsigned)top_p, (unsigned)t) : top_p;
                 const float cd = (1.f + s) * (c.x - lse_p) - s * (c.y - lse_q);
-                best = top2_merge(best, Top2{cd, t, -INFINITY});
+                best = top2_merge(best, Top2{cd, t, -INFINITY, c.x, c.y});
                 lc = lse_merge(lc, Lse{cd, 1.f});
             }
             wave_lds_sync();
         }
     }
-    lc = wave_lse(lc);
-    best = wave_top2(best);
-    count = wave_sum(count);
-    top_p = wave_min_unsigned(top_p);
+    // the four trees one level at a time (the same merges as separate trees)
+#pragma unroll
+    for (int d = kWaveSize / 2; d > 0; d >>= 1) {
+        const Lse oc{__shfl_down(lc.m, d, kWaveSize), __shfl_down(lc.s, d, kWaveSize)};
+        const Top2 ob{__shfl_down(best.v, d, kWaveSize), __shfl_down(best.id, d, kWaveSize),
+                      __shfl_down(best.v2, d, kWaveSize), __shfl_down(best.zp, d, kWaveSize),
+                      __shfl_down(best.zq, d, kWaveSize)};
+        const int on = __shfl_down(count, d, kWaveSize), ot = __shfl_down(top_p, d, kWaveSize);
+        lc = lse_merge(lc, oc);
+        best = top2_merge(best, ob);
+        count += on;
+        top_p = (int)min((unsigned)top_p, (unsigned)ot);
+    }
 
     if (lane == 0) {
         const float logZ = lc.m + __logf(lc.s);
-        float signal = NAN;
-        if (best.id >= 0) {
-            const float2 c = cz[best.id];
-            signal = (c.x - lse_p) - (c.y - lse_q);
-        }
+        // the best candidate's logits came along with it (no second fetch)
+        const float signal = best.id >= 0 ? (best.zp - lse_p) - (best.zq - lse_q) : NAN;
         float ri[kRowInfo] = {};
         ri[RI_MAXP] = max_p;
         ri[RI_LSEP] = lse_p;
