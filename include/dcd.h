@@ -61,7 +61,7 @@ enum {
     DCD_ERR_PARAM = -3,       /* plaus_thresh, cd_strength, temperature or dtype invalid */
     DCD_ERR_ALIGN = -4,       /* pointer or hidden-size alignment violated */
     DCD_ERR_WORKSPACE = -5,   /* workspace NULL, not 256-byte aligned, or smaller than dcd_workspace_bytes() */
-    DCD_ERR_UNSUPPORTED = -6, /* valid request this build does not implement */
+    DCD_ERR_UNSUPPORTED = -6, /* valid request the library does not implement */
     DCD_ERR_HIP = -7          /* the HIP runtime rejected a launch */
 };
 
