@@ -198,7 +198,7 @@ size_t workspace_layout(Plan &p, char *base) {
     }
     p.rowinfo = (float *)take(R * kRowInfo * sizeof(float));
     p.tcount = (int *)take(R * p.ntiles * sizeof(int));
-    p.bound = (int *)take(R * sizeof(int));
+    p.bound = (int *)take((size_t)kBoundCopies * R * sizeof(int));
     p.nodez = (float4 *)take(R * sizeof(float4));
     p.seqdone = (int *)take((size_t)p.B * sizeof(int));
     if (p.final_norm) {

@@ -60,7 +60,7 @@ struct Plan {
                        //    token whose z_p is the tile's expert max)
     float *rowinfo;    // [R][kRowInfo]
     int *tcount;       // [R][ntiles]   candidates per (row, tile); bitmap words valid where > 0
-    int *bound;        // [R]           running lower bound on max z_p (order-preserving int key)
+    int *bound;        // [kBoundCopies][R] running lower bound on max z_p (order-preserving int key)
     float4 *nodez;     // [R]           (z_p, z_q, candidate?) of node r's token under its parent row
     int *seqdone;      // [B]           rows of each sequence finished by the combine step
     void *hn_p, *hn_q; // [R][d_p], [R][d_q] final_norm: the normalised hidden states
@@ -91,6 +91,25 @@ __device__ __forceinline__ int ordered_key(float f) {
 }
 __device__ __forceinline__ float key_value(int k) {
     return __int_as_float(k >= 0 ? k : k ^ 0x7fffffff);
+}
+
+// The streaming LM-head kernel keeps the running row bounds in one copy per XCD (a
+// workgroup raises the copy of its XCD, blockIdx.x % 8): every tile's expert
+// epilogue raises the bounds of its rows at about the same time, and 8 copies
+// divide the contention on each word by 8.  A reader takes the max over the
+// copies, a lower bound on the row's max either way.  The many-row kernel, whose
+// epilogues are spread out, uses copy 0 alone.
+constexpr int kBoundCopies = 8;
+
+__device__ __forceinline__ void raise_bound(int *bound, int R, int row, float v) {
+    atomicMax(&bound[(int)(blockIdx.x % kBoundCopies) * R + row], ordered_key(v));
+}
+
+__device__ __forceinline__ float read_bound(const int *bound, int R, int row) {
+    int k = __atomic_load_n(&bound[row], __ATOMIC_RELAXED);
+#pragma unroll
+    for (int c = 1; c < kBoundCopies; ++c) k = max(k, __atomic_load_n(&bound[c * R + row], __ATOMIC_RELAXED));
+    return key_value(k);
 }
 
 // Untruncated target: statistics of y = (1+s) z_p - s z_q over a set of tokens.

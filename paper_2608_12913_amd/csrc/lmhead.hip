@@ -453,7 +453,7 @@ __device__ __forceinline__ void tile_body(const Plan &P, const Inputs &in, int t
             stash[rb * kWaveSize + lane] = first;
             over |= (f & (f - 1)) != 0;
             // running lower bound on the row's expert max: one update per (row, tile)
-            if (wave == 0 && g == 0 && row < P.R) atomicMax(&P.bound[row], ordered_key(pmax[rb]));
+            if (wave == 0 && g == 0 && row < P.R) raise_bound(P.bound, P.R, row, pmax[rb]);
         }
         if (__builtin_amdgcn_ballot_w64(over)) {  // wave-uniform: some lane has more than one
 #pragma unroll
@@ -566,7 +566,7 @@ __device__ __forceinline__ void tile_body(const Plan &P, const Inputs &in, int t
 #pragma unroll
         for (int rb = 0; rb < RB; ++rb) {
             const int row = min(row0 + rb * 16 + n, P.R - 1);
-            bnd[rb] = flags[rb] ? key_value(__atomic_load_n(&P.bound[row], __ATOMIC_RELAXED)) : 0.f;
+            bnd[rb] = flags[rb] ? read_bound(P.bound, P.R, row) : 0.f;
         }
         for (int i = tid; i < ROWS * kWordsPerTile; i += NT) twords[i] = 0;
         if (tid < ROWS) tcnt[tid] = 0;
@@ -649,7 +649,7 @@ __global__ __launch_bounds__(NT, kMinBlocks) void lmhead_kernel(Plan P, Inputs i
 // step at 0, for every call.
 __global__ void init_kernel(int *bound, int R, int *seqdone, int B) {
     const int r = blockIdx.x * blockDim.x + threadIdx.x;
-    if (r < R) bound[r] = ordered_key(-INFINITY);
+    if (r < kBoundCopies * R) bound[r] = ordered_key(-INFINITY);
     if (r < B) seqdone[r] = 0;
 }
 #endif
@@ -684,7 +684,7 @@ hipError_t launch_skinny(const Plan &p, const Inputs &in, hipStream_t st) {
 hipError_t launch_lmhead_rows64(const Plan &p, const Inputs &in, hipStream_t st) { return launch_skinny(p, in, st); }
 
 hipError_t launch_lmhead(const Plan &p, const Inputs &in, hipStream_t st) {
-    const int ninit = p.R > p.B ? p.R : p.B;
+    const int ninit = kBoundCopies * p.R > p.B ? kBoundCopies * p.R : p.B;
     hipLaunchKernelGGL(init_kernel, dim3((ninit + 255) / 256), dim3(256), 0, st, p.bound, p.R, p.seqdone,
                        p.B);
     if (use_wide_lmhead(p)) return launch_lmhead_wide(p, in, st);
