@@ -290,7 +290,7 @@ __device__ __forceinline__ float wave_sum16_32(float x) {
 
 // Logits of this lane's 16*VB (token, row) values and, per row, the tile's max and
 // sum of exp relative to it.  One LDS exchange of (wave max, wave sum) pairs,
-// merged in wave order.
+// merged in wave order by one thread per row.
 //   bias_lds        the tile's bias already divided by T (0 without a bias)
 //   z[vb][rb][j]    logit (divided by T); -inf for tokens >= V (ragged tile only)
 //   tmax[rb], tsum[rb]   of row 16rb + lane%16
@@ -333,21 +333,29 @@ __device__ __forceinline__ void tile_softmax(const f32x4 (&acc)[VB][RB], const f
         if (g == 0) pairs[wave * ROWS + rb * 16 + n] = float2{m, s};
     }
     __syncthreads();
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb) {
+    // one thread per row merges the waves' pairs in wave order and leaves the result
+    // in wave 0's slot of the row (only that thread touches the row's slots)
+    if (threadIdx.x < ROWS) {
+        const int r = threadIdx.x;
         float m = -INFINITY;
 #pragma unroll
-        for (int w = 0; w < NW; ++w) m = fmaxf(m, pairs[w * ROWS + rb * 16 + n].x);
+        for (int w = 0; w < NW; ++w) m = fmaxf(m, pairs[w * ROWS + r].x);
         float s = 0.f;
         if (m != -INFINITY) {
 #pragma unroll
             for (int w = 0; w < NW; ++w) {
-                const float2 pw = pairs[w * ROWS + rb * 16 + n];
+                const float2 pw = pairs[w * ROWS + r];
                 if (pw.x != -INFINITY) s += pw.y * __expf(pw.x - m);
             }
         }
-        tmax[rb] = m;
-        tsum[rb] = s;
+        pairs[r] = float2{m, s};
+    }
+    __syncthreads();
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+        const float2 t = pairs[rb * 16 + n];
+        tmax[rb] = t.x;
+        tsum[rb] = t.y;
     }
     __syncthreads();  // the pairs are reused
 }
