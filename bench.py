@@ -29,6 +29,14 @@ HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # dense bf16 MFMA, TFLOP/s
 
 METRIC = "verified draft nodes/sec (8B/1B-shaped, 64-node tree); % of HBM peak"
+# the same metric on the other workloads, named by what each is
+METRICS = {
+    "b8_tree64": METRIC,
+    "tiny_chain8": "verified draft nodes/sec (tiny fp32 chain of 8 nodes)",
+    "s8_chain16x8": "verified draft nodes/sec (8B/1B-shaped, 16 sampled chains of 8 nodes); % of HBM peak",
+    "b8_batch32x64": "verified draft nodes/sec (8B/1B-shaped, 32 x 64-node trees); % of MFMA peak",
+    "b70_tree64": "verified draft nodes/sec (70B/8B-shaped, 64-node tree); % of HBM peak",
+}
 
 
 def algorithmic_bytes(case) -> int:
@@ -122,10 +130,11 @@ def main():
         dev = DeviceProblem.from_case(case, tokens, draft_probs=probs, **norm)
     else:
         # draft tokens: half copy the target argmax of the parent row (taken from a first
-        # verification call on the GPU), half are uniform
+        # verification call on the GPU), half are uniform; in a tree, the nodes of one
+        # deepest path all copy it, so the walk accepts a full-depth path
         dev = DeviceProblem.from_case(case, np.zeros((case.B, case.N), np.int32), **norm)
         first = dev.run("greedy")
-        tokens = synth.greedy_tokens(case, first["row_argmax"])
+        tokens = synth.greedy_tokens(case, first["row_argmax"], spine=case.cfg["tree"] == "tree")
         dev.set_tokens(tokens)
     if mode == "propose":
         u = torch.from_numpy(case.u_res.astype(np.float32)).to(dev.device)
@@ -205,10 +214,12 @@ def main():
         log("cpu baseline: only for the greedy verification of the workload's own rows")
     elif not args.no_cpu_baseline:
         cpu = cpu_baseline(case, tokens, log)
+        cpu["single_core"] = cpu_single_core(case, tokens, log)
 
     step_bytes = algorithmic_bytes(case)
+    metric = METRICS.get(args.workload, f"verified draft nodes/sec ({args.workload})")
     line = {
-        "metric": METRIC if mode != "propose" else "proposal rows/sec (recombined heads)",
+        "metric": metric if mode != "propose" else "proposal rows/sec (recombined heads)",
         "value": round(nodes_per_s, 1),
         "unit": "nodes/s",
         "n_gpus": 1,
@@ -225,6 +236,10 @@ def main():
                    "cd_strength": case.s, "rows": R, "seed": args.seed, "mode": mode,
                    "final_norm": bool(args.final_norm)},
         "hbm_frac_step": round(step_bytes / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        # rows scored per second without the roots (each sequence's root is the last
+        # committed token, not a drafted one), and what the timed calls accepted
+        "drafted_nodes_per_s": round((R - case.B) / (ms_step * 1e-3), 1),
+        "accept_len": out["accept_len"].tolist() if mode != "propose" else None,
         "roofline": roofline,
         "cpu_baseline": cpu,
     }
@@ -323,9 +338,45 @@ def cpu_baseline(case, tokens, log, min_seconds=10.0):
             break
     log(f"cpu baseline: {reps} verifications in {dt:.2f} s")
     return {"value": round(reps * case.R / dt, 3), "unit": "nodes/s", "cores": threads,
-            "kind": "oracle",
+            "kind": "oracle", "cpu_model": cpu_model(),
             "sample": f"{reps} full {case.name} verifications ({case.R} rows each, fp64 "
                       f"oracle) in {dt:.2f} s"}
+
+
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
+def cpu_single_core(case, tokens, log, max_macs=8e9):
+    """The oracle on one thread: complete verifications when one takes at most
+    max_macs multiply-adds, else the first rows of the workload (the LM-head dot
+    products are nearly all of a row's work and the walk is negligible), timed and
+    scaled to nodes/s."""
+    import oracle
+
+    hp, hq = oracle.as_f32(case.hp), oracle.as_f32(case.hq)
+    wp, wq = oracle.as_f32(case.wp), oracle.as_f32(case.wq)
+    per_row = case.V * (case.dp + case.dq)
+    t0 = time.perf_counter()
+    if per_row * case.R <= max_macs:
+        oracle.verify("greedy", case.B, case.N, hp, hq, wp, wq, case.bias, case.bias,
+                      case.parents, tokens, theta=case.theta, s=case.s, nthreads=1)
+        n, what = case.R, f"1 full {case.name} verification ({case.R} rows)"
+    else:
+        n = max(1, int(max_macs // per_row))
+        oracle.eval_rows(hp, hq, wp, wq, case.bias, case.bias, theta=case.theta, s=case.s,
+                         rows=np.arange(n), nthreads=1)
+        what = f"the first {n} of {case.R} rows of {case.name} (row evaluation only)"
+    dt = time.perf_counter() - t0
+    log(f"cpu baseline, 1 thread: {what} in {dt:.2f} s")
+    return {"value": round(n / dt, 3), "unit": "nodes/s", "cores": 1,
+            "sample": f"{what} in {dt:.2f} s"}
 
 
 if __name__ == "__main__":

@@ -121,7 +121,8 @@ static void max_and_lse(const double *z, int V, double *M, double *lse)
 typedef struct {
     double stats[RS_N];
     int argmax;
-    double gap; /* min over v of |z_p[v] - M_p - ln theta|; +inf when theta = 0 */
+    double gap; /* min over v below the max of |z_p[v] - M_p - ln theta|; +inf when
+                   theta = 0 or every token is at the max */
 } row_result;
 
 /*
@@ -136,11 +137,14 @@ static void cd_row(const double *zp, const double *zq, int V, double theta, doub
     max_and_lse(zq, V, &Mq, &lseq);
     const double log_theta = theta > 0.0 ? log(theta) : -INFINITY;
 
-    /* pass 1: mask membership, cd score, argmax (lowest id on ties), runner-up */
+    /* pass 1: mask membership, cd score, argmax (lowest id on ties), runner-up.
+       gap: how close a token's membership test comes to flipping.  A token at the
+       expert max is a member for every theta (its test is 0 >= ln theta), so only
+       the tokens below the max count. */
     int best = -1, count = 0;
     double top1 = -INFINITY, top2 = -INFINITY, gap = INFINITY;
     for (int v = 0; v < V; ++v) {
-        if (theta > 0.0) {
+        if (theta > 0.0 && zp[v] != Mp) {
             double dist = fabs(zp[v] - Mp - log_theta);
             if (dist < gap) gap = dist;
         }

@@ -61,7 +61,8 @@ struct Plan {
     float *rowinfo;    // [R][kRowInfo]
     int *tcount;       // [R][ntiles]   candidates per (row, tile); bitmap words valid where > 0
     int *bound;        // [kBoundCopies][R] running lower bound on max z_p (order-preserving int key)
-    float4 *nodez;     // [R]           (z_p, z_q, candidate?) of node r's token under its parent row
+    float4 *nodez;     // [R]           node r's token under its parent row: (z_p, z_q) as a candidate
+                       //   (NaN: not one), (z_p, z_q) by dot product (NaN: not computed)
     int *seqdone;      // [B]           rows of each sequence finished by the combine step
     void *hn_p, *hn_q; // [R][d_p], [R][d_q] final_norm: the normalised hidden states
 };

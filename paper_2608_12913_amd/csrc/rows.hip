@@ -12,7 +12,12 @@
 //   tree / token checks, draft-token statistics under the parent row, then either
 //   the greedy walk from the root or Alg. 1's accept test with the residual /
 //   bonus draw along a chain.
-// All reductions run in a fixed order, so repeated calls are bit-identical.
+// Repeated calls are bit-identical.  All reductions run in a fixed order, and
+// nothing read depends on timing: which vocabulary tiles keep their candidates
+// depends on when each read the running bound of the LM-head step, so the row
+// phase takes only the tiles whose own expert max reaches the row's threshold
+// (those are never dropped, and hold every mask member), and a draft token's
+// logits come from the candidates only when the token is a mask member.
 #include "dcd_internal.h"
 
 namespace dcd {
@@ -299,27 +304,29 @@ __device__ __forceinline__ void combine_row(const Plan &P, const Inputs &in, con
                                   (const char *)in.wq + (size_t)x * P.dq * esz, P.dq, lane);
                 zq = (zq + (in.bq ? in.bq[x] : 0.f)) * P.inv_T;
             }
-            if (lane == 0) P.nodez[row] = float4{zp, zq, 1.f, 0.f};
+            if (lane == 0) P.nodez[row] = float4{zp, zq, zp, zq};
             __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
             return;
         }
-        // count, bitmap word and candidate slot are fetched together
+        // count, bitmap word and candidate slot are fetched together.  The parent
+        // row's threshold is not known yet, so both forms are kept: the candidate's
+        // logits (NaN when the token is not a candidate of a kept tile) and, when
+        // node statistics are wanted, a dot product.  The sequence phase takes the
+        // candidate's only for a mask member, whose tile is never dropped, so the
+        // choice does not depend on which tiles the running bound pruned.
         const int tcnt = P.tcount[rowj * P.ntiles + x / kTileTokens];
         const uint32_t word = P.bits[rowj * P.wstride + (x >> 5)];
         const float2 c = P.cand[rowj * P.V + x];
         const bool cand = tcnt > 0 && (word >> (x & 31) & 1u);
-        float4 nz{0.f, 0.f, 0.f, 0.f};
-        if (cand) {
-            nz = float4{c.x, c.y, 1.f, 0.f};
-        } else if (want_node_logits) {
+        float4 nz{cand ? c.x : NAN, cand ? c.y : NAN, NAN, NAN};
+        if (want_node_logits) {
             const size_t esz = DT == kBF16 ? 2 : 4;
             float zp = wave_dot<DT>((const char *)in.hp + rowj * P.dp * esz,
                                     (const char *)in.wp + (size_t)x * P.dp * esz, P.dp, lane);
             float zq = wave_dot<DT>((const char *)in.hq + rowj * P.dq * esz,
                                     (const char *)in.wq + (size_t)x * P.dq * esz, P.dq, lane);
-            zp = (zp + (in.bp ? in.bp[x] : 0.f)) * P.inv_T;
-            zq = (zq + (in.bq ? in.bq[x] : 0.f)) * P.inv_T;
-            nz = float4{zp, zq, 0.f, 0.f};
+            nz.z = (zp + (in.bp ? in.bp[x] : 0.f)) * P.inv_T;
+            nz.w = (zq + (in.bq ? in.bq[x] : 0.f)) * P.inv_T;
         }
         if (lane == 0) P.nodez[row] = nz;
         // publish nodez at device scope before the row is counted (wave 0's
@@ -344,6 +351,7 @@ __device__ __forceinline__ void combine_row(const Plan &P, const Inputs &in, con
     // Loads are issued unconditionally from clamped indices and masked
     // afterwards (with selects), so that all of them are in flight together.
     int c[kTilesPerLane];
+    float tm[kTilesPerLane];  // the tile's expert max (its partial)
     auto issue_partials = [&](int base) {
 #pragma unroll
         for (int k = 0; k < kTilesPerLane; ++k) v[k] = pr[min(base + lane + k * kWaveSize, P.ntiles - 1)];
@@ -353,6 +361,7 @@ __device__ __forceinline__ void combine_row(const Plan &P, const Inputs &in, con
         for (int k = 0; k < kTilesPerLane; ++k) {
             const int t = min(base + lane + k * kWaveSize, P.ntiles - 1);
             c[k] = tc[t];
+            tm[k] = pr[t].x;
 #pragma unroll
             for (int q = 0; q < kTileU4; ++q) w[k][q] = bw[kTileU4 * t + q];
         }
@@ -364,11 +373,16 @@ __device__ __forceinline__ void combine_row(const Plan &P, const Inputs &in, con
             v[k] = ok ? v[k] : float4{-INFINITY, 0.f, -INFINITY, 0.f};
         }
     };
+    // (called once thr is known) the words of a tile count only if the tile kept
+    // candidates (otherwise they are stale) and its expert max reaches thr: only
+    // such a tile can hold mask members, and the LM-head step never drops it,
+    // whatever the timing; the others are dropped here too
+    float thr = 0.f;
     auto mask_cands = [&](int base) {
 #pragma unroll
         for (int k = 0; k < kTilesPerLane; ++k) {
-            // words of tiles without candidates are stale
-            const uint32_t keep = (base + lane + k * kWaveSize < P.ntiles && c[k] > 0) ? ~0u : 0u;
+            const uint32_t keep =
+                (base + lane + k * kWaveSize < P.ntiles && c[k] > 0 && tm[k] >= thr) ? ~0u : 0u;
 #pragma unroll
             for (int q = 0; q < kTileU4; ++q) w[k][q] = mask4(w[k][q], keep);
         }
@@ -402,7 +416,7 @@ __device__ __forceinline__ void combine_row(const Plan &P, const Inputs &in, con
     const float max_p = __shfl(lp.m, 0, kWaveSize);
     const float lse_p = __shfl(lp.m + __logf(lp.s), 0, kWaveSize);
     const float lse_q = __shfl(lq.m + __logf(lq.s), 0, kWaveSize);
-    const float thr = max_p + P.log_theta;
+    thr = max_p + P.log_theta;
     const float s = P.s;
 
     // 2. candidates of the tiles that kept any, compacted into LDS so that their
@@ -500,11 +514,16 @@ struct NodeStat {
     bool in_mask;
 };
 
+// nz = (z_p, z_q) of the token as a candidate (NaN: not one) and by dot product
+// (NaN when node statistics are not wanted).  A token is a mask member iff it is a
+// candidate at or above the row's threshold; then the candidate's values are the
+// ones the row phase used, otherwise the dot product's.
 __device__ __forceinline__ NodeStat node_stat(float4 nz, RowInfo rj, float s) {
     NodeStat n;
-    n.in_mask = nz.z != 0.f && nz.x >= rj.b.x;
-    n.lpp = nz.x - rj.a.y;
-    n.lpq = nz.y - rj.a.z;
+    n.in_mask = nz.x >= rj.b.x;
+    const float zp = n.in_mask ? nz.x : nz.z, zq = n.in_mask ? nz.y : nz.w;
+    n.lpp = zp - rj.a.y;
+    n.lpq = zq - rj.a.z;
     n.cd = (1.f + s) * n.lpp - s * n.lpq;
     n.lpcd = n.in_mask ? n.cd - rj.a.w : -INFINITY;
     return n;
@@ -585,11 +604,15 @@ __device__ __forceinline__ int masked_scan(const Plan &P, size_t jrow, const Res
     // token order
     const int t0 = (int)((long long)tid * P.ntiles / NT);
     const int t1 = (int)((long long)(tid + 1) * P.ntiles / NT);
+    const float4 *pr = P.partials + jrow * P.ntiles;
     auto tile_words = [&](int t, uint4 (&w)[kTileU4]) {
         const int c = tc[t];
+        const float tmax = pr[t].x;
 #pragma unroll
         for (int q = 0; q < kTileU4; ++q) w[q] = bw[kTileU4 * t + q];
-        const uint32_t keep = c > 0 ? ~0u : 0u;  // words are stale without candidates
+        // words are stale without candidates; a tile below thr holds no mask member
+        // (the row phase's rule, so the gathered list never depends on timing)
+        const uint32_t keep = c > 0 && tmax >= thr ? ~0u : 0u;
 #pragma unroll
         for (int q = 0; q < kTileU4; ++q) w[q] = mask4(w[q], keep);
     };
@@ -698,7 +721,9 @@ __device__ __forceinline__ int full_scan(const Plan &P, size_t jrow, const Resid
     const int k = 4 * max(1, (P.V + 4 * kList * kWaveSize - 1) / (4 * kList * kWaveSize));
     const int bt = k * kWaveSize;
     const int nblk = (P.V + bt - 1) / bt;
-    const bool q4 = P.V % 4 == 0;  // draft_probs rows are 16-byte aligned
+    // 16-byte loads of the proposal row only where it is 16-byte aligned (the ABI
+    // asks 4 bytes of draft_probs)
+    const bool q4 = P.V % 4 == 0 && (reinterpret_cast<uintptr_t>(res.qnext) & 15) == 0;
     // the raw inputs of tokens t .. t+3: loads clamped into the rows (the dense and
     // stored rows have zstride entries, the proposal rows V), values past the
     // vocabulary discarded by weigh4

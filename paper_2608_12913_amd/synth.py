@@ -199,19 +199,50 @@ def _pick_excluding(u: float, V: int, excluded: set) -> int:
     return k
 
 
-def greedy_tokens(case: Case, row_argmax: np.ndarray) -> np.ndarray:
+def deepest_path(parents: np.ndarray) -> list:
+    """Nodes of the root-to-node path that ends at the deepest node (the lowest index
+    among equally deep ones), root first."""
+    N = len(parents)
+    depth = np.zeros(N, dtype=np.int64)
+    for i in range(1, N):
+        depth[i] = depth[parents[i]] + 1
+    node = int(np.argmax(depth))
+    path = [node]
+    while node > 0:
+        node = int(parents[node])
+        path.append(node)
+    return path[::-1]
+
+
+def greedy_tokens(case: Case, row_argmax: np.ndarray, spine: bool = False) -> np.ndarray:
     """Draft tokens for greedy workloads: with probability 1/2 (the case's coin) a
     node copies the target argmax of its parent's row (given by the caller), else it
-    is uniform over the vocabulary; siblings never repeat a token."""
+    is uniform over the vocabulary; siblings never repeat a token.  An unknown argmax
+    (< 0: the caller did not compute that row) makes the node's token uniform.
+
+    spine=True: in addition, every node of one deepest root-to-leaf path copies its
+    parent row's argmax (the token is reserved before its siblings draw theirs), so
+    the tree holds a full-depth path that a greedy target accepts.  A sequence whose
+    path crosses a row with an unknown argmax (< 0) keeps the coin rule."""
     row_argmax = np.asarray(row_argmax).reshape(case.B, case.N)
     tokens = np.zeros((case.B, case.N), dtype=np.int32)
     for b in range(case.B):
         used = {}
+        forced = {}
+        if spine:
+            path = deepest_path(case.parents[b])
+            if all(row_argmax[b, j] >= 0 for j in path[:-1]):
+                for j, c in zip(path[:-1], path[1:]):
+                    forced[c] = int(row_argmax[b, j])
+                    used.setdefault(j, set()).add(forced[c])
         for i in range(1, case.N):
             j = int(case.parents[b, i])
             sib = used.setdefault(j, set())
+            if i in forced:
+                tokens[b, i] = forced[i]
+                continue
             t = int(row_argmax[b, j])
-            if not (case.coins[b, i] and t not in sib):
+            if not (case.coins[b, i] and t >= 0 and t not in sib):
                 t = _pick_excluding(float(case.u_token[b, i]), case.V, sib)
             sib.add(t)
             tokens[b, i] = t

@@ -49,9 +49,15 @@ def _check(case, u, label):
     sup = ok[:, None] & (po > 1e-30)
     d = np.abs(np.log(pg[sup]) - np.log(po[sup]))
     assert d.max() <= parity.ATOL, f"log-prob max diff {d.max()}"
+    # the draw's gate: each probability within a factor e^delta of the oracle's moves a
+    # cumulative breakpoint, relative to the total, by at most about 2 delta
+    assert d.max() <= parity.CDF_GATE / 2, f"log-prob max diff {d.max()} exceeds CDF_GATE / 2"
+    assert (~ok).sum() <= 0.01 * case.R + 1, f"{int((~ok).sum())} ambiguous rows"
     np.testing.assert_allclose(pg[ok].sum(axis=1), 1.0, atol=1e-4)
     assert np.array_equal(g["argmax"][ok], o["argmax"][ok])
     clear = ok & (o["gap"] > parity.CDF_GATE)
+    # every draw is gated by its distance to the nearest breakpoint: few may be
+    assert clear.sum() >= 0.95 * ok.sum() - 1, f"{int(ok.sum() - clear.sum())} draws gated"
     assert np.array_equal(g["tokens"][clear], o["tokens"][clear]), "drawn tokens"
     print(f"[propose] {label}: ok, {int(ok.sum())}/{case.R} rows compared, "
           f"{int(clear.sum())} draws", flush=True)
@@ -94,10 +100,17 @@ def test_proposals_feed_sampled_verification():
     o = oracle.verify("sample", case.B, case.N, case.hp, case.hq, case.wp, case.wq, case.bias,
                       case.bias, case.parents, tokens, theta=case.theta, s=case.s, temperature=case.T,
                       draft_probs=probs, u_acc=case.u_acc, u_res=case.u_res)
-    v = DeviceProblem.from_case(case, tokens, draft_probs=probs).run("sample")
+    lp = oracle.eval_rows(case.hp, case.hq, case.wp, case.wq, case.bias, case.bias,
+                          theta=case.theta, s=case.s, temperature=case.T, want_lpcd=True)["lpcd"]
+    vdev = DeviceProblem.from_case(case, tokens, draft_probs=probs)
+    v = vdev.run("sample")
     report = {}
     amb = parity.compare_rows(v, o, np.arange(case.R), report)
-    parity.compare_sample(v, o, case.parents, case.u_acc, tokens, o["row_gap"] <= parity.BOUNDARY_GATE,
-                          report)
+    parity.compare_nodes(v, o, case.parents, amb, report)
+    boundary = o["row_gap"] <= parity.BOUNDARY_GATE
+    parity.measure_target_error(vdev.propose(case.u_res)["probs"], lp, boundary, report)
+    parity.compare_sample(v, o, lp, probs, case.parents, tokens, case.u_acc, case.u_res,
+                          boundary, report)
+    parity.check_gates(report)
     print(f"[propose] feeding verification: {report}, accept lengths {v['accept_len'].tolist()}",
           flush=True)

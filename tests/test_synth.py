@@ -67,3 +67,34 @@ def test_greedy_tokens_siblings_distinct_and_coins():
             if tok[0, k] == 7 and c.coins[0, k]:
                 break
     assert np.all((tok[0, 1:] >= 0) & (tok[0, 1:] < 1000))
+
+
+def test_spine_tokens_give_a_full_depth_path():
+    """spine=True: the deepest root-to-leaf path copies its parent rows' argmax (no
+    sibling holds that token), the other nodes follow the coin rule, and the oracle's
+    greedy walk accepts the path to full depth."""
+    import oracle
+
+    c = synth.make_case("b8_tree64", 0, V=500, dp=16, dq=8)
+    rng = np.random.default_rng(3)
+    amax = rng.integers(0, 500, c.R).astype(np.int32)
+    tok = synth.greedy_tokens(c, amax, spine=True)
+    path = synth.deepest_path(c.parents[0])
+    assert len(path) == 9 and path[0] == 0
+    for j, k in zip(path[:-1], path[1:]):
+        assert c.parents[0, k] == j and tok[0, k] == amax[j]
+        sib = np.flatnonzero(c.parents[0] == j)
+        assert np.sum(tok[0, sib] == amax[j]) == 1
+        assert len(set(tok[0, sib])) == len(sib)
+    plain = synth.greedy_tokens(c, amax)
+    off = [i for i in range(1, c.N) if i not in path and c.parents[0, i] not in path[:-1]]
+    assert np.array_equal(tok[0, off], plain[0, off])
+    L, walk, nxt = oracle.greedy_walk(c.parents[0], tok[0], amax)
+    assert L == 8 and list(walk[:9]) == path and nxt == amax[path[-1]]
+    # an unknown argmax (< 0) on the path keeps the coin rule for that sequence, and a
+    # heads coin under an unknown argmax draws a random token
+    amax2 = amax.copy()
+    amax2[path[3]] = -1
+    t2 = synth.greedy_tokens(c, amax2, spine=True)
+    assert np.array_equal(t2, synth.greedy_tokens(c, amax2))
+    assert np.all(t2 >= 0)
