@@ -12,6 +12,7 @@ import os
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(PKG, "libdcd.so")
+PROBE_LIB_PATH = os.path.join(PKG, "libdcd_probe.so")  # the benchmark's measurement probes
 
 DCD_OK, DCD_ERR_NULL, DCD_ERR_SHAPE, DCD_ERR_PARAM = 0, -1, -2, -3
 DCD_ERR_ALIGN, DCD_ERR_WORKSPACE, DCD_ERR_UNSUPPORTED, DCD_ERR_HIP = -4, -5, -6, -7
@@ -21,9 +22,8 @@ ROW_MAX_P, ROW_LSE_P, ROW_LSE_Q, ROW_LOGZ, ROW_TOP1, ROW_MARGIN, ROW_COUNT, ROW_
 NODE_LOGP_P, NODE_LOGP_Q, NODE_CD, NODE_LOGP_CD, NODE_IN_MASK, NODE_RATIO = range(6)
 
 EXPORTS = ("dcd_workspace_bytes", "dcd_verify_greedy", "dcd_verify_sample",
-           "dcd_lmhead_partials", "dcd_propose", "dcd_error_string", "dcd_abi_version",
-           # include/dcd_probe.h
-           "dcd_probe_stream_read", "dcd_probe_mfma_bf16")
+           "dcd_lmhead_partials", "dcd_propose", "dcd_error_string", "dcd_abi_version")
+PROBE_EXPORTS = ("dcd_probe_stream_read", "dcd_probe_mfma_bf16")  # include/dcd_probe.h
 
 
 class DcdError(RuntimeError):
@@ -81,13 +81,28 @@ def lib() -> ctypes.CDLL:
         L.dcd_error_string.restype = ctypes.c_char_p
         L.dcd_abi_version.argtypes = []
         L.dcd_abi_version.restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+_probe_lib = None
+
+
+def probe_lib() -> ctypes.CDLL:
+    """The measurement probes (include/dcd_probe.h), a library of their own."""
+    global _probe_lib
+    if _probe_lib is None:
+        if not os.path.exists(PROBE_LIB_PATH):
+            raise RuntimeError(f"{PROBE_LIB_PATH} is not built: run __graft_entry__.build()")
+        L = ctypes.CDLL(PROBE_LIB_PATH)
+        P = ctypes.c_void_p
         L.dcd_probe_stream_read.argtypes = [P, ctypes.c_size_t, P, P]
         L.dcd_probe_stream_read.restype = ctypes.c_int
         L.dcd_probe_mfma_bf16.argtypes = [ctypes.c_int, ctypes.c_int, P,
                                           ctypes.POINTER(ctypes.c_double), P]
         L.dcd_probe_mfma_bf16.restype = ctypes.c_int
-        _lib = L
-    return _lib
+        _probe_lib = L
+    return _probe_lib
 
 
 def error_string(code: int) -> str:
@@ -162,14 +177,14 @@ def lmhead_partials(problem: Problem, inputs: Inputs, sampled: bool, workspace,
 
 def probe_stream_read(buf, nbytes: int, sink, stream=None) -> None:
     """Enqueue one streaming read of `nbytes` at `buf` (include/dcd_probe.h)."""
-    _check(lib().dcd_probe_stream_read(ptr(buf), int(nbytes), ptr(sink), _stream(stream)))
+    _check(probe_lib().dcd_probe_stream_read(ptr(buf), int(nbytes), ptr(sink), _stream(stream)))
 
 
 def probe_mfma_bf16(workgroups: int, iters: int, sink, stream=None) -> float:
     """Enqueue the bf16 MFMA loop; returns the flops one launch performs."""
     flops = ctypes.c_double(0.0)
-    _check(lib().dcd_probe_mfma_bf16(int(workgroups), int(iters), ptr(sink), ctypes.byref(flops),
-                                      _stream(stream)))
+    _check(probe_lib().dcd_probe_mfma_bf16(int(workgroups), int(iters), ptr(sink),
+                                            ctypes.byref(flops), _stream(stream)))
     return flops.value
 
 

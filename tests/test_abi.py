@@ -13,21 +13,32 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADERS = sorted(glob.glob(os.path.join(ROOT, "include", "*.h")))
 
 
-def _declared_functions():
+def _declared_functions(header=None):
     names = set()
     for h in HEADERS:
+        if header and os.path.basename(h) != header:
+            continue
         text = re.sub(r"/\*.*?\*/", "", open(h).read(), flags=re.S)
         names |= set(re.findall(r"\b(dcd_[a-z_0-9]+)\s*\(", text))
     return sorted(names)
 
 
 def test_library_exports_every_declared_function():
-    names = _declared_functions()
+    """libdcd.so exports dcd.h; the benchmark's probes (dcd_probe.h) live in
+    libdcd_probe.so and nowhere in the product library."""
+    assert [os.path.basename(h) for h in HEADERS] == ["dcd.h", "dcd_probe.h"]
+    names = _declared_functions("dcd.h")
     assert set(names) == set(dcd.EXPORTS)
     L = dcd.lib()
     for n in names:
         assert hasattr(L, n), n
     assert L.dcd_abi_version() == 5
+    probes = _declared_functions("dcd_probe.h")
+    assert set(probes) == set(dcd.PROBE_EXPORTS)
+    PL = dcd.probe_lib()
+    for n in probes:
+        assert hasattr(PL, n), n
+        assert not hasattr(L, n), n
 
 
 def test_struct_layouts_match_the_header(tmp_path):
@@ -146,7 +157,7 @@ def test_binding_raises():
 
 def test_probe_host_validation():
     """The measurement probes reject invalid requests before any launch."""
-    L = dcd.lib()
+    L = dcd.probe_lib()
     buf = (ctypes.c_char * 64)()
     a = (ctypes.addressof(buf) + 15) // 16 * 16
     flops = ctypes.c_double(0.0)
