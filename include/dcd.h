@@ -29,7 +29,8 @@
  *  - Pointers named "device" are HIP device pointers (or host-coherent memory the
  *    GPU can read); the caller owns every buffer.  Matrices are row-major and
  *    densely packed.  The library allocates no memory and keeps no state between
- *    calls; calls on distinct streams with distinct workspaces may run concurrently.
+ *    calls (dcd_verify_greedy_noalloc's static per-GPU array aside); calls on
+ *    distinct streams with distinct workspaces may run concurrently.
  *  - Asynchrony: work is enqueued on `hip_stream` (a hipStream_t passed as void*,
  *    NULL = the default stream); calls return without synchronising.  Outputs are
  *    valid once the stream has reached the call.
@@ -62,7 +63,9 @@ enum {
     DCD_ERR_ALIGN = -4,       /* pointer or hidden-size alignment violated */
     DCD_ERR_WORKSPACE = -5,   /* workspace NULL, not 256-byte aligned, or smaller than dcd_workspace_bytes() */
     DCD_ERR_UNSUPPORTED = -6, /* valid request the library does not implement */
-    DCD_ERR_HIP = -7          /* the HIP runtime rejected a launch */
+    DCD_ERR_HIP = -7,         /* the HIP runtime rejected a launch */
+    DCD_ERR_TOO_LARGE = -8    /* dcd_verify_greedy_noalloc: the problem needs more than
+                                 dcd_noalloc_max_bytes() of device memory */
 };
 
 /* per-sequence status written to outputs.status[b] */
@@ -249,11 +252,36 @@ int dcd_propose(const dcd_problem *p, const dcd_inputs *in, const float *u, int3
 int dcd_lmhead_partials(const dcd_problem *p, const dcd_inputs *in, int sampled, void *workspace,
                         size_t workspace_bytes, void *hip_stream);
 
+/*
+ * dcd_verify_greedy without a workspace argument, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid allocation).  Same arguments, outputs and errors as dcd_verify_greedy,
+ * same kernels; the workspace is a static device array inside the library instead
+ * of the caller's memory.
+ *  - The call allocates nothing (no hipMalloc, hipFree or allocating library call).
+ *  - One array per GPU, of dcd_noalloc_max_bytes() bytes (80 MiB: 64 rows of a
+ *    128,256-token vocabulary in every mode), created when the library's code is
+ *    loaded on that GPU and held until the process ends.  A problem whose
+ *    dcd_workspace_bytes() exceeds it returns DCD_ERR_TOO_LARGE before anything
+ *    touches a device.
+ *  - The GPU is the one of hip_stream (of the current device for NULL); the first
+ *    call on a GPU looks up the array's device address (DCD_ERR_HIP if that fails).
+ *  - Every call on a GPU uses that GPU's one array and leaves its contents behind:
+ *    calls that overlap on one GPU (on different streams, or from several threads)
+ *    race and must be serialised by the caller.  Calls in stream order are safe.
+ */
+int dcd_verify_greedy_noalloc(const dcd_problem *p, const dcd_inputs *in, const dcd_outputs *out,
+                              void *hip_stream);
+
+/* bytes of device memory the allocation-free entry point holds per GPU */
+size_t dcd_noalloc_max_bytes(void);
+
 /* static description of a return code (never NULL) */
 const char *dcd_error_string(int code);
 
-/* ABI version of this header: 5 (2: dcd_outputs gained row_argmax_expert and row_kl;
-   3: dcd_verify_sample takes trees; 4: dcd_propose; 5: the final RMS normalisation) */
+/* ABI version of this header: 6 (2: dcd_outputs gained row_argmax_expert and row_kl;
+   3: dcd_verify_sample takes trees; 4: dcd_propose; 5: the final RMS normalisation;
+   6: dcd_verify_greedy_noalloc) */
 int dcd_abi_version(void);
 
 #ifdef __cplusplus

@@ -2,6 +2,8 @@
 // sequence (LM heads + partials -> per-row combine -> per-sequence verification).
 #include <math.h>
 
+#include <mutex>
+
 #include "../../include/dcd.h"
 #include "dcd_internal.h"
 
@@ -209,9 +211,72 @@ size_t workspace_layout(Plan &p, char *base) {
     return off;
 }
 
+// ---------------------------------------------------------------------------
+// The allocation-free entry point: the same launches as dcd_verify_greedy, with
+// the workspace taken from a static device array instead of the caller.
+//
+// One array per GPU the library runs on, held until the process ends.  Its size
+// covers 64 rows of a 128,256-token vocabulary in every mode (about 69 MB at
+// plaus_thresh 0, 67 MB with a mask); larger problems are refused.  Host code never
+// passes the array's name to a kernel (on the host it is only a handle of the
+// symbol): the device address comes from hipGetSymbolAddress, once per device,
+// with that device current.  The calls share each GPU's array, so calls that
+// overlap on one GPU race; nothing in it needs to start at zero (every call clears
+// the words it reads before writing them, exactly as with a caller's workspace).
+constexpr size_t kScratchBytes = (size_t)80 << 20;
+static __device__ __align__(256) char scratch[kScratchBytes];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+void *g_scratch[kMaxDevices];  // device address of `scratch` per device (null: not looked up)
+
+// Device address of this device's scratch array, looked up on the first call that
+// runs on it (with that device current).  Returns DCD_OK or DCD_ERR_HIP.
+int scratch_for(hipStream_t stream, void **out) {
+    int dev = -1;
+    hipError_t e = stream ? hipStreamGetDevice(stream, &dev) : hipGetDevice(&dev);
+    if (e != hipSuccess || dev < 0 || dev >= kMaxDevices) return DCD_ERR_HIP;
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    if (!g_scratch[dev]) {
+        int cur = -1;
+        if (hipGetDevice(&cur) != hipSuccess) return DCD_ERR_HIP;
+        if (cur != dev && hipSetDevice(dev) != hipSuccess) return DCD_ERR_HIP;
+        void *ptr = nullptr;
+        e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        if (cur != dev) hipSetDevice(cur);
+        if (e != hipSuccess || !ptr) return DCD_ERR_HIP;
+        g_scratch[dev] = ptr;
+    }
+    *out = g_scratch[dev];
+    return DCD_OK;
+}
+
+int run_greedy_noalloc(const dcd_problem *p, const dcd_inputs *in, const dcd_outputs *out,
+                       void *stream) {
+    // the size check needs no device: refuse before touching one
+    Plan P;
+    int rc = make_plan(p, false, P);
+    if (rc) return rc;
+    if (workspace_layout(P, nullptr) > kScratchBytes) return DCD_ERR_TOO_LARGE;
+    void *ws = nullptr;
+    if ((rc = scratch_for((hipStream_t)stream, &ws))) return rc;
+    return run(p, in, nullptr, out, ws, kScratchBytes, stream);
+}
+
+}  // namespace
+
 }  // namespace dcd
 
 extern "C" {
+
+int dcd_verify_greedy_noalloc(const dcd_problem *p, const dcd_inputs *in, const dcd_outputs *out,
+                              void *hip_stream) {
+    return dcd::run_greedy_noalloc(p, in, out, hip_stream);
+}
+
+size_t dcd_noalloc_max_bytes(void) { return dcd::kScratchBytes; }
 
 size_t dcd_workspace_bytes(const dcd_problem *p) {
     dcd::Plan P;
@@ -253,10 +318,12 @@ const char *dcd_error_string(int code) {
         case DCD_ERR_WORKSPACE: return "workspace missing, misaligned or too small";
         case DCD_ERR_UNSUPPORTED: return "request not supported by this build";
         case DCD_ERR_HIP: return "the HIP runtime rejected a launch";
+        case DCD_ERR_TOO_LARGE:
+            return "the problem needs more device memory than the allocation-free entry point holds";
         default: return "unknown error code";
     }
 }
 
-int dcd_abi_version(void) { return 5; }
+int dcd_abi_version(void) { return 6; }
 
 }  // extern "C"

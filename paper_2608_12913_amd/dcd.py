@@ -16,13 +16,15 @@ PROBE_LIB_PATH = os.path.join(PKG, "libdcd_probe.so")  # the benchmark's measure
 
 DCD_OK, DCD_ERR_NULL, DCD_ERR_SHAPE, DCD_ERR_PARAM = 0, -1, -2, -3
 DCD_ERR_ALIGN, DCD_ERR_WORKSPACE, DCD_ERR_UNSUPPORTED, DCD_ERR_HIP = -4, -5, -6, -7
+DCD_ERR_TOO_LARGE = -8
 SEQ_OK, SEQ_BAD_TREE, SEQ_BAD_TOKEN, SEQ_NONFINITE, SEQ_NOT_CHAIN = range(5)
 DCD_F32, DCD_BF16 = 0, 1
 ROW_MAX_P, ROW_LSE_P, ROW_LSE_Q, ROW_LOGZ, ROW_TOP1, ROW_MARGIN, ROW_COUNT, ROW_SIGNAL = range(8)
 NODE_LOGP_P, NODE_LOGP_Q, NODE_CD, NODE_LOGP_CD, NODE_IN_MASK, NODE_RATIO = range(6)
 
 EXPORTS = ("dcd_workspace_bytes", "dcd_verify_greedy", "dcd_verify_sample",
-           "dcd_lmhead_partials", "dcd_propose", "dcd_error_string", "dcd_abi_version")
+           "dcd_lmhead_partials", "dcd_propose", "dcd_error_string", "dcd_abi_version",
+           "dcd_verify_greedy_noalloc", "dcd_noalloc_max_bytes")
 PROBE_EXPORTS = ("dcd_probe_stream_read", "dcd_probe_mfma_bf16")  # include/dcd_probe.h
 
 
@@ -77,6 +79,11 @@ def lib() -> ctypes.CDLL:
         L.dcd_lmhead_partials.argtypes = [ctypes.POINTER(Problem), ctypes.POINTER(Inputs),
                                           ctypes.c_int, P, ctypes.c_size_t, P]
         L.dcd_lmhead_partials.restype = ctypes.c_int
+        L.dcd_verify_greedy_noalloc.argtypes = [ctypes.POINTER(Problem), ctypes.POINTER(Inputs),
+                                                ctypes.POINTER(Outputs), P]
+        L.dcd_verify_greedy_noalloc.restype = ctypes.c_int
+        L.dcd_noalloc_max_bytes.argtypes = []
+        L.dcd_noalloc_max_bytes.restype = ctypes.c_size_t
         L.dcd_error_string.argtypes = [ctypes.c_int]
         L.dcd_error_string.restype = ctypes.c_char_p
         L.dcd_abi_version.argtypes = []
@@ -156,6 +163,16 @@ def verify_greedy(problem: Problem, inputs: Inputs, outputs: Outputs, workspace,
                                  _stream(stream))
     if rc != DCD_OK:
         raise DcdError(rc)
+
+
+def verify_greedy_noalloc(problem: Problem, inputs: Inputs, outputs: Outputs, stream=None) -> None:
+    """dcd_verify_greedy on the library's static per-GPU workspace (no allocation)."""
+    _check(lib().dcd_verify_greedy_noalloc(ctypes.byref(problem), ctypes.byref(inputs),
+                                           ctypes.byref(outputs), _stream(stream)))
+
+
+def noalloc_max_bytes() -> int:
+    return int(lib().dcd_noalloc_max_bytes())
 
 
 def verify_sample(problem: Problem, inputs: Inputs, draft_probs, u_accept, u_resample,

@@ -32,7 +32,7 @@ def test_library_exports_every_declared_function():
     L = dcd.lib()
     for n in names:
         assert hasattr(L, n), n
-    assert L.dcd_abi_version() == 5
+    assert L.dcd_abi_version() == 6
     probes = _declared_functions("dcd_probe.h")
     assert set(probes) == set(dcd.PROBE_EXPORTS)
     PL = dcd.probe_lib()
@@ -67,7 +67,7 @@ def test_struct_layouts_match_the_header(tmp_path):
 
 
 def test_error_strings():
-    for code in range(0, -8, -1):
+    for code in range(0, -9, -1):
         assert dcd.error_string(code) and dcd.error_string(code) != "unknown error code"
     assert dcd.error_string(-99) == "unknown error code"
 
@@ -209,3 +209,21 @@ def test_final_norm_host_validation():
     assert _call_greedy(p1, dcd.Inputs(a, a, a, a, a, a, a, a, a, None), out, a, need) == dcd.DCD_ERR_NULL
     assert _call_greedy(p1, dcd.Inputs(a, a, a, a, a, a, a, a, a + 4, a), out, a, need) == dcd.DCD_ERR_ALIGN
     assert _call_greedy(p1, dcd.Inputs(a, a, a, a, a, a, a, a, a, a), out, a, need - 1) == dcd.DCD_ERR_WORKSPACE
+
+
+def test_noalloc_refuses_problems_beyond_its_array():
+    """dcd_verify_greedy_noalloc checks the problem's workspace size against its static
+    array before it touches a device (so this runs without a GPU)."""
+    cap = dcd.noalloc_max_bytes()
+    assert cap == 80 << 20
+    assert dcd.workspace_bytes(_problem()) <= cap  # the 64-row 8B/1B tree fits
+    assert dcd.workspace_bytes(_problem(plaus_thresh=0.0)) <= cap
+    big = _problem(batch=2)
+    assert dcd.workspace_bytes(big) > cap
+    ins, outs = dcd.Inputs(), dcd.Outputs()
+    with pytest.raises(dcd.DcdError) as e:
+        dcd.verify_greedy_noalloc(big, ins, outs)
+    assert e.value.code == dcd.DCD_ERR_TOO_LARGE
+    with pytest.raises(dcd.DcdError) as e:  # invalid problems first
+        dcd.verify_greedy_noalloc(_problem(vocab=0), ins, outs)
+    assert e.value.code == dcd.DCD_ERR_SHAPE
