@@ -187,7 +187,10 @@ size_t dcd_workspace_bytes(const dcd_problem *p);
  * when no child matches; next_token is the argmax of the last accepted node.
  * A draft token outside the mask is never accepted.
  * Workspace: device memory of at least dcd_workspace_bytes(p) bytes, 256-byte
- * aligned, not used by any concurrently running call.
+ * aligned, not used by any concurrently running call.  Its first 8 bytes hold a
+ * count of the calls made on it, which the library keeps from call to call (for
+ * every problem the workspace is large enough for); zero-fill a new workspace
+ * once.  The rest is scratch.
  */
 int dcd_verify_greedy(const dcd_problem *p, const dcd_inputs *in, const dcd_outputs *out,
                       void *workspace, size_t workspace_bytes, void *hip_stream);

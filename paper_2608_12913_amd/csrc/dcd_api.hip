@@ -128,7 +128,10 @@ int run(const dcd_problem *p, const dcd_inputs *in, const SampleInputs *smp,
     hipStream_t st = (hipStream_t)stream;
     if (normalise(P, I, st) != hipSuccess) return DCD_ERR_HIP;
     if (launch_lmhead(P, I, st) != hipSuccess) return DCD_ERR_HIP;
-    if (launch_finish(P, I, O, smp, st) != hipSuccess) return DCD_ERR_HIP;
+    if (launch_finish(P, I, O, smp, st) != hipSuccess) {
+        launch_advance_call(P, st);  // the next call must not see this call's ready word
+        return DCD_ERR_HIP;
+    }
     return DCD_OK;
 }
 
@@ -149,7 +152,8 @@ int run_lmhead(const dcd_problem *p, const dcd_inputs *in, int sampled, void *ws
     Inputs I{in->h_expert, in->h_amateur, in->w_expert, in->w_amateur, in->bias_expert,
              in->bias_amateur, in->parents, in->tokens, in->norm_expert, in->norm_amateur};
     if (normalise(P, I, (hipStream_t)stream) != hipSuccess) return DCD_ERR_HIP;
-    return launch_lmhead(P, I, (hipStream_t)stream) == hipSuccess ? DCD_OK : DCD_ERR_HIP;
+    if (launch_lmhead(P, I, (hipStream_t)stream) != hipSuccess) return DCD_ERR_HIP;
+    return launch_advance_call(P, (hipStream_t)stream) == hipSuccess ? DCD_OK : DCD_ERR_HIP;
 }
 
 int run_propose(const dcd_problem *p, const dcd_inputs *in, const ProposeOutputs &o, void *ws,
@@ -174,7 +178,10 @@ int run_propose(const dcd_problem *p, const dcd_inputs *in, const ProposeOutputs
     hipStream_t st = (hipStream_t)stream;
     if (normalise(P, I, st) != hipSuccess) return DCD_ERR_HIP;
     if (launch_lmhead(P, I, st) != hipSuccess) return DCD_ERR_HIP;
-    if (launch_propose(P, I, o, st) != hipSuccess) return DCD_ERR_HIP;
+    if (launch_propose(P, I, o, st) != hipSuccess) {
+        launch_advance_call(P, st);
+        return DCD_ERR_HIP;
+    }
     return DCD_OK;
 }
 
@@ -188,6 +195,8 @@ size_t workspace_layout(Plan &p, char *base) {
         return ptr;
     };
     const size_t R = (size_t)p.R;
+    // first, at the same place for every problem: the call count and ready word
+    p.ctl = (uint32_t *)take(2 * sizeof(uint32_t));
     p.partials = (float4 *)take(R * p.ntiles * sizeof(float4));
     if (p.full) {  // dense logits of both models, per-tile statistics of y
         p.zp_full = (float *)take(R * (size_t)p.zstride * sizeof(float));
@@ -200,7 +209,7 @@ size_t workspace_layout(Plan &p, char *base) {
     }
     p.rowinfo = (float *)take(R * kRowInfo * sizeof(float));
     p.tcount = (int *)take(R * p.ntiles * sizeof(int));
-    p.bound = (int *)take((size_t)kBoundCopies * R * sizeof(int));
+    p.bound = (uint32_t *)take((size_t)kBoundCopies * R * sizeof(uint32_t));
     p.nodez = (float4 *)take(R * sizeof(float4));
     p.seqdone = (int *)take((size_t)p.B * sizeof(int));
     if (p.final_norm) {
@@ -221,8 +230,9 @@ size_t workspace_layout(Plan &p, char *base) {
 // passes the array's name to a kernel (on the host it is only a handle of the
 // symbol): the device address comes from hipGetSymbolAddress, once per device,
 // with that device current.  The calls share each GPU's array, so calls that
-// overlap on one GPU race; nothing in it needs to start at zero (every call clears
-// the words it reads before writing them, exactly as with a caller's workspace).
+// overlap on one GPU race.  Like a caller's workspace, it starts with the call
+// count and ready word of the LM-head launch's clearing step (zero at load); every
+// other word a call reads it has written or cleared first.
 constexpr size_t kScratchBytes = (size_t)80 << 20;
 static __device__ __align__(256) char scratch[kScratchBytes];
 

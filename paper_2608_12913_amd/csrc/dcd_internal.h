@@ -58,9 +58,10 @@ struct Plan {
                        //   (max y, sum exp(y - max y), second-best y, sum exp(z_p - max_p)(z_p - z_q))
                        //   (argmax bits, z_p and z_q at the argmax, bits of the lowest
                        //    token whose z_p is the tile's expert max)
+    uint32_t *ctl;     // [2] at the workspace's start: the call counter and the ready word (below)
     float *rowinfo;    // [R][kRowInfo]
     int *tcount;       // [R][ntiles]   candidates per (row, tile); bitmap words valid where > 0
-    int *bound;        // [kBoundCopies][R] running lower bound on max z_p (order-preserving int key)
+    uint32_t *bound;   // [kBoundCopies][R] running lower bound on max z_p (bound_key; 0: none)
     float4 *nodez;     // [R]           node r's token under its parent row: (z_p, z_q) as a candidate
                        //   (NaN: not one), (z_p, z_q) by dot product (NaN: not computed)
     int *seqdone;      // [B]           rows of each sequence finished by the combine step
@@ -85,13 +86,15 @@ struct SampleInputs {
     const float *draft_probs, *u_acc, *u_res;
 };
 
-// float <-> int keys whose signed-integer order is the float order (for atomicMax)
-__device__ __forceinline__ int ordered_key(float f) {
-    const int i = __float_as_int(f);
-    return i >= 0 ? i : i ^ 0x7fffffff;
+// float -> unsigned keys whose order is the float order, every key above 0 (so an
+// all-zero word is an empty bound, below every float; for atomicMax)
+__device__ __forceinline__ uint32_t bound_key(float f) {
+    const uint32_t u = __float_as_uint(f);
+    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);  // -inf -> 0x007fffff > 0
 }
-__device__ __forceinline__ float key_value(int k) {
-    return __int_as_float(k >= 0 ? k : k ^ 0x7fffffff);
+__device__ __forceinline__ float bound_value(uint32_t k) {
+    if (k == 0u) return -INFINITY;
+    return __uint_as_float((k & 0x80000000u) ? (k & 0x7fffffffu) : ~k);
 }
 
 // The streaming LM-head kernel keeps the running row bounds in one copy per XCD (a
@@ -102,16 +105,55 @@ __device__ __forceinline__ float key_value(int k) {
 // epilogues are spread out, uses copy 0 alone.
 constexpr int kBoundCopies = 8;
 
-__device__ __forceinline__ void raise_bound(int *bound, int R, int row, float v) {
-    atomicMax(&bound[(int)(blockIdx.x % kBoundCopies) * R + row], ordered_key(v));
+__device__ __forceinline__ void raise_bound(uint32_t *bound, int R, int row, float v) {
+    atomicMax(&bound[(int)(blockIdx.x % kBoundCopies) * R + row], bound_key(v));
 }
 
-__device__ __forceinline__ float read_bound(const int *bound, int R, int row) {
-    int k = __atomic_load_n(&bound[row], __ATOMIC_RELAXED);
+__device__ __forceinline__ float read_bound(const uint32_t *bound, int R, int row) {
+    uint32_t k = __atomic_load_n(&bound[row], __ATOMIC_RELAXED);
 #pragma unroll
     for (int c = 1; c < kBoundCopies; ++c) k = max(k, __atomic_load_n(&bound[c * R + row], __ATOMIC_RELAXED));
-    return key_value(k);
+    return bound_value(k);
 }
+
+// Per-call clearing of the bounds and the per-sequence row counters, inside the
+// LM-head launch.  The workspace starts with two words: ctl[0] counts the calls
+// made on it and ctl[1] is the ready word.  Workgroup 0 of the LM-head kernel
+// clears the bounds and counters, then stores ready = count + 1 (release); every
+// other workgroup waits for that value (acquire) before it touches a bound, which
+// it first does at its expert epilogue, long after.  The last kernel of the call
+// advances the count (advance_call), so the next call waits for a new value.
+// The wait is bounded: a workgroup that gives up prunes nothing and raises no
+// bound (its candidates are then a larger superset of the mask, still exact).
+__device__ __forceinline__ void clear_call_state(const uint32_t *ctl, uint32_t *bound, int nbound,
+                                                 int *seqdone, int B) {
+    const uint32_t count = ctl[0];
+    for (int i = threadIdx.x; i < nbound; i += blockDim.x) bound[i] = 0u;
+    for (int i = threadIdx.x; i < B; i += blockDim.x) seqdone[i] = 0;
+    __syncthreads();
+    if (threadIdx.x == 0)
+        __hip_atomic_store(const_cast<uint32_t *>(ctl) + 1, count + 1, __ATOMIC_RELEASE,
+                           __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Called by every thread of a workgroup (contains a barrier); true once the bounds
+// of this call are cleared, false if the wait gave up.
+__device__ __forceinline__ bool await_call_state(const uint32_t *ctl) {
+    __shared__ int ok;
+    if (threadIdx.x == 0) {
+        const uint32_t want = ctl[0] + 1;
+        int tries = 0;
+        while (__hip_atomic_load(ctl + 1, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) != want &&
+               ++tries < (1 << 16))
+            __builtin_amdgcn_s_sleep(8);
+        ok = tries < (1 << 16);
+    }
+    __syncthreads();
+    return ok != 0;
+}
+
+// The call's last kernel advances the call count (one thread of one workgroup).
+__device__ __forceinline__ void advance_call(uint32_t *ctl) { ctl[0] = ctl[0] + 1; }
 
 // Untruncated target: statistics of y = (1+s) z_p - s z_q over a set of tokens.
 // cd = y - (1+s) lse_p + s lse_q, so the argmax, margin and log-normaliser of the
@@ -143,8 +185,10 @@ size_t workspace_layout(Plan &p, char *base);  // fills the pointers when base !
 
 // final RMS normalisation of both models' rows into hn_p / hn_q (final_norm)
 hipError_t launch_rmsnorm(const Plan &p, const Inputs &in, hipStream_t st);
-// LM heads with softmax partials and candidates (clears bound and seqdone first)
+// LM heads with softmax partials and candidates (clears bound and seqdone itself)
 hipError_t launch_lmhead(const Plan &p, const Inputs &in, hipStream_t st);
+// advances the workspace's call count (after an LM-head launch no other kernel follows)
+hipError_t launch_advance_call(const Plan &p, hipStream_t st);
 // the many-row variant (bf16, masked target, R >= kWideMinRows): same outputs
 bool use_wide_lmhead(const Plan &p);
 hipError_t launch_lmhead_wide(const Plan &p, const Inputs &in, hipStream_t st);

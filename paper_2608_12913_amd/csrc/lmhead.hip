@@ -416,6 +416,7 @@ __device__ __forceinline__ void tile_body(const Plan &P, const Inputs &in, int t
     float z[VB][RB][4];
     float pmax[RB], psum[RB], qmax[RB], qsum[RB];
     uint32_t flags[RB];  // bit (vb*4 + j): tile-local candidate
+    bool pruning = false;  // the row bounds of this call are usable
     Batch b;
 
     // ---- expert head (the amateur stream starts before its epilogue)
@@ -440,6 +441,8 @@ __device__ __forceinline__ void tile_body(const Plan &P, const Inputs &in, int t
         // block waits in its LDS slot; most tiles are pruned at the end, and global
         // stores issued here would delay the amateur stream's first loads behind
         // them.  Further candidates of a row block (rare) are stored at once.
+        // The row bounds of this call are cleared by workgroup 0 (long done by now).
+        pruning = await_call_state(P.ctl);
         bool over = false;
 #pragma unroll
         for (int rb = 0; rb < RB; ++rb) {
@@ -461,7 +464,7 @@ __device__ __forceinline__ void tile_body(const Plan &P, const Inputs &in, int t
             stash[rb * kWaveSize + lane] = first;
             over |= (f & (f - 1)) != 0;
             // running lower bound on the row's expert max: one update per (row, tile)
-            if (wave == 0 && g == 0 && row < P.R) raise_bound(P.bound, P.R, row, pmax[rb]);
+            if (pruning && wave == 0 && g == 0 && row < P.R) raise_bound(P.bound, P.R, row, pmax[rb]);
         }
         if (__builtin_amdgcn_ballot_w64(over)) {  // wave-uniform: some lane has more than one
 #pragma unroll
@@ -574,7 +577,7 @@ __device__ __forceinline__ void tile_body(const Plan &P, const Inputs &in, int t
 #pragma unroll
         for (int rb = 0; rb < RB; ++rb) {
             const int row = min(row0 + rb * 16 + n, P.R - 1);
-            bnd[rb] = flags[rb] ? read_bound(P.bound, P.R, row) : 0.f;
+            bnd[rb] = flags[rb] && pruning ? read_bound(P.bound, P.R, row) : -INFINITY;
         }
         for (int i = tid; i < ROWS * kWordsPerTile; i += NT) twords[i] = 0;
         if (tid < ROWS) tcnt[tid] = 0;
@@ -638,6 +641,8 @@ __device__ __forceinline__ void tile_body(const Plan &P, const Inputs &in, int t
 template <int DT, bool FULL, bool STREAM>
 __global__ __launch_bounds__(NT, kMinBlocks) void lmhead_kernel(Plan P, Inputs in) {
     extern __shared__ __align__(16) char lds[];
+    // workgroup 0 clears this call's row bounds and sequence counters first
+    if (blockIdx.x == 0) clear_call_state(P.ctl, P.bound, kBoundCopies * P.R, P.seqdone, P.B);
     // workgroup -> (vocabulary tile, row block); the row blocks of one tile are
     // dispatched back to back on the same XCD (workgroup id modulo 8) so the
     // tile's weights are re-read from that XCD's L2
@@ -653,13 +658,9 @@ __global__ __launch_bounds__(NT, kMinBlocks) void lmhead_kernel(Plan P, Inputs i
 }
 
 #if DCD_STREAM_ROWS == 64
-// Row bounds start at -inf and the per-sequence row counters of the finishing
-// step at 0, for every call.
-__global__ void init_kernel(int *bound, int R, int *seqdone, int B) {
-    const int r = blockIdx.x * blockDim.x + threadIdx.x;
-    if (r < kBoundCopies * R) bound[r] = ordered_key(-INFINITY);
-    if (r < B) seqdone[r] = 0;
-}
+// The call count of a workspace advanced after an LM-head launch that no other
+// kernel of the library follows (dcd_lmhead_partials).
+__global__ void advance_call_kernel(uint32_t *ctl) { advance_call(ctl); }
 #endif
 
 template <int DT, bool FULL, bool STREAM>
@@ -692,11 +693,13 @@ hipError_t launch_skinny(const Plan &p, const Inputs &in, hipStream_t st) {
 hipError_t launch_lmhead_rows64(const Plan &p, const Inputs &in, hipStream_t st) { return launch_skinny(p, in, st); }
 
 hipError_t launch_lmhead(const Plan &p, const Inputs &in, hipStream_t st) {
-    const int ninit = kBoundCopies * p.R > p.B ? kBoundCopies * p.R : p.B;
-    hipLaunchKernelGGL(init_kernel, dim3((ninit + 255) / 256), dim3(256), 0, st, p.bound, p.R, p.seqdone,
-                       p.B);
     if (use_wide_lmhead(p)) return launch_lmhead_wide(p, in, st);
     return p.rows_blk == kStreamRowsLarge ? launch_lmhead_rows128(p, in, st) : launch_lmhead_rows64(p, in, st);
+}
+
+hipError_t launch_advance_call(const Plan &p, hipStream_t st) {
+    hipLaunchKernelGGL(advance_call_kernel, dim3(1), dim3(1), 0, st, p.ctl);
+    return hipGetLastError();
 }
 #else
 hipError_t launch_lmhead_rows128(const Plan &p, const Inputs &in, hipStream_t st) { return launch_skinny(p, in, st); }

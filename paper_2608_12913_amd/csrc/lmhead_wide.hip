@@ -352,6 +352,8 @@ __device__ __forceinline__ void wide_tile(const Plan &P, const Inputs &in, int t
     sq.prefetch(1, sink);
     const float *bias = bias_p + wt * WT;  // this wave's half of the tile (then bias_q's)
     tile_softmax<RAGGED>(acc, bias, P.inv_T, tok0, P.V, wt, wr, pairs, pmax, psum);
+    // the row bounds of this call are cleared by workgroup 0 (long done by now)
+    const bool pruning = await_call_state(P.ctl);
     // tile-local candidates; the lane's first of each row block waits in its LDS
     // slot, further ones (rare) are stored now from the row block's logit buffer
 #pragma unroll
@@ -386,7 +388,7 @@ __device__ __forceinline__ void wide_tile(const Plan &P, const Inputs &in, int t
                     zbuf[bit * kWaveSize + lane];
             }
         }
-        if (wt == 0 && g == 0 && row < P.R) atomicMax(&P.bound[row], ordered_key(pmax[rb]));
+        if (pruning && wt == 0 && g == 0 && row < P.R) atomicMax(&P.bound[row], bound_key(pmax[rb]));
     }
 
     // ---- amateur head (chunks from stage 1, 0, 1, ...: its second chunk loads into
@@ -396,7 +398,8 @@ __device__ __forceinline__ void wide_tile(const Plan &P, const Inputs &in, int t
 #pragma unroll
     for (int rb = 0; rb < BR; ++rb) {
         const int row = min(row0 + wr * WR + rb * 16 + n, P.R - 1);
-        bnd[rb] = flags[rb] ? key_value(__atomic_load_n(&P.bound[row], __ATOMIC_RELAXED)) : 0.f;
+        bnd[rb] = flags[rb] && pruning ? bound_value(__atomic_load_n(&P.bound[row], __ATOMIC_RELAXED))
+                                       : -INFINITY;
     }
     bias = bias_q + wt * WT;
     for (int i = tid; i < TR * kWordsPerTile; i += NT) twords[i] = 0;
@@ -454,6 +457,8 @@ __global__ __launch_bounds__(NT, 1) void lmhead_wide_kernel(Plan P, Inputs in) {
     __shared__ __align__(16) char stage1[kStageBytes];
     __shared__ __align__(16) float misc[kMiscFloats];
     __shared__ __align__(16) char sink[4 * 512];  // L2 prefetches land here, unread
+    // workgroup 0 clears this call's row bounds and sequence counters first
+    if (blockIdx.x == 0) clear_call_state(P.ctl, P.bound, kBoundCopies * P.R, P.seqdone, P.B);
     // workgroup -> (vocabulary tile, row tile); the row tiles of one vocabulary tile
     // are dispatched back to back on the same XCD (workgroup id modulo 8), so the
     // tile's weights are read from HBM once and from that XCD's L2 otherwise

@@ -135,7 +135,8 @@ __device__ float wave_dot(const void *h, const void *w, int d, int lane) {
     float acc = 0.f;
     if constexpr (DT == kBF16) {
         const uint16_t *hr = (const uint16_t *)h, *wr = (const uint16_t *)w;
-#pragma unroll 4
+        // unrolled 8 times: a 4096-element row is one round of loads
+#pragma unroll 8
         for (int k = lane * 8; k < d; k += kWaveSize * 8) {
             const uint4 hv = *(const uint4 *)(hr + k), wv = *(const uint4 *)(wr + k);
             const uint32_t hs[4] = {hv.x, hv.y, hv.z, hv.w}, ws[4] = {wv.x, wv.y, wv.z, wv.w};
@@ -147,7 +148,7 @@ __device__ float wave_dot(const void *h, const void *w, int d, int lane) {
         }
     } else {
         const float *hr = (const float *)h, *wr = (const float *)w;
-#pragma unroll 4
+#pragma unroll 8
         for (int k = lane * 4; k < d; k += kWaveSize * 4) {
             const float4 hv = *(const float4 *)(hr + k), wv = *(const float4 *)(wr + k);
             acc += hv.x * wv.x + hv.y * wv.y + hv.z * wv.z + hv.w * wv.w;
@@ -189,6 +190,8 @@ __device__ __forceinline__ void emit_ids(const uint4 (&w)[kTileU4], int tile, in
 struct Smem {
     int list[kList];    // candidate ids (row phase: wave 0; draw: whole group)
     double wts[kList];  // draw weights
+    float4 nodez;       // the row's draft token under its parent row (waves 1-3)
+    int node_ok;        // nodez is to be written
     int wave_tot[NT / kWaveSize];
     int flag[4];
     int ints[4];
@@ -278,63 +281,64 @@ __device__ __forceinline__ void row_stats_full(const Plan &P, int row, int lane,
 }
 
 // ---------------------------------------------------------------------------
-// Row phase.  wave 0: the row's statistics; wave 1: the row as a draft node.
+// Row phase.  wave 0: the row's statistics; waves 1-3: the row as a draft node,
+// its token's logits under the parent row, left in sm.nodez (node_ok set) for the
+// thread that counts the row.
 template <int DT>
 __device__ __forceinline__ void combine_row(const Plan &P, const Inputs &in, const Outputs &out, int row, int lane,
-                            int wave, int *list) {
+                            int wave, Smem &sm) {
     const bool want_node_logits = out.node_stats != nullptr;
-    if (wave == 1) {
+    if (wave >= 1) {
         if (!in.parents) return;  // rows without a tree (proposals)
-        // this row's draft token under the parent row: from the parent's
-        // candidates when the token is one (the numbers the mask saw), otherwise
-        // (node statistics wanted) a dot product
         const int i = row % P.N;
         if (i == 0) return;
         const int j = in.parents[row], x = in.tokens[row];
         if (j < 0 || j >= i || x < 0 || x >= P.V) return;  // the sequence is rejected later
         const size_t rowj = (size_t)(row - i + j);
+        const size_t esz = DT == kBF16 ? 2 : 4;
+        // the three parts go to the three waves, so their loads are in flight together
         if (P.full) {  // every token is in the support; the expert logit is stored densely
-            const size_t esz = DT == kBF16 ? 2 : 4;
-            const float zp = P.zp_full[rowj * P.zstride + x];
-            float zq = 0.f;
-            if (P.store_q) {
-                zq = P.zq_full[rowj * P.zstride + x];
-            } else if (want_node_logits) {
-                zq = wave_dot<DT>((const char *)in.hq + rowj * P.dq * esz,
-                                  (const char *)in.wq + (size_t)x * P.dq * esz, P.dq, lane);
-                zq = (zq + (in.bq ? in.bq[x] : 0.f)) * P.inv_T;
+            if (wave == 1 && lane == 0) {
+                const float zp = P.zp_full[rowj * P.zstride + x];
+                sm.nodez.x = sm.nodez.z = zp;
+                if (P.store_q) sm.nodez.y = sm.nodez.w = P.zq_full[rowj * P.zstride + x];
+                else if (!want_node_logits) sm.nodez.y = sm.nodez.w = 0.f;
+                sm.node_ok = 1;
+            } else if (wave == 3 && !P.store_q && want_node_logits) {
+                float zq = wave_dot<DT>((const char *)in.hq + rowj * P.dq * esz,
+                                        (const char *)in.wq + (size_t)x * P.dq * esz, P.dq, lane);
+                if (lane == 0) sm.nodez.y = sm.nodez.w = (zq + (in.bq ? in.bq[x] : 0.f)) * P.inv_T;
             }
-            if (lane == 0) P.nodez[row] = float4{zp, zq, zp, zq};
-            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
             return;
         }
-        // count, bitmap word and candidate slot are fetched together.  The parent
-        // row's threshold is not known yet, so both forms are kept: the candidate's
-        // logits (NaN when the token is not a candidate of a kept tile) and, when
-        // node statistics are wanted, a dot product.  The sequence phase takes the
-        // candidate's only for a mask member, whose tile is never dropped, so the
-        // choice does not depend on which tiles the running bound pruned.
-        const int tcnt = P.tcount[rowj * P.ntiles + x / kTileTokens];
-        const uint32_t word = P.bits[rowj * P.wstride + (x >> 5)];
-        const float2 c = P.cand[rowj * P.V + x];
-        const bool cand = tcnt > 0 && (word >> (x & 31) & 1u);
-        float4 nz{cand ? c.x : NAN, cand ? c.y : NAN, NAN, NAN};
-        if (want_node_logits) {
-            const size_t esz = DT == kBF16 ? 2 : 4;
+        // The parent row's threshold is not known yet, so both forms are kept: the
+        // candidate's logits (NaN when the token is not a candidate of a kept tile)
+        // and, when node statistics are wanted, a dot product.  The sequence phase
+        // takes the candidate's only for a mask member, whose tile is never dropped,
+        // so the choice does not depend on which tiles the running bound pruned.
+        if (wave == 1) {
+            if (lane == 0) {  // count, bitmap word and candidate slot fetched together
+                const int tcnt = P.tcount[rowj * P.ntiles + x / kTileTokens];
+                const uint32_t word = P.bits[rowj * P.wstride + (x >> 5)];
+                const float2 c = P.cand[rowj * P.V + x];
+                const bool cand = tcnt > 0 && (word >> (x & 31) & 1u);
+                sm.nodez.x = cand ? c.x : NAN;
+                sm.nodez.y = cand ? c.y : NAN;
+                if (!want_node_logits) sm.nodez.z = sm.nodez.w = NAN;
+                sm.node_ok = 1;
+            }
+        } else if (want_node_logits && wave == 2) {
             float zp = wave_dot<DT>((const char *)in.hp + rowj * P.dp * esz,
                                     (const char *)in.wp + (size_t)x * P.dp * esz, P.dp, lane);
+            if (lane == 0) sm.nodez.z = (zp + (in.bp ? in.bp[x] : 0.f)) * P.inv_T;
+        } else if (want_node_logits && wave == 3) {
             float zq = wave_dot<DT>((const char *)in.hq + rowj * P.dq * esz,
                                     (const char *)in.wq + (size_t)x * P.dq * esz, P.dq, lane);
-            nz.z = (zp + (in.bp ? in.bp[x] : 0.f)) * P.inv_T;
-            nz.w = (zq + (in.bq ? in.bq[x] : 0.f)) * P.inv_T;
+            if (lane == 0) sm.nodez.w = (zq + (in.bq ? in.bq[x] : 0.f)) * P.inv_T;
         }
-        if (lane == 0) P.nodez[row] = nz;
-        // publish nodez at device scope before the row is counted (wave 0's
-        // results are published by the counting atomic itself)
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
         return;
     }
-    if (wave != 0) return;
+    int *list = sm.list;
     if (P.full) {
         row_stats_full(P, row, lane, out);
         return;
@@ -1097,7 +1101,7 @@ __device__ __forceinline__ void verify_sequence(const Plan &P, const Inputs &in,
 }
 
 // One workgroup per row; the workgroup that finishes a sequence's last row
-// (counted in seqdone, cleared before the LM-head launch) runs the sequence phase.
+// (counted in seqdone, cleared by the LM-head launch) runs the sequence phase.
 template <int DT, bool SAMPLE>
 __global__ __launch_bounds__(NT) void finish_kernel(Plan P, Inputs in, Outputs out,
                                                     SampleInputs smp) {
@@ -1105,14 +1109,20 @@ __global__ __launch_bounds__(NT) void finish_kernel(Plan P, Inputs in, Outputs o
     __shared__ int last;
     extern __shared__ __align__(16) int dyn[];
     const int row = blockIdx.x, tid = threadIdx.x;
-    combine_row<DT>(P, in, out, row, tid % kWaveSize, tid / kWaveSize, sm.list);
-    // count the row once both of its waves are done; the release half of the
-    // atomic publishes wave 0's results, wave 1 released its own
+    if (row == 0 && tid == 0) advance_call(P.ctl);  // the call's last kernel
+    if (tid == 0) sm.node_ok = 0;
+    __syncthreads();
+    combine_row<DT>(P, in, out, row, tid % kWaveSize, tid / kWaveSize, sm);
+    // count the row once all of its waves are done; thread 0 stores the node's
+    // logits, and the release half of the counting atomic publishes them together
+    // with wave 0's results (the workgroup barrier orders those before it)
     __syncthreads();
     const int b = row / P.N;
-    if (tid == 0)
+    if (tid == 0) {
+        if (sm.node_ok) P.nodez[row] = sm.nodez;
         last = __hip_atomic_fetch_add(&P.seqdone[b], 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT) ==
                P.N - 1;
+    }
     __syncthreads();
     if (!last) return;
     // acquire: the other rows of the sequence are visible from here on
@@ -1128,9 +1138,10 @@ template <int DT>
 __global__ __launch_bounds__(NT) void propose_kernel(Plan P, Inputs in, ProposeOutputs po) {
     __shared__ Smem sm;
     const int row = blockIdx.x, tid = threadIdx.x;
+    if (row == 0 && tid == 0) advance_call(P.ctl);  // the last kernel using the call state
     Outputs out{};
     out.row_argmax = po.argmax;
-    combine_row<DT>(P, in, out, row, tid % kWaveSize, tid / kWaveSize, sm.list);
+    combine_row<DT>(P, in, out, row, tid % kWaveSize, tid / kWaveSize, sm);
     __syncthreads();  // the row's statistics are visible to the whole group
     const Residual target{nullptr, nullptr, nullptr, 0, nullptr, P.V};
     if (po.tokens) {

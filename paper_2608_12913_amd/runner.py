@@ -57,7 +57,8 @@ class DeviceProblem:
         self.ws_bytes = dcd.workspace_bytes(self.problem)
         if self.ws_bytes == 0:
             raise dcd.DcdError(dcd.DCD_ERR_SHAPE)
-        self.workspace = torch.empty(self.ws_bytes, dtype=torch.uint8, device=self.device)
+        # zero-filled once: its first words are the call count the library keeps
+        self.workspace = torch.zeros(self.ws_bytes, dtype=torch.uint8, device=self.device)
         self.inputs = dcd.make_inputs(self.hp, self.hq, self.wp, self.wq, self.bias_p, self.bias_q,
                                       self.parents, self.tokens, self.norm_p, self.norm_q)
         self.outputs = dcd.make_outputs(self.accept_len, self.accept_path, self.next_token,

@@ -244,6 +244,36 @@ def test_repeated_calls_are_bit_identical():
         assert np.array_equal(a[k].view(np.uint8), b[k].view(np.uint8)), k
 
 
+def test_workspace_reused_across_problems():
+    """One workspace, filled with garbage, serves problems of different shapes in
+    turn, some of them only through dcd_lmhead_partials.  The LM-head launch clears
+    the row bounds of each call itself: a problem whose logits are four times
+    smaller than the previous one's (so stale bounds would drop every tile holding
+    its mask members) must come out bit for bit as on a fresh workspace."""
+    from paper_2608_12913_amd import dcd
+    big = synth.make_case("b8_tree64", 80, N=40, depth=5, max_children=6, V=6000, dp=256, dq=128)
+    small = synth.make_case("b8_tree64", 81, B=3, N=24, depth=4, max_children=4, V=6000, dp=256,
+                            dq=128, h_scale=1.0)
+    runs = []
+    for case in (big, small):
+        dp = _runner().from_case(case, _greedy_tokens(case))
+        runs.append((dp, dp.run("greedy")))
+    need = max(dp.ws_bytes for dp, _ in runs)
+    shared = torch.full((need,), 0xAB, dtype=torch.uint8, device="cuda:0")
+    stream = torch.cuda.current_stream()
+    for step, k in enumerate((0, 1, 1, 0, 1)):
+        dp, ref = runs[k]
+        other = runs[1 - k][0]
+        # the other problem's LM heads alone on the same workspace first
+        dcd.lmhead_partials(other.problem, other.inputs, False, shared, need, stream)
+        dcd.verify_greedy(dp.problem, dp.inputs, dp.outputs, shared, need, stream)
+        torch.cuda.synchronize()
+        got = {k2: getattr(dp, k2).cpu().numpy() for k2 in ref}
+        for k2 in ref:
+            assert np.array_equal(ref[k2].view(np.uint8), got[k2].view(np.uint8)), (step, k2)
+    _say("workspace reuse: ok")
+
+
 # ------------------------------------------------------------------ sampled
 def _sampled_setup(case):
     rows = oracle.eval_rows(case.hp, case.hq, case.wp, case.wq, case.bias, case.bias,
