@@ -74,7 +74,9 @@ enum {
     DCD_SEQ_BAD_TREE = 1,   /* parents[b,0] != -1 or parents[b,i] outside [0, i) */
     DCD_SEQ_BAD_TOKEN = 2,  /* a draft token (i >= 1) outside [0, vocab) */
     DCD_SEQ_NONFINITE = 3,  /* a row of the sequence has a non-finite max, log-normaliser or log Z */
-    DCD_SEQ_NOT_CHAIN = 4   /* not produced since ABI 3 (sampled verification takes trees) */
+    DCD_SEQ_NOT_CHAIN = 4,  /* not produced since ABI 3 (sampled verification takes trees) */
+    DCD_SEQ_WALK_TIMEOUT = 5 /* sampled, plaus_thresh = 0: the workgroups sharing the sequence's
+                                walk did not meet in time (a device fault; outputs undefined) */
 };
 
 /* element type of hidden states and LM-head weights (bias is always fp32) */
@@ -217,6 +219,10 @@ int dcd_verify_greedy(const dcd_problem *p, const dcd_inputs *in, const dcd_outp
  * in token-id order: the smallest token whose cumulative weight exceeds
  * u_resample times the total.  node_stats[DCD_NODE_RATIO] is pi_CD / pi_e of the
  * node's token under its parent row (the ratio of a first sibling).
+ * With plaus_thresh = 0 and at most 64 sequences, each sequence's walk is spread
+ * over several workgroups of one cooperative kernel launch on hip_stream (so such a
+ * call is not for stream capture); a sequence whose workgroups failed to meet gets
+ * status DCD_SEQ_WALK_TIMEOUT.
  */
 int dcd_verify_sample(const dcd_problem *p, const dcd_inputs *in, const float *draft_probs,
                       const float *u_accept, const float *u_resample, const dcd_outputs *out,
@@ -282,9 +288,9 @@ size_t dcd_noalloc_max_bytes(void);
 /* static description of a return code (never NULL) */
 const char *dcd_error_string(int code);
 
-/* ABI version of this header: 6 (2: dcd_outputs gained row_argmax_expert and row_kl;
+/* ABI version of this header: 7 (2: dcd_outputs gained row_argmax_expert and row_kl;
    3: dcd_verify_sample takes trees; 4: dcd_propose; 5: the final RMS normalisation;
-   6: dcd_verify_greedy_noalloc) */
+   6: dcd_verify_greedy_noalloc; 7: sequence status DCD_SEQ_WALK_TIMEOUT) */
 int dcd_abi_version(void);
 
 #ifdef __cplusplus

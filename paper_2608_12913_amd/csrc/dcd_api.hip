@@ -126,12 +126,16 @@ int run(const dcd_problem *p, const dcd_inputs *in, const SampleInputs *smp,
                     out->row_argmax,        out->row_stats,   out->node_stats,
                     out->row_argmax_expert, out->row_kl};
     hipStream_t st = (hipStream_t)stream;
+    // untruncated sampled verification: each sequence's walk spread over a group of
+    // workgroups when they fit one cooperative launch
+    P.walk_group = smp && P.full ? walk_group_size(P) : 0;
     if (normalise(P, I, st) != hipSuccess) return DCD_ERR_HIP;
     if (launch_lmhead(P, I, st) != hipSuccess) return DCD_ERR_HIP;
     if (launch_finish(P, I, O, smp, st) != hipSuccess) {
         launch_advance_call(P, st);  // the next call must not see this call's ready word
         return DCD_ERR_HIP;
     }
+    if (P.walk_group && launch_walk(P, I, O, *smp, st) != hipSuccess) return DCD_ERR_HIP;
     return DCD_OK;
 }
 
@@ -203,6 +207,8 @@ size_t workspace_layout(Plan &p, char *base) {
         p.zq_full = (float *)take(R * (size_t)p.zstride * sizeof(float));
         p.ypart = (float4 *)take(R * p.ntiles * 2 * sizeof(float4));
         p.resbuf = (double *)take((size_t)p.B * 2 * p.zstride * sizeof(double));
+        p.walkbar = (int *)take((size_t)p.B * 2 * sizeof(int));
+        p.walkpart = (double *)take((size_t)p.B * 2 * kWalkMaxGroup * sizeof(double));
     } else {  // candidates of the mask
         p.cand = (float2 *)take(R * (size_t)p.V * sizeof(float2));
         p.bits = (uint32_t *)take(R * (size_t)p.wstride * sizeof(uint32_t));
@@ -334,6 +340,6 @@ const char *dcd_error_string(int code) {
     }
 }
 
-int dcd_abi_version(void) { return 6; }
+int dcd_abi_version(void) { return 7; }
 
 }  // extern "C"

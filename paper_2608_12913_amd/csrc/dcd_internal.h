@@ -19,6 +19,7 @@ constexpr int kRowInfo = 16;                         // floats of per-row result
 constexpr int kMaxNodes = 4096;                      // nodes per sequence (staged in LDS)
 constexpr int kWideRows = 256;                       // rows per workgroup of the many-row LM-head kernel
 constexpr int kWideMinRows = 512;                    // rows from which that kernel is used
+constexpr int kWalkMaxGroup = 64;                    // workgroups per sequence of the spread walk
 
 // rowinfo slots (floats; the argmax is stored as an int bit pattern)
 enum {
@@ -65,6 +66,11 @@ struct Plan {
     float4 *nodez;     // [R]           node r's token under its parent row: (z_p, z_q) as a candidate
                        //   (NaN: not one), (z_p, z_q) by dot product (NaN: not computed)
     int *seqdone;      // [B]           rows of each sequence finished by the combine step
+    // untruncated sampled verification with the walk spread over a group of
+    // workgroups per sequence (walk_kernel; walk_group = 0: the finish kernel walks)
+    int walk_group;    // workgroups per sequence
+    int *walkbar;      // [B][2] barrier arrivals of each group, and a failed-wait flag
+    double *walkpart;  // [B][2][kWalkMaxGroup] the group's slice sums of a pass (two passes kept)
     void *hn_p, *hn_q; // [R][d_p], [R][d_q] final_norm: the normalised hidden states
 };
 
@@ -143,10 +149,13 @@ __device__ __forceinline__ bool await_call_state(const uint32_t *ctl) {
     if (threadIdx.x == 0) {
         const uint32_t want = ctl[0] + 1;
         int tries = 0;
-        while (__hip_atomic_load(ctl + 1, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) != want &&
+        while (__hip_atomic_load(ctl + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != want &&
                ++tries < (1 << 16))
             __builtin_amdgcn_s_sleep(8);
         ok = tries < (1 << 16);
+        // after the poll, once for the workgroup (it invalidates the CU's and the
+        // XCD's caches, which all of its waves share)
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
     }
     __syncthreads();
     return ok != 0;
@@ -206,5 +215,10 @@ hipError_t launch_propose(const Plan &p, const Inputs &in, const ProposeOutputs 
 // per-row combination and per-sequence verification (greedy when smp is null)
 hipError_t launch_finish(const Plan &p, const Inputs &in, const Outputs &out,
                          const SampleInputs *smp, hipStream_t st);
+// untruncated sampled verification: workgroups per sequence for the spread walk
+// (0 when the sequences do not fit a cooperative launch), and that launch
+int walk_group_size(const Plan &p);
+hipError_t launch_walk(const Plan &p, const Inputs &in, const Outputs &out, const SampleInputs &smp,
+                       hipStream_t st);
 
 }  // namespace dcd

@@ -18,6 +18,7 @@
 // phase takes only the tiles whose own expert max reaches the row's threshold
 // (those are never dropped, and hold every mask member), and a draft token's
 // logits come from the candidates only when the token is a mask member.
+#include "dcd.h"
 #include "dcd_internal.h"
 
 namespace dcd {
@@ -1100,6 +1101,379 @@ __device__ __forceinline__ void verify_sequence(const Plan &P, const Inputs &in,
     }
 }
 
+
+// ---------------------------------------------------------------------------
+// Untruncated target, sampled verification: each sequence's walk spread over a
+// group of G workgroups (one cooperative launch, every workgroup resident).
+//
+// With plaus_thresh = 0 every token is in the support, so a rejection needs the
+// normaliser Z of the residual max(0, p - pi_e) over the whole vocabulary, and the
+// final draw an inverse CDF over it: passes over V tokens that one workgroup can
+// only stream at latency-bound rates.  Here every workgroup of the group takes a
+// contiguous slice of the vocabulary (each thread a contiguous run of it), and all
+// of them follow the same walk: the decisions are taken from the same values by
+// thread 0 of each workgroup, and a pass's slice sums are exchanged through the
+// workspace with a group barrier in between (each workgroup adds them in slice
+// order, so all agree on the total).  The residual of the last applied rejection
+// is kept as a stored row (two rows of V doubles per sequence, as in the
+// single-workgroup walk), written slice by slice.  The draw finds the slice that
+// holds u times the total from the slice sums; that slice's workgroup finds the
+// token.  Each slice sum is the last entry of a fixed-order scan of its threads'
+// run sums, the same scan the draw walks, so the two agree.
+
+struct WalkShared {
+    double wave_tot[NT / kWaveSize];
+    double dval, dval2;
+    int ival[4];
+};
+
+// inclusive scan of one double per thread over the workgroup, in thread order;
+// *total = the last thread's value (every thread gets it)
+__device__ __forceinline__ double block_inclusive_scan(double x, int tid, double *total, WalkShared &ws) {
+    const int lane = tid % kWaveSize, wave = tid / kWaveSize;
+    double incl = x;
+#pragma unroll
+    for (int d = 1; d < kWaveSize; d <<= 1) {
+        const double y = __shfl_up(incl, d, kWaveSize);
+        if (lane >= d) incl += y;
+    }
+    if (lane == kWaveSize - 1) ws.wave_tot[wave] = incl;
+    __syncthreads();
+    double before = 0.0, all = 0.0;
+#pragma unroll
+    for (int w = 0; w < NT / kWaveSize; ++w) {
+        before += w < wave ? ws.wave_tot[w] : 0.0;
+        all += ws.wave_tot[w];
+    }
+    __syncthreads();
+    *total = all;
+    return before + incl;
+}
+
+// Arrival at the group's barrier number k (1, 2, ...): the workgroup's writes are
+// released at agent scope, then it waits (acquire) until all G workgroups arrived.
+// The wait is bounded; a workgroup that gives up sets the group's failure flag and
+// goes on, so every workgroup ends.
+// Every wave first waits for its own stores to complete (vmcnt(0)); thread 0 then
+// releases the workgroup's writes at agent scope with its arrival and, once all
+// have arrived, acquires at agent scope for the workgroup (the caches it
+// invalidates are the CU's and its XCD's, shared by all waves of the workgroup).
+// One agent-scope fence pair per workgroup and barrier: each is a cache writeback
+// or invalidate, far too costly to issue from every wave.
+__device__ __forceinline__ void group_barrier(int *bar, int G, int k, WalkShared &ws) {
+    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): this wave's stores have landed
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        __hip_atomic_fetch_add(bar, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+        // relaxed polling (an acquire per poll would invalidate the caches every
+        // time), one acquire fence once the count is reached
+        int tries = 0;
+        while (__hip_atomic_load(bar, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < G * k) {
+            if (++tries >= (1 << 22)) {
+                __hip_atomic_store(bar + 1, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                break;
+            }
+            __builtin_amdgcn_s_sleep(1);
+        }
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    }
+    __syncthreads();
+}
+
+template <int DT>
+__global__ __launch_bounds__(NT) void walk_kernel(Plan P, Inputs in, Outputs out, SampleInputs smp) {
+    __shared__ WalkShared ws;
+    extern __shared__ __align__(16) int dyn[];
+    const int G = P.walk_group;
+    const int b = blockIdx.x / G, m = blockIdx.x % G, tid = threadIdx.x;
+    const int N = P.N, V = P.V;
+    const size_t r0 = (size_t)b * N;
+    int *s_par = dyn, *s_tok = dyn + N;
+    float *s_p0 = reinterpret_cast<float *>(dyn + 2 * N), *s_qx = s_p0 + N;
+    int *bar = P.walkbar + 2 * b;
+    double *part = P.walkpart + (size_t)b * 2 * kWalkMaxGroup;
+    const bool lead = m == 0;  // writes the sequence's outputs
+
+    // the sequence's tree, tokens and row checks (every workgroup the same)
+    if (tid < 4) ws.ival[tid] = 0;
+    __syncthreads();
+    for (int i = tid; i < N; i += NT) {
+        const int p = in.parents[r0 + i], x = in.tokens[r0 + i];
+        const RowInfo r = load_rowinfo(P.rowinfo, r0 + i);
+        s_par[i] = p;
+        s_tok[i] = x;
+        if (i == 0 ? p != -1 : (p < 0 || p >= i)) atomicOr(&ws.ival[0], 1);
+        if (i > 0 && (x < 0 || x >= V)) atomicOr(&ws.ival[1], 1);
+        if (!isfinite(r.a.x) || !isfinite(r.a.y) || !isfinite(r.a.z) || !isfinite(r.a.w))
+            atomicOr(&ws.ival[2], 1);
+    }
+    __syncthreads();
+    const int status = ws.ival[0] ? DCD_SEQ_BAD_TREE : ws.ival[1] ? DCD_SEQ_BAD_TOKEN
+                                                       : ws.ival[2] ? DCD_SEQ_NONFINITE : 0;
+    if (status != 0) {
+        if (!lead) return;
+        for (int i = tid; i < N; i += NT) {
+            out.accept_path[r0 + i] = -1;
+            if (out.node_stats)
+                for (int k = 0; k < 6; ++k) out.node_stats[(r0 + i) * 6 + k] = NAN;
+        }
+        if (tid == 0) {
+            out.status[b] = status;
+            out.accept_len[b] = 0;
+            out.next_token[b] = -1;
+        }
+        return;
+    }
+    // per node: the target probability of its token under the parent row and its
+    // proposal probability; the lead writes the node statistics
+    if (lead && out.node_stats && tid < 6) out.node_stats[r0 * 6 + tid] = NAN;
+    for (int i = 1 + tid; i < N; i += NT) {
+        const int x = s_tok[i];
+        const NodeStat n = node_stat(P.nodez[r0 + i], load_rowinfo(P.rowinfo, r0 + s_par[i]), P.s);
+        const float pe = smp.draft_probs[(r0 + i) * V + x];
+        const float p0 = n.in_mask ? __expf(n.lpcd) : 0.f;
+        s_p0[i] = p0;
+        s_qx[i] = pe;
+        if (lead && out.node_stats)
+            write_node_stats(out.node_stats + (r0 + i) * 6, n, pe > 0.f ? p0 / pe : INFINITY);
+    }
+    __syncthreads();
+
+    // this workgroup's slice of the vocabulary and this thread's run of it
+    const int S = ((V + G - 1) / G + 3) / 4 * 4;
+    const int v0 = min(V, m * S), v1 = min(V, v0 + S);
+    const int k = ((S + NT - 1) / NT + 3) / 4 * 4;
+    const int t0 = v0 + tid * k, t1 = min(v1, t0 + k);
+    double *const xrow0 = P.resbuf + (size_t)b * 2 * P.zstride, *const xrow1 = xrow0 + P.zstride;
+    const double *xcur = nullptr;  // the stored residual row (null: pi_CD of the row)
+    double xs = 0.0;               // its normaliser 1/Z
+    int cur = 0, len = 0, nbar = 0;
+    bool last_pass_applied = false;  // the slice sums of the last pass are the current weights
+    const float *rj = nullptr;
+    float lse_p = 0.f, lse_q = 0.f, logZ = 0.f;
+    const float *zp = nullptr, *zq = nullptr;
+    auto set_row = [&](int j) {
+        rj = P.rowinfo + (r0 + j) * kRowInfo;
+        lse_p = rj[RI_LSEP];
+        lse_q = rj[RI_LSEQ];
+        logZ = rj[RI_LOGZ];
+        zp = P.zp_full + (r0 + j) * P.zstride;
+        zq = P.zq_full + (r0 + j) * P.zstride;
+    };
+    set_row(0);
+    // weight of token t under the walk's current target
+    auto weight = [&](int t) -> double {
+        if (xcur) return xcur[t] * xs;
+        return (double)__expf((1.f + P.s) * (zp[t] - lse_p) - P.s * (zq[t] - lse_q) - logZ);
+    };
+    // one pass over this thread's run: with q, the residual max(0, w - q) is stored
+    // to xout; returns the run's sum in token order.  Whole chunks of 8 tokens (the
+    // run starts at a multiple of 4) issue all their loads before any weight is
+    // formed: 16-byte loads of the dense or stored rows, and of the proposal row
+    // where it is 16-byte aligned.
+    auto run_sum = [&](const float *q, double *xout) -> double {
+        double sum = 0.0;
+        const bool q4 = q && (reinterpret_cast<uintptr_t>(q) & 15) == 0;
+        int t = t0;
+        for (; t + 8 <= t1; t += 8) {
+            double xv[8];
+            float pz[8], qz[8], pr[8];
+            if (xcur) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const double2 a = *reinterpret_cast<const double2 *>(xcur + t + 2 * i);
+                    xv[2 * i] = a.x;
+                    xv[2 * i + 1] = a.y;
+                }
+            } else {
+#pragma unroll
+                for (int i = 0; i < 2; ++i) {
+                    const float4 a = *reinterpret_cast<const float4 *>(zp + t + 4 * i);
+                    const float4 c = *reinterpret_cast<const float4 *>(zq + t + 4 * i);
+                    pz[4 * i] = a.x, pz[4 * i + 1] = a.y, pz[4 * i + 2] = a.z, pz[4 * i + 3] = a.w;
+                    qz[4 * i] = c.x, qz[4 * i + 1] = c.y, qz[4 * i + 2] = c.z, qz[4 * i + 3] = c.w;
+                }
+            }
+            if (q4) {
+#pragma unroll
+                for (int i = 0; i < 2; ++i) {
+                    const float4 a = *reinterpret_cast<const float4 *>(q + t + 4 * i);
+                    pr[4 * i] = a.x, pr[4 * i + 1] = a.y, pr[4 * i + 2] = a.z, pr[4 * i + 3] = a.w;
+                }
+            } else if (q) {
+#pragma unroll
+                for (int i = 0; i < 8; ++i) pr[i] = q[t + i];
+            }
+            double w[8];
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                const double cur = xcur ? xv[i] * xs
+                                        : (double)__expf((1.f + P.s) * (pz[i] - lse_p) -
+                                                         P.s * (qz[i] - lse_q) - logZ);
+                w[i] = q ? fmax(0.0, cur - (double)pr[i]) : cur;
+            }
+            if (q) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    *reinterpret_cast<double2 *>(xout + t + 2 * i) = double2{w[2 * i], w[2 * i + 1]};
+            }
+#pragma unroll
+            for (int i = 0; i < 8; ++i) sum += w[i];
+        }
+        for (; t < t1; ++t) {  // the run's last, partial chunk
+            double w = weight(t);
+            if (q) {
+                w = fmax(0.0, w - (double)q[t]);
+                xout[t] = w;
+            }
+            sum += w;
+        }
+        return sum;
+    };
+    // The group's slice sums as wave 0 sees them: lane g loads slice g's sum (all
+    // in one round) and a fixed-order inclusive scan over the lanes gives each the
+    // running sum up to its slice, so every workgroup computes the same numbers.
+    auto slice_scan = [&](const double *src, double *mine, double *incl) {
+        const int lane = tid % kWaveSize;
+        const double v = lane < G ? src[lane] : 0.0;
+        double x = v;
+#pragma unroll
+        for (int d = 1; d < kWaveSize; d <<= 1) {
+            const double y = __shfl_up(x, d, kWaveSize);
+            if (lane >= d) x += y;
+        }
+        *mine = v;
+        *incl = x;
+    };
+    // slice sums of a pass exchanged through `part` (pass parity nbar % 2); returns
+    // the group total
+    auto exchange = [&](double slice_sum) -> double {
+        double *dst = part + (nbar % 2) * kWalkMaxGroup;
+        if (tid == 0) dst[m] = slice_sum;
+        group_barrier(bar, G, ++nbar, ws);
+        if (tid < kWaveSize) {
+            double mine, incl;
+            slice_scan(dst, &mine, &incl);
+            if (tid == kWaveSize - 1) ws.dval = incl;
+        }
+        __syncthreads();
+        const double tot = ws.dval;
+        __syncthreads();
+        return tot;
+    };
+
+    for (int c = 1; c < N; ++c) {
+        if (s_par[c] != cur) continue;
+        // Alg. 1's accept test, taken alike by every workgroup
+        if (tid == 0) {
+            const double w = xcur ? xcur[s_tok[c]] * xs : (double)s_p0[c];
+            const double ratio = s_qx[c] > 0.f ? w / (double)s_qx[c] : INFINITY;
+            ws.ival[3] = w > 0.0 && (double)smp.u_acc[r0 + c] <= ratio;
+        }
+        __syncthreads();
+        const bool accepted = ws.ival[3] != 0;
+        __syncthreads();
+        if (accepted) {
+            ++len;
+            if (lead && tid == 0) out.accept_path[r0 + len] = c;
+            cur = c;
+            xcur = nullptr;
+            last_pass_applied = false;
+            set_row(cur);
+            continue;
+        }
+        // rejected: the residual max(0, p - pi_e^(c)), stored and summed slice by slice
+        double *xout = xcur == xrow0 ? xrow1 : xrow0;
+        double tot_all;
+        block_inclusive_scan(run_sum(smp.draft_probs + (r0 + c) * V, xout), tid, &tot_all, ws);
+        const double total = exchange(tot_all);
+        if (total > 0.0) {  // applied; a zero residual (rounding only) leaves p as it was
+            xcur = xout;
+            xs = 1.0 / total;
+        }
+        last_pass_applied = total > 0.0;
+    }
+
+    // the emitted token: inverse CDF of the current weights in token order
+    const float u = smp.u_res[r0 + cur];
+    double total;
+    if (last_pass_applied) {
+        // the last pass stored exactly these weights, unnormalised: its slice sums
+        // serve (the draw uses xcur without the 1/Z scale)
+        xs = 1.0;
+    } else {
+        double tot_all;
+        block_inclusive_scan(run_sum(nullptr, nullptr), tid, &tot_all, ws);
+        exchange(tot_all);
+    }
+    const double *sums = part + ((nbar - 1) % 2) * kWalkMaxGroup;
+    // the slice holding u * total (the last slice of positive weight if rounding
+    // leaves none), found alike by every workgroup: wave 0's lanes hold the slices
+    if (tid < kWaveSize) {
+        double mine, incl;
+        slice_scan(sums, &mine, &incl);
+        const double tot = __shfl(incl, kWaveSize - 1, kWaveSize);
+        const double target = (double)u * tot, before = incl - mine;
+        const unsigned long long cross = __ballot(tid < G && mine > 0.0 && before + mine > target);
+        const unsigned long long pos = __ballot(tid < G && mine > 0.0);
+        const int pick = cross ? __builtin_ctzll(cross) : (pos ? 63 - __builtin_clzll(pos) : -1);
+        if (tid == (pick < 0 ? 0 : pick)) {
+            ws.ival[0] = pick;
+            ws.dval = before;
+        }
+        if (tid == 0) ws.dval2 = tot;
+    }
+    __syncthreads();
+    total = ws.dval2;
+    const int slice = ws.ival[0];
+    const double slice_before = ws.dval;
+    __syncthreads();
+    if (m == slice) {
+        // this workgroup's slice: the thread whose run crosses the target scans it
+        const double target = (double)u * total;
+        const double rs = run_sum(nullptr, nullptr);
+        double tot_all;
+        const double incl = block_inclusive_scan(rs, tid, &tot_all, ws);
+        const double start = slice_before + incl - rs;
+        if (tid == 0) ws.ival[1] = NT;
+        __syncthreads();
+        if (rs > 0.0 && start + rs > target) atomicMin(&ws.ival[1], tid);
+        __syncthreads();
+        int who = ws.ival[1];
+        if (who == NT) {  // rounding left no crossing: the last thread of positive weight
+            if (tid == 0) ws.ival[1] = -1;
+            __syncthreads();
+            if (rs > 0.0) atomicMax(&ws.ival[1], tid);
+            __syncthreads();
+            who = ws.ival[1];
+        }
+        if (tid == who) {
+            double run = start;
+            int found = -1, lastpos = -1;
+            for (int t = t0; t < t1 && found < 0; ++t) {
+                const double w = weight(t);
+                run += w;
+                if (w > 0.0) {
+                    lastpos = t;
+                    if (run > target) found = t;
+                }
+            }
+            out.next_token[b] = found >= 0 ? found : lastpos;
+        }
+    }
+    if (lead) {
+        for (int i = len + 1 + tid; i < N; i += NT) out.accept_path[r0 + i] = -1;
+        if (tid == 0) {
+            out.accept_path[r0] = 0;
+            out.accept_len[b] = len;
+            if (slice < 0) out.next_token[b] = -1;  // empty support
+            // a barrier wait that gave up: the walk's workgroups may not have agreed
+            out.status[b] = __hip_atomic_load(bar + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
+                                ? DCD_SEQ_WALK_TIMEOUT : 0;
+        }
+    }
+}
+
 // One workgroup per row; the workgroup that finishes a sequence's last row
 // (counted in seqdone, cleared by the LM-head launch) runs the sequence phase.
 template <int DT, bool SAMPLE>
@@ -1109,8 +1483,10 @@ __global__ __launch_bounds__(NT) void finish_kernel(Plan P, Inputs in, Outputs o
     __shared__ int last;
     extern __shared__ __align__(16) int dyn[];
     const int row = blockIdx.x, tid = threadIdx.x;
-    if (row == 0 && tid == 0) advance_call(P.ctl);  // the call's last kernel
+    if (row == 0 && tid == 0) advance_call(P.ctl);  // the call's last use of the call count
     if (tid == 0) sm.node_ok = 0;
+    // the spread walk that follows starts its group's barrier count from zero
+    if (SAMPLE && P.walk_group && row % P.N == 0 && tid < 2) P.walkbar[(row / P.N) * 2 + tid] = 0;
     __syncthreads();
     combine_row<DT>(P, in, out, row, tid % kWaveSize, tid / kWaveSize, sm);
     // count the row once all of its waves are done; thread 0 stores the node's
@@ -1124,7 +1500,7 @@ __global__ __launch_bounds__(NT) void finish_kernel(Plan P, Inputs in, Outputs o
                P.N - 1;
     }
     __syncthreads();
-    if (!last) return;
+    if (!last || (SAMPLE && P.walk_group)) return;  // walk_kernel walks the sequence
     // acquire: the other rows of the sequence are visible from here on
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
     verify_sequence<DT, SAMPLE>(P, in, out, smp, b, tid, sm, dyn);
@@ -1220,6 +1596,41 @@ hipError_t launch_propose(const Plan &p, const Inputs &in, const ProposeOutputs 
 // node); sampled also the walk's state: target and proposal probability of each
 // node's token, the rejected siblings and their normalisers (20 more bytes per
 // node; the doubles follow 6 N 4-byte slots, so they are 8-byte aligned for any N)
+// dynamic LDS of the spread walk: parents, tokens, target and proposal probability
+// of each node's token (16 bytes per node)
+size_t walk_lds_bytes(int N) { return (size_t)4 * N * sizeof(int); }
+
+// The spread walk pays where the single-workgroup walk leaves the chip idle (B
+// sequences walked by B CUs).  Each sequence gets CUs / B workgroups, one per CU, at
+// most kWalkMaxGroup; with fewer than 4 per sequence (B > 64 on 256 CUs) the finish
+// kernel walks each sequence in its own workgroup.  One workgroup per CU in all: with
+// 16 sequences of 64 workgroups each (4 per CU) the walk took 133 us, against about
+// 110 us for the finish kernel's walk; with 16 each, the step dropped by 48 us.
+int walk_group_size(const Plan &p) {
+    int dev = 0, cus = 0, per_cu = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+    const int G = cus / p.B < kWalkMaxGroup ? cus / p.B : kWalkMaxGroup;
+    if (G < 4) return 0;
+    const void *fn = p.dtype == kBF16 ? (const void *)walk_kernel<kBF16> : (const void *)walk_kernel<kF32>;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, NT, walk_lds_bytes(p.N)) != hipSuccess ||
+        per_cu < 1)
+        return 0;  // the cooperative launch needs every workgroup resident
+    return G;
+}
+
+hipError_t launch_walk(const Plan &p, const Inputs &in, const Outputs &out, const SampleInputs &smp,
+                       hipStream_t st) {
+    Plan pc = p;
+    Inputs ic = in;
+    Outputs oc = out;
+    SampleInputs sc = smp;
+    void *args[] = {&pc, &ic, &oc, &sc};
+    const void *fn = p.dtype == kBF16 ? (const void *)walk_kernel<kBF16> : (const void *)walk_kernel<kF32>;
+    return hipLaunchCooperativeKernel(fn, dim3(p.B * p.walk_group), dim3(NT), args,
+                                      (unsigned)walk_lds_bytes(p.N), st);
+}
+
 size_t seq_lds_bytes(int N, bool sampled) {
     return sampled ? (size_t)6 * N * sizeof(int) + (size_t)N * sizeof(double)
                    : (size_t)3 * N * sizeof(int);

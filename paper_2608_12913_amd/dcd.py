@@ -17,7 +17,7 @@ PROBE_LIB_PATH = os.path.join(PKG, "libdcd_probe.so")  # the benchmark's measure
 DCD_OK, DCD_ERR_NULL, DCD_ERR_SHAPE, DCD_ERR_PARAM = 0, -1, -2, -3
 DCD_ERR_ALIGN, DCD_ERR_WORKSPACE, DCD_ERR_UNSUPPORTED, DCD_ERR_HIP = -4, -5, -6, -7
 DCD_ERR_TOO_LARGE = -8
-SEQ_OK, SEQ_BAD_TREE, SEQ_BAD_TOKEN, SEQ_NONFINITE, SEQ_NOT_CHAIN = range(5)
+SEQ_OK, SEQ_BAD_TREE, SEQ_BAD_TOKEN, SEQ_NONFINITE, SEQ_NOT_CHAIN, SEQ_WALK_TIMEOUT = range(6)
 DCD_F32, DCD_BF16 = 0, 1
 ROW_MAX_P, ROW_LSE_P, ROW_LSE_Q, ROW_LOGZ, ROW_TOP1, ROW_MARGIN, ROW_COUNT, ROW_SIGNAL = range(8)
 NODE_LOGP_P, NODE_LOGP_Q, NODE_CD, NODE_LOGP_CD, NODE_IN_MASK, NODE_RATIO = range(6)

@@ -32,7 +32,7 @@ def test_library_exports_every_declared_function():
     L = dcd.lib()
     for n in names:
         assert hasattr(L, n), n
-    assert L.dcd_abi_version() == 6
+    assert L.dcd_abi_version() == 7
     probes = _declared_functions("dcd_probe.h")
     assert set(probes) == set(dcd.PROBE_EXPORTS)
     PL = dcd.probe_lib()

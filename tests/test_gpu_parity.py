@@ -478,6 +478,32 @@ def test_sampled_tree_forced_paths():
     assert g["accept_len"][1] == 0
 
 
+@pytest.mark.parametrize("seed,B,V,dtype", [(0, 4, 2500, "bf16"), (1, 3, 1499, "f32"), (2, 1, 3001, "bf16"),
+                                           (3, 2, 130, "bf16")])
+def test_untruncated_sampled_trees_spread_walk(seed, B, V, dtype):
+    """theta = 0 with at most 4 sequences: each sequence's walk is spread over 64
+    workgroups, one slice of the vocabulary each (ragged at the vocabulary's end;
+    with V = 130 most slices are empty), with several rejections per node."""
+    case = synth.make_case("s8_chain16x8", 80 + seed, B=B, N=24, tree="tree", depth=4,
+                           max_children=5, V=V, dp=256, dq=128, theta=0.0, dtype=dtype)
+    probs, tokens = _sampled_tree_setup(case)
+    g, o = _check_sample(case, probs, tokens, f"spread walk seed {seed} B={B} V={V} {dtype}")
+    assert np.all(g["status"] == 0)
+    walked = np.isfinite(o["walk_ratio"]) | np.isinf(o["walk_ratio"])
+    _say(f"spread walk seed {seed}: {int(walked.sum())} nodes tested, accept lengths "
+         f"{g['accept_len'].tolist()}")
+
+
+@pytest.mark.parametrize("B", [64, 65])
+def test_untruncated_sampled_many_sequences(B):
+    """theta = 0: 64 sequences get 4 workgroups each for their walks (the fewest the
+    spread walk takes); 65 are walked by the finish kernel, one workgroup each."""
+    case = synth.make_case("s8_chain16x8", 90 + B, B=B, N=3, V=997, dp=64, dq=32, theta=0.0)
+    probs, tokens = _sampled_setup(case)
+    g, _ = _check_sample(case, probs, tokens, f"untruncated sampled B={B}")
+    assert np.all(g["status"] == 0)
+
+
 def test_sampled_tree_at_the_node_limit():
     """4096 nodes (the largest sequence): the walk's state fills most of the LDS."""
     case = synth.make_case("s8_chain16x8", 51, B=1, N=4096, tree="tree", depth=12,
@@ -563,6 +589,23 @@ def test_full_s8_chain16x8(theta):
 
 @pytest.mark.slow
 @pytest.mark.parametrize("theta", [0.1, 0.0])
+def test_full_b8_tree64_sampled(theta):
+    """The sampled 64-node tree against the oracle (theta = 0: the walk spread over 64
+    workgroups)."""
+    case = synth.make_case("b8_tree64", 0, mode="sample", theta=theta)
+    probs, tokens = _full_sampled_setup(case)
+    _say(f"b8_tree64 sampled theta {theta}: oracle")
+    o, lp = _oracle_sample(case, probs, tokens)
+    dev = _runner().from_case(case, tokens, draft_probs=probs)
+    g = dev.run("sample")
+    report = {}
+    _compare_sampled(g, o, lp, case, probs, tokens, report, dev)
+    assert np.all(g["status"] == 0)
+    _say(f"b8_tree64 sampled: ok {report}; accept lengths {g['accept_len'].tolist()}")
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("theta", [0.1, 0.0])
 def test_full_b8_batch32x64(theta):
     # theta 0.1: the many-row kernel; theta 0: the streaming kernel's 64-row shape
     # with 32 row blocks per tile.  Eight sequences spread over the batch (rows in
@@ -601,15 +644,15 @@ def test_full_b8_batch32x64(theta):
 
 
 @pytest.mark.slow
-@pytest.mark.parametrize("workload,mode", [("b8_tree64", "greedy"), ("s8_chain16x8", "sample"),
-                                           ("b8_tree64", "sample")])
-def test_full_size_repeated_calls_are_bit_identical(workload, mode):
+@pytest.mark.parametrize("workload,mode,theta", [("b8_tree64", "greedy", 0.1), ("s8_chain16x8", "sample", 0.1),
+                                                 ("b8_tree64", "sample", 0.1), ("b8_tree64", "sample", 0.0)])
+def test_full_size_repeated_calls_are_bit_identical(workload, mode, theta):
     """Which vocabulary tiles keep their candidates depends on when each reads the
     running bound; the outputs must not.  Full-size calls (64 rows: one row block per
     tile; 128 rows: the 128-row shape, 501 tiles on 256 CUs in two rounds) repeated
     with another call of a different problem in between, every output compared bit
     for bit."""
-    case = synth.make_case(workload, 0, mode=mode)
+    case = synth.make_case(workload, 0, mode=mode, theta=theta)
     if mode == "sample":
         probs, tokens = _full_sampled_setup(case)
     else:
