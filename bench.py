@@ -189,10 +189,11 @@ def main():
     kernel = ("lmhead_wide_kernel" if case.dtype == "bf16" and case.theta > 0 and R >= 512
               else "lmhead_kernel")
     ridge = MFMA_BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9)
-    # the committed counters cover the default workloads of each kernel only
-    traffic, traffic_src = (counted_traffic(kernel, args.workload)
-                            if not over and own_mode and not args.final_norm
-                            else (None, "no counters for this workload"))
+    # committed counters: per kernel and workload, and per mode and theta where they
+    # differ from the workload's own
+    variant = "" if own_mode and not over else f"_{mode}_theta{case.theta:g}"
+    traffic, traffic_src = (counted_traffic(kernel, args.workload + variant)
+                            if not args.final_norm else (None, "no counters for this workload"))
     if case.dtype == "bf16" and flops / kbytes > ridge:
         achieved = flops / (ms_lmhead * 1e-3) / 1e12
         roofline = dict(bound="mfma", achieved=round(achieved, 1), peak=MFMA_BF16_PEAK_TFLOPS,
