@@ -204,6 +204,9 @@ def main():
                         frac=round(achieved / HBM_PEAK_GBS, 4))
     roofline.update(traffic=traffic, kernel=kernel, algorithmic_bytes=kbytes, flops=flops,
                     avg_us=round(ms_lmhead * 1e3, 2), traffic_source=traffic_src)
+    util = counted_utilisation(kernel, args.workload + variant) if not args.final_norm else None
+    if util:
+        roofline["counters"] = util
     if not args.no_probes:
         measured = measured_ceilings(torch, stream, log)
         roofline["measured_peak"] = measured
@@ -296,6 +299,35 @@ def code_sha256(root, rels):
             if line:
                 h.update(line.encode() + b"\n")
     return h.hexdigest()
+
+
+def read_profile_fields(path, root):
+    """The key: value fields of a committed profiler summary, or None when the code of
+    its listed sources no longer hashes to the recorded digest."""
+    fields = {}
+    for line in open(path):
+        if ":" in line and not line.startswith(" "):
+            k, v = line.split(":", 1)
+            fields[k.strip()] = v.strip()
+    rels = fields.get("sources", "").split()
+    if not rels or code_sha256(root, rels) != fields.get("sources_code_sha256"):
+        return None
+    return fields
+
+
+def counted_utilisation(kernel, workload):
+    """MFMA-busy and LDS-busy fractions of the LM-head kernel and its waves' wait
+    share, from the committed SQ-counter summary of this kernel and workload (None when
+    there is none or the kernel has changed since)."""
+    root = os.path.dirname(os.path.abspath(__file__))
+    path = os.path.join(root, "profiles", f"{kernel}_{workload}_sq_counters.txt")
+    if not os.path.exists(path):
+        return None
+    f = read_profile_fields(path, root)
+    if f is None:
+        return None
+    return {"mfma_busy": float(f["mfma_busy"]), "lds_busy": float(f["lds_busy"]),
+            "wave_wait": float(f["wave_wait"]), "source": os.path.relpath(path, root)}
 
 
 def counted_traffic(kernel, workload):
