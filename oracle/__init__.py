@@ -19,7 +19,10 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "dcd_oracle.c")
-_LIB = os.path.join(_HERE, "liboracle.so")
+# the library the loader uses; DCD_ORACLE_LIB names another build of the same source
+# (the sanitised one, see build)
+_LIB = os.environ.get("DCD_ORACLE_LIB") or os.path.join(_HERE, "liboracle.so")
+_SAN_LIB = os.path.join(_HERE, "liboracle_san.so")
 
 # row_stats slots
 RS_MAXP, RS_LSEP, RS_LSEQ, RS_LOGZ, RS_TOP1, RS_MARGIN, RS_COUNT, RS_SIGNAL = range(8)
@@ -30,15 +33,20 @@ NS_LPP, NS_LPQ, NS_CD, NS_LPCD, NS_INMASK, NS_RATIO = range(6)
 SEQ_OK, SEQ_BAD_TREE, SEQ_BAD_TOKEN, SEQ_NONFINITE, SEQ_NOT_CHAIN = range(5)
 
 
-def build(force: bool = True) -> str:
-    """Compile the oracle with gcc (-O2, OpenMP, no fast-math)."""
-    if force or not os.path.exists(_LIB):
-        tmp = _LIB + ".tmp"
+def build(force: bool = True, sanitize: bool = False) -> str:
+    """Compile the oracle with gcc (-O2, OpenMP, no fast-math).  sanitize: a separate
+    build with AddressSanitizer and UndefinedBehaviorSanitizer (any report aborts), for
+    running the pins under them; loading it needs libasan preloaded."""
+    lib = _SAN_LIB if sanitize else _LIB
+    if force or not os.path.exists(lib):
+        tmp = lib + ".tmp"
+        opt = (["-O1", "-g", "-fno-omit-frame-pointer", "-fsanitize=address,undefined",
+                "-fno-sanitize-recover=all"] if sanitize else ["-O2"])
         subprocess.check_call(
-            ["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-fopenmp", "-Wall", _SRC, "-o", tmp, "-lm"]
+            ["gcc", *opt, "-std=c11", "-fPIC", "-shared", "-fopenmp", "-Wall", _SRC, "-o", tmp, "-lm"]
         )
-        os.replace(tmp, _LIB)
-    return _LIB
+        os.replace(tmp, lib)
+    return lib
 
 
 _lib = None
