@@ -166,6 +166,39 @@ def main():
     ms_step = ev0.elapsed_time(ev1) / args.steps
     out = dev.run("greedy" if mode == "propose" else mode)
 
+    norm_cost = None
+    if args.final_norm and mode != "propose":
+        # the normalisation's own cost: the same step without the flag on rows already
+        # normalised the same way (fp32 statistics, bf16 roundings; the last bit of an
+        # element may differ from the library's, which does not matter for timing)
+        plain = {}
+        for key, hkey, d in (("hp", "norm_p", case.dp), ("hq", "norm_q", case.dq)):
+            x = getattr(case, key)
+            xf = synth.bf16_to_f32(x) if case.dtype == "bf16" else np.asarray(x, np.float32)
+            gf = synth.bf16_to_f32(norm[hkey]) if case.dtype == "bf16" else norm[hkey]
+            r = (1.0 / np.sqrt(np.mean(xf * xf, axis=1, dtype=np.float32) + np.float32(norm["norm_eps"])))
+            t = xf * r[:, None].astype(np.float32)
+            if case.dtype == "bf16":
+                plain[key] = synth.bf16_bits(gf[None, :] * synth.bf16_to_f32(synth.bf16_bits(t)))
+            else:
+                plain[key] = (gf[None, :] * t).astype(np.float32)
+        dev_plain = DeviceProblem.from_case(case, tokens, draft_probs=probs, **plain)
+        for _ in range(args.warmup):
+            dev_plain.launch(mode, stream)
+        torch.cuda.synchronize()
+        p0, p1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        p0.record(stream)
+        for _ in range(args.steps):
+            dev_plain.launch(mode, stream)
+        p1.record(stream)
+        torch.cuda.synchronize()
+        ms_plain = p0.elapsed_time(p1) / args.steps
+        del dev_plain
+        norm_cost = {"step_us_without_norm": round(ms_plain * 1e3, 2),
+                     "cost_us": round((ms_step - ms_plain) * 1e3, 2)}
+        log(f"final normalisation: step {ms_step * 1e3:.1f} us with it, {ms_plain * 1e3:.1f} us "
+            f"on the same rows normalised beforehand")
+
     # the dominant kernel alone (LM heads + partials), same stream, HIP events
     lm_mode = "greedy" if mode == "greedy" else "sample"
     for _ in range(5):
@@ -247,6 +280,8 @@ def main():
         "roofline": roofline,
         "cpu_baseline": cpu,
     }
+    if norm_cost:
+        line["final_norm_cost"] = norm_cost
     print(json.dumps(line), flush=True)
 
 
