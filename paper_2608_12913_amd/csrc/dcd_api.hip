@@ -128,7 +128,7 @@ int run(const dcd_problem *p, const dcd_inputs *in, const SampleInputs *smp,
     hipStream_t st = (hipStream_t)stream;
     // untruncated sampled verification: each sequence's walk spread over a group of
     // workgroups when they fit one cooperative launch
-    P.walk_group = smp && P.full ? walk_group_size(P) : 0;
+    P.walk_group = smp && P.full ? walk_group_size(P, (hipStream_t)stream) : 0;
     if (normalise(P, I, st) != hipSuccess) return DCD_ERR_HIP;
     if (launch_lmhead(P, I, st) != hipSuccess) return DCD_ERR_HIP;
     if (launch_finish(P, I, O, smp, st) != hipSuccess) {
@@ -217,7 +217,10 @@ size_t workspace_layout(Plan &p, char *base) {
     p.tcount = (int *)take(R * p.ntiles * sizeof(int));
     p.bound = (uint32_t *)take((size_t)kBoundCopies * R * sizeof(uint32_t));
     p.nodez = (float4 *)take(R * sizeof(float4));
-    p.seqdone = (int *)take((size_t)p.B * sizeof(int));
+    p.seqdone = (int *)take((size_t)2 * p.B * sizeof(int));  // seqdone, then seqfail
+    p.seqfail = p.seqdone + p.B;
+    p.wratio = (double *)take(R * sizeof(double));
+    p.wterm = (int *)take(R * sizeof(int));
     if (p.final_norm) {
         const size_t esz = p.dtype == kBF16 ? 2 : 4;
         p.hn_p = take(R * p.dp * esz);

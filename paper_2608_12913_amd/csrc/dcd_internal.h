@@ -66,6 +66,12 @@ struct Plan {
     float4 *nodez;     // [R]           node r's token under its parent row: (z_p, z_q) as a candidate
                        //   (NaN: not one), (z_p, z_q) by dot product (NaN: not computed)
     int *seqdone;      // [B]           rows of each sequence finished by the combine step
+    int *seqfail;      // [B]           (after seqdone, cleared with it) sampled, masked: a row of
+                       //   the sequence could not settle its children's walk decisions
+    double *wratio;    // [R]           sampled, masked: node r's accept ratio under its parent
+                       //   (every earlier sibling rejected; -1: rejected whatever u is)
+    int *wterm;        // [R]           sampled, masked: the token emitted if the walk ends at
+                       //   node r (-1: an empty support)
     // untruncated sampled verification with the walk spread over a group of
     // workgroups per sequence (walk_kernel; walk_group = 0: the finish kernel walks)
     int walk_group;    // workgroups per sequence
@@ -217,7 +223,7 @@ hipError_t launch_finish(const Plan &p, const Inputs &in, const Outputs &out,
                          const SampleInputs *smp, hipStream_t st);
 // untruncated sampled verification: workgroups per sequence for the spread walk
 // (0 when the sequences do not fit a cooperative launch), and that launch
-int walk_group_size(const Plan &p);
+int walk_group_size(const Plan &p, hipStream_t st);
 hipError_t launch_walk(const Plan &p, const Inputs &in, const Outputs &out, const SampleInputs &smp,
                        hipStream_t st);
 

@@ -642,7 +642,7 @@ template <int DT, bool FULL, bool STREAM>
 __global__ __launch_bounds__(NT, kMinBlocks) void lmhead_kernel(Plan P, Inputs in) {
     extern __shared__ __align__(16) char lds[];
     // workgroup 0 clears this call's row bounds and sequence counters first
-    if (blockIdx.x == 0) clear_call_state(P.ctl, P.bound, kBoundCopies * P.R, P.seqdone, P.B);
+    if (blockIdx.x == 0) clear_call_state(P.ctl, P.bound, kBoundCopies * P.R, P.seqdone, 2 * P.B);
     // workgroup -> (vocabulary tile, row block); the row blocks of one tile are
     // dispatched back to back on the same XCD (workgroup id modulo 8) so the
     // tile's weights are re-read from that XCD's L2

@@ -458,7 +458,7 @@ __global__ __launch_bounds__(NT, 1) void lmhead_wide_kernel(Plan P, Inputs in) {
     __shared__ __align__(16) float misc[kMiscFloats];
     __shared__ __align__(16) char sink[4 * 512];  // L2 prefetches land here, unread
     // workgroup 0 clears this call's row bounds and sequence counters first
-    if (blockIdx.x == 0) clear_call_state(P.ctl, P.bound, kBoundCopies * P.R, P.seqdone, P.B);
+    if (blockIdx.x == 0) clear_call_state(P.ctl, P.bound, kBoundCopies * P.R, P.seqdone, 2 * P.B);
     // workgroup -> (vocabulary tile, row tile); the row tiles of one vocabulary tile
     // are dispatched back to back on the same XCD (workgroup id modulo 8), so the
     // tile's weights are read from HBM once and from that XCD's L2 otherwise

@@ -18,6 +18,8 @@
 // phase takes only the tiles whose own expert max reaches the row's threshold
 // (those are never dropped, and hold every mask member), and a draft token's
 // logits come from the candidates only when the token is a mask member.
+#include <atomic>
+
 #include "dcd.h"
 #include "dcd_internal.h"
 
@@ -30,6 +32,11 @@ constexpr int kTilesPerLane = kTileTokens <= 256 ? 8 : 4;  // tiles a lane takes
 static_assert(kWordsPerTile % 4 == 0, "a tile's bitmap is whole 16-byte words");
 constexpr int kPass = kWaveSize * kTilesPerLane;
 constexpr int kList = 1024;              // candidate ids gathered per round
+// masked target, sampled verification: the walk's decisions settled per row (settle_children)
+constexpr int kMembers = kList;          // mask members of a row kept in LDS
+constexpr int kMaxKids = 64;             // children of a node
+constexpr int kKidQ = 4096;              // proposal values gathered: children x members
+constexpr size_t kSettleLds = (size_t)kMaxKids * 3 * 4 + (size_t)kMembers * 8 + (size_t)kKidQ * 4;
 
 struct Lse {  // running log-sum-exp: value = m + log(s)
     float m, s;
@@ -190,7 +197,10 @@ __device__ __forceinline__ void emit_ids(const uint4 (&w)[kTileU4], int tile, in
 // parents, tokens and row argmax: 12 bytes per node).
 struct Smem {
     int list[kList];    // candidate ids (row phase: wave 0; draw: whole group)
-    double wts[kList];  // draw weights
+    double wts[kList];  // draw weights; in a sampled call's row phase, the row's mask
+                        //   members in token order (token, cd score) packed (kMembers)
+    int mcount;         // sampled, masked: the row's mask members (more than kMembers: not kept)
+    float mlogz;        //   and its log Z
     float4 nodez;       // the row's draft token under its parent row (waves 1-3)
     int node_ok;        // nodez is to be written
     int wave_tot[NT / kWaveSize];
@@ -287,7 +297,7 @@ __device__ __forceinline__ void row_stats_full(const Plan &P, int row, int lane,
 // thread that counts the row.
 template <int DT>
 __device__ __forceinline__ void combine_row(const Plan &P, const Inputs &in, const Outputs &out, int row, int lane,
-                            int wave, Smem &sm) {
+                            int wave, Smem &sm, bool members = false) {
     const bool want_node_logits = out.node_stats != nullptr;
     if (wave >= 1) {
         if (!in.parents) return;  // rows without a tree (proposals)
@@ -430,30 +440,49 @@ __device__ __forceinline__ void combine_row(const Plan &P, const Inputs &in, con
     Top2 best{-INFINITY, -1, -INFINITY, 0.f, 0.f};
     int count = 0;
     int top_p = -1;  // the expert's top-1: the lowest candidate whose z_p is max_p
+    // members: the mask members (token, cd) in token order, for the children's walk
+    // decisions settled in the same workgroup (kept: how many seen so far)
+    unsigned long long *const mlist = reinterpret_cast<unsigned long long *>(sm.wts);
+    int kept = 0;
     for (int base = 0; base < P.ntiles; base += kPass) {
         if (base > 0) issue_cands(base);
         mask_cands(base);
-        int nset = 0;
+        // list positions in token order: tile base + lane + k * 64 is the (k * 64 +
+        // lane)-th tile of the pass, so the tiles are counted k-major
+        int nset[kTilesPerLane], first[kTilesPerLane];
+        int total = 0;
 #pragma unroll
-        for (int k = 0; k < kTilesPerLane; ++k) nset += popc_tile(w[k]);
-        int total;
-        const int first = wave_exclusive_scan(nset, lane, &total);
+        for (int k = 0; k < kTilesPerLane; ++k) {
+            nset[k] = popc_tile(w[k]);
+            int tk;
+            first[k] = total + wave_exclusive_scan(nset[k], lane, &tk);
+            total += tk;
+        }
         for (int lo = 0; lo < total; lo += kList) {
-            if (nset > 0 && first < lo + kList && first + nset > lo) {
-                int idx = first;
 #pragma unroll
-                for (int k = 0; k < kTilesPerLane; ++k)
+            for (int k = 0; k < kTilesPerLane; ++k)
+                if (nset[k] > 0 && first[k] < lo + kList && first[k] + nset[k] > lo) {
+                    int idx = first[k];
                     emit_ids(w[k], base + lane + k * kWaveSize, lo, &idx, list);
-            }
+                }
             wave_lds_sync();
             const int n = min(kList, total - lo);
-            for (int m = lane; m < n; m += kWaveSize) {
-                const int t = list[m];
+            for (int mb = 0; mb < n; mb += kWaveSize) {
+                const int m = mb + lane;
+                const int t = list[min(m, n - 1)];
                 const float2 c = cz[t];
-                if (!(c.x >= thr)) continue;
+                const bool member = m < n && c.x >= thr;
+                const float cd = (1.f + s) * (c.x - lse_p) - s * (c.y - lse_q);
+                if (members) {  // kept in token order: list order, then lane order
+                    const unsigned long long mask = __ballot(member);
+                    const int pos = kept + __popcll(mask & ((1ull << lane) - 1ull));
+                    if (member && pos < kMembers)
+                        mlist[pos] = (unsigned long long)(uint32_t)t << 32 | __float_as_uint(cd);
+                    kept += __popcll(mask);
+                }
+                if (!member) continue;
                 ++count;
                 top_p = c.x == max_p ? (int)min((unsigned)top_p, (unsigned)t) : top_p;
-                const float cd = (1.f + s) * (c.x - lse_p) - s * (c.y - lse_q);
                 best = top2_merge(best, Top2{cd, t, -INFINITY, c.x, c.y});
                 lc = lse_merge(lc, Lse{cd, 1.f});
             }
@@ -476,6 +505,10 @@ __device__ __forceinline__ void combine_row(const Plan &P, const Inputs &in, con
 
     if (lane == 0) {
         const float logZ = lc.m + __logf(lc.s);
+        if (members) {
+            sm.mcount = kept;
+            sm.mlogz = logZ;
+        }
         // the best candidate's logits came along with it (no second fetch)
         const float signal = best.id >= 0 ? (best.zp - lse_p) - (best.zq - lse_q) : NAN;
         float ri[kRowInfo] = {};
@@ -1012,7 +1045,12 @@ __device__ __forceinline__ void verify_sequence(const Plan &P, const Inputs &in,
     }
 
     // sampled: node statistics, and per node the target probability of its token
-    // under the parent row and its proposal probability, staged for the walk
+    // under the parent row and its proposal probability, staged for the walk.  With
+    // a mask, the rows settled the walk's decisions (settle_children) unless one of
+    // them could not: then each child's accept ratio, its uniform and each node's
+    // terminal token are staged instead, in the same round.
+    const bool settled = !P.full && P.seqfail[b] == 0;
+    float *s_u = reinterpret_cast<float *>(s_amax);  // the sampled walk has no use for the argmax
     if (out.node_stats && tid < 6) out.node_stats[r0 * 6 + tid] = NAN;
     for (int i = 1 + tid; i < N; i += NT) {
         const int x = s_tok[i];
@@ -1021,9 +1059,43 @@ __device__ __forceinline__ void verify_sequence(const Plan &P, const Inputs &in,
         const float p0 = n.in_mask ? __expf(n.lpcd) : 0.f;
         s_p0[i] = p0;
         s_qx[i] = pe;
+        if (settled) {
+            s_invz[i] = P.wratio[r0 + i];
+            s_u[i] = smp.u_acc[r0 + i];
+        }
         if (out.node_stats) write_node_stats(out.node_stats + (r0 + i) * 6, n, pe > 0.f ? p0 / pe : INFINITY);
     }
+    if (settled)
+        for (int i = tid; i < N; i += NT) s_rej[i] = P.wterm[r0 + i];
     __syncthreads();
+    if (settled) {
+        // the walk from the settled decisions: child c of the current node (every
+        // earlier child of it rejected) is accepted iff its uniform is at most its
+        // ratio; where the walk ends, the node's terminal token is emitted
+        if (tid == 0) {
+            int cur = 0, len = 0;
+            for (int c = 1; c < N; ++c) {
+                if (s_par[c] != cur) continue;
+                if ((double)s_u[c] <= s_invz[c]) {
+                    ++len;
+                    out.accept_path[r0 + len] = c;
+                    cur = c;  // its children have larger indices
+                }
+            }
+            sm.ints[0] = len;
+            sm.ints[1] = s_rej[cur];
+        }
+        __syncthreads();
+        const int len = sm.ints[0];
+        for (int i = len + 1 + tid; i < N; i += NT) out.accept_path[r0 + i] = -1;
+        if (tid == 0) {
+            out.accept_path[r0] = 0;
+            out.status[b] = 0;
+            out.accept_len[b] = len;
+            out.next_token[b] = sm.ints[1];
+        }
+        return;
+    }
     // The walk (Alg. 1 over a tree): the children of the current node are tried in
     // index order, each against the target left by the siblings rejected before it;
     // an accepted child becomes the current node; when every child is rejected (or
@@ -1474,6 +1546,135 @@ __global__ __launch_bounds__(NT) void walk_kernel(Plan P, Inputs in, Outputs out
     }
 }
 
+// ---------------------------------------------------------------------------
+// Masked target, sampled verification: the walk's decisions at a node, settled by
+// the node's own row workgroup before the sequence phase.
+//
+// At node i the walk (Alg. 1 over a tree) tries i's children in index order; when
+// it reaches child c every earlier child of i has been rejected, so what it does at
+// c depends only on row i's target, those children's proposals and c's uniform:
+// the ratio of the residual left by the earlier children, at c's token, to c's
+// proposal of that token.  If the walk ends at i, every child of i was rejected, so
+// the token it emits is the draw, with u_resample of node i, from the residual left
+// by all of them.  Row i's workgroup holds the row's mask members (the support) in
+// LDS after the row phase, so it computes these: per child the accept ratio (-1:
+// rejected whatever its uniform) and the residual's normaliser, and the row's
+// terminal token.  The sequence phase then only compares uniforms with ratios.  The
+// residual arithmetic is the walk's own (Residual): w <- max(0, w - q) * (1/Z) per
+// applied rejection, Z the residual's sum over the support (a rejection whose
+// residual sums to zero leaves w as it was).  A row with more mask members than
+// kMembers, a node with more than kMaxKids children, or more than kKidQ proposal
+// values to gather marks its sequence, which the sequence phase then walks itself.
+template <int DT>
+__device__ __forceinline__ void settle_children(const Plan &P, const Inputs &in, const SampleInputs &smp, int row, int tid,
+                                Smem &sm, int *dyn) {
+    const int N = P.N, V = P.V, i = row % N, b = row / N;
+    const size_t r0 = (size_t)row - i;
+    int *kids = dyn, *ktok = dyn + kMaxKids;
+    float *kq = reinterpret_cast<float *>(dyn + 2 * kMaxKids);
+    double *w = reinterpret_cast<double *>(dyn + 3 * kMaxKids);  // [kMembers]
+    float *q = reinterpret_cast<float *>(w + kMembers);          // [kKidQ]: child k, member t at k*L + t
+    const unsigned long long *mlist = reinterpret_cast<const unsigned long long *>(sm.wts);
+    const int L = sm.mcount;
+    const float logZ = sm.mlogz;
+    // the children of node i (all later nodes), in index order: each thread takes a
+    // contiguous range of the later nodes
+    const int per = (N - 1 - i + NT - 1) / NT;
+    const int c0 = i + 1 + tid * per, c1 = min(N, c0 + per);
+    int mine = 0;
+    for (int c = c0; c < c1; ++c) mine += in.parents[r0 + c] == i;
+    int m;
+    const int first = group_exclusive_scan(mine, tid, &m, sm);
+    const bool ok = L <= kMembers && m <= kMaxKids && (size_t)m * (size_t)L <= (size_t)kKidQ;
+    if (ok) {
+        if (mine > 0) {
+            int k = first;
+            for (int c = c0; c < c1; ++c)
+                if (in.parents[r0 + c] == i) {
+                    // a token outside the vocabulary fails the sequence later; read in range
+                    const int x = min(max(in.tokens[r0 + c], 0), V - 1);
+                    kids[k] = c;
+                    ktok[k] = x;
+                    kq[k] = smp.draft_probs[(r0 + c) * V + x];
+                    ++k;
+                }
+        }
+        // the target over the support (the row phase's cd scores, in token order)
+        for (int t = tid; t < L; t += NT) w[t] = (double)__expf(__uint_as_float((uint32_t)mlist[t]) - logZ);
+    }
+    __syncthreads();
+    if (ok)  // every child's proposal over the support, gathered in one round
+        for (int e = tid; e < m * L; e += NT)
+            q[e] = smp.draft_probs[(r0 + kids[e / L]) * V + (int)(mlist[e % L] >> 32)];
+    __syncthreads();
+    if (!ok) {
+        if (tid == 0) atomicOr(&P.seqfail[b], 1);
+        return;
+    }
+    if (tid >= kWaveSize) return;
+    const int lane = tid;
+    // sums over the support in a fixed order: lane-strided partials, then a tree
+    auto wave_sum_d = [&](double x) {
+#pragma unroll
+        for (int d = kWaveSize / 2; d > 0; d >>= 1) x += __shfl_down(x, d, kWaveSize);
+        return __shfl(x, 0, kWaveSize);
+    };
+    for (int k = 0; k < m; ++k) {
+        // the residual left by the earlier children, at this child's token (0 off
+        // the support; a token appears at most once there)
+        int at = -1;
+        for (int t = lane; t < L; t += kWaveSize) at = (int)(mlist[t] >> 32) == ktok[k] ? t : at;
+#pragma unroll
+        for (int d = kWaveSize / 2; d > 0; d >>= 1) at = max(at, __shfl_xor(at, d, kWaveSize));
+        const double wx = at >= 0 ? w[at] : 0.0;
+        if (lane == 0) {
+            const double ratio = kq[k] > 0.f ? wx / (double)kq[k] : INFINITY;
+            P.wratio[r0 + kids[k]] = wx > 0.0 ? ratio : -1.0;
+        }
+        const float *qk = q + (size_t)k * L;
+        double part = 0.0;
+        for (int t = lane; t < L; t += kWaveSize) part += fmax(0.0, w[t] - (double)qk[t]);
+        const double total = wave_sum_d(part);
+        if (total > 0.0) {
+            const double invz = 1.0 / total;
+            for (int t = lane; t < L; t += kWaveSize) w[t] = fmax(0.0, w[t] - (double)qk[t]) * invz;
+        }
+        wave_lds_sync();
+    }
+    // the terminal draw: inverse CDF of what is left, in token order (lane l a
+    // contiguous run of the support, an inclusive scan over the lanes), at u * total;
+    // the last token of positive weight if rounding leaves none above it
+    const int per2 = (L + kWaveSize - 1) / kWaveSize;
+    const int ta = min(L, lane * per2), te = min(L, ta + per2);
+    double run = 0.0;
+    for (int t = ta; t < te; ++t) run += w[t];
+    double incl = run;
+#pragma unroll
+    for (int d = 1; d < kWaveSize; d <<= 1) {
+        const double y = __shfl_up(incl, d, kWaveSize);
+        if (lane >= d) incl += y;
+    }
+    const double tot = __shfl(incl, kWaveSize - 1, kWaveSize);
+    const double target = (double)smp.u_res[row] * tot, before = incl - run;
+    const unsigned long long cross = __ballot(run > 0.0 && before + run > target);
+    const unsigned long long pos = __ballot(run > 0.0);
+    const int who = cross ? __builtin_ctzll(cross) : (pos ? 63 - __builtin_clzll(pos) : -1);
+    if (who < 0) {
+        if (lane == 0) P.wterm[row] = -1;  // an empty support
+    } else if (lane == who) {
+        double acc = before;
+        int found = -1, last = -1;
+        for (int t = ta; t < te && found < 0; ++t) {
+            acc += w[t];
+            if (w[t] > 0.0) {
+                last = t;
+                if (acc > target) found = t;
+            }
+        }
+        P.wterm[row] = (int)(mlist[found >= 0 ? found : last] >> 32);
+    }
+}
+
 // One workgroup per row; the workgroup that finishes a sequence's last row
 // (counted in seqdone, cleared by the LM-head launch) runs the sequence phase.
 template <int DT, bool SAMPLE>
@@ -1488,11 +1689,16 @@ __global__ __launch_bounds__(NT) void finish_kernel(Plan P, Inputs in, Outputs o
     // the spread walk that follows starts its group's barrier count from zero
     if (SAMPLE && P.walk_group && row % P.N == 0 && tid < 2) P.walkbar[(row / P.N) * 2 + tid] = 0;
     __syncthreads();
-    combine_row<DT>(P, in, out, row, tid % kWaveSize, tid / kWaveSize, sm);
+    combine_row<DT>(P, in, out, row, tid % kWaveSize, tid / kWaveSize, sm, SAMPLE && !P.full);
     // count the row once all of its waves are done; thread 0 stores the node's
     // logits, and the release half of the counting atomic publishes them together
-    // with wave 0's results (the workgroup barrier orders those before it)
+    // with wave 0's results and the settled walk decisions (the workgroup barrier
+    // orders those before it)
     __syncthreads();
+    if (SAMPLE && !P.full) {
+        settle_children<DT>(P, in, smp, row, tid, sm, dyn);
+        __syncthreads();
+    }
     const int b = row / P.N;
     if (tid == 0) {
         if (sm.node_ok) P.nodez[row] = sm.nodez;
@@ -1606,17 +1812,39 @@ size_t walk_lds_bytes(int N) { return (size_t)4 * N * sizeof(int); }
 // kernel walks each sequence in its own workgroup.  One workgroup per CU in all: with
 // 16 sequences of 64 workgroups each (4 per CU) the walk took 133 us, against about
 // 110 us for the finish kernel's walk; with 16 each, the step dropped by 48 us.
-int walk_group_size(const Plan &p) {
-    int dev = 0, cus = 0, per_cu = 0;
-    if (hipGetDevice(&dev) != hipSuccess) return 0;
-    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+int walk_group_size(const Plan &p, hipStream_t st) {
+    // per device, looked up once: its CU count and whether a workgroup of the walk
+    // (at the largest LDS it asks for) fits on a CU, per element type
+    constexpr int kDevices = 64;
+    static std::atomic<int> cus_of[kDevices], fits_of[kDevices][2];  // 0: not looked up yet
+    int dev = -1;
+    if ((st ? hipStreamGetDevice(st, &dev) : hipGetDevice(&dev)) != hipSuccess || dev < 0 || dev >= kDevices)
+        return 0;
+    int cus = cus_of[dev].load(std::memory_order_relaxed);
+    if (cus == 0) {
+        if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+            return 0;
+        cus_of[dev].store(cus, std::memory_order_relaxed);
+    }
     const int G = cus / p.B < kWalkMaxGroup ? cus / p.B : kWalkMaxGroup;
     if (G < 4) return 0;
-    const void *fn = p.dtype == kBF16 ? (const void *)walk_kernel<kBF16> : (const void *)walk_kernel<kF32>;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, NT, walk_lds_bytes(p.N)) != hipSuccess ||
-        per_cu < 1)
-        return 0;  // the cooperative launch needs every workgroup resident
-    return G;
+    const int t = p.dtype == kBF16 ? 1 : 0;
+    int fits = fits_of[dev][t].load(std::memory_order_relaxed);
+    if (fits == 0) {
+        // the cooperative launch needs every workgroup resident; one per CU is asked
+        // for, so a single workgroup with the most LDS the walk uses must fit
+        int per_cu = 0, cur = -1;
+        const void *fn = t ? (const void *)walk_kernel<kBF16> : (const void *)walk_kernel<kF32>;
+        if (hipGetDevice(&cur) != hipSuccess) return 0;
+        if (cur != dev && hipSetDevice(dev) != hipSuccess) return 0;
+        const hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, NT,
+                                                                          walk_lds_bytes(kMaxNodes));
+        if (cur != dev) hipSetDevice(cur);
+        if (e != hipSuccess) return 0;
+        fits = per_cu >= 1 ? 1 : 2;
+        fits_of[dev][t].store(fits, std::memory_order_relaxed);
+    }
+    return fits == 1 ? G : 0;
 }
 
 hipError_t launch_walk(const Plan &p, const Inputs &in, const Outputs &out, const SampleInputs &smp,
@@ -1631,18 +1859,20 @@ hipError_t launch_walk(const Plan &p, const Inputs &in, const Outputs &out, cons
                                       (unsigned)walk_lds_bytes(p.N), st);
 }
 
-size_t seq_lds_bytes(int N, bool sampled) {
-    return sampled ? (size_t)6 * N * sizeof(int) + (size_t)N * sizeof(double)
-                   : (size_t)3 * N * sizeof(int);
+size_t seq_lds_bytes(int N, bool sampled, bool masked) {
+    if (!sampled) return (size_t)3 * N * sizeof(int);
+    const size_t walk = (size_t)6 * N * sizeof(int) + (size_t)N * sizeof(double);
+    // with a mask, the settled walk decisions use it first
+    return masked && kSettleLds > walk ? kSettleLds : walk;
 }
 
 hipError_t launch_finish(const Plan &p, const Inputs &in, const Outputs &out,
                          const SampleInputs *smp, hipStream_t st) {
     const SampleInputs s = smp ? *smp : SampleInputs{nullptr, nullptr, nullptr};
-    const size_t lds = seq_lds_bytes(p.N, smp != nullptr);
+    const size_t lds = seq_lds_bytes(p.N, smp != nullptr, !p.full);
     // the sampled walk's LDS can exceed the default 64 KB limit of dynamic LDS
     static const hipError_t attr = [] {
-        const int most = (int)seq_lds_bytes(kMaxNodes, true);
+        const int most = (int)seq_lds_bytes(kMaxNodes, true, true);
         hipError_t e = hipFuncSetAttribute((const void *)finish_kernel<kBF16, true>,
                                            hipFuncAttributeMaxDynamicSharedMemorySize, most);
         if (e == hipSuccess)
