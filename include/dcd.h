@@ -220,9 +220,10 @@ int dcd_verify_greedy(const dcd_problem *p, const dcd_inputs *in, const dcd_outp
  * u_resample times the total.  node_stats[DCD_NODE_RATIO] is pi_CD / pi_e of the
  * node's token under its parent row (the ratio of a first sibling).
  * With plaus_thresh = 0 and at most 64 sequences, each sequence's walk is spread
- * over several workgroups of one cooperative kernel launch on hip_stream (so such a
- * call is not for stream capture); a sequence whose workgroups failed to meet gets
- * status DCD_SEQ_WALK_TIMEOUT.
+ * over several workgroups (at most one per CU, all of them resident together on a
+ * device running nothing else), which meet at barriers with bounded waits; a
+ * sequence whose workgroups failed to meet (other work holding the CUs for seconds)
+ * gets status DCD_SEQ_WALK_TIMEOUT.
  */
 int dcd_verify_sample(const dcd_problem *p, const dcd_inputs *in, const float *draft_probs,
                       const float *u_accept, const float *u_resample, const dcd_outputs *out,

@@ -127,7 +127,7 @@ int run(const dcd_problem *p, const dcd_inputs *in, const SampleInputs *smp,
                     out->row_argmax_expert, out->row_kl};
     hipStream_t st = (hipStream_t)stream;
     // untruncated sampled verification: each sequence's walk spread over a group of
-    // workgroups when they fit one cooperative launch
+    // workgroups, one per CU
     P.walk_group = smp && P.full ? walk_group_size(P, (hipStream_t)stream) : 0;
     if (normalise(P, I, st) != hipSuccess) return DCD_ERR_HIP;
     if (launch_lmhead(P, I, st) != hipSuccess) return DCD_ERR_HIP;

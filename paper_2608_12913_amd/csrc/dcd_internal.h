@@ -222,7 +222,7 @@ hipError_t launch_propose(const Plan &p, const Inputs &in, const ProposeOutputs 
 hipError_t launch_finish(const Plan &p, const Inputs &in, const Outputs &out,
                          const SampleInputs *smp, hipStream_t st);
 // untruncated sampled verification: workgroups per sequence for the spread walk
-// (0 when the sequences do not fit a cooperative launch), and that launch
+// (0 when there are too many sequences for one workgroup per CU), and that launch
 int walk_group_size(const Plan &p, hipStream_t st);
 hipError_t launch_walk(const Plan &p, const Inputs &in, const Outputs &out, const SampleInputs &smp,
                        hipStream_t st);

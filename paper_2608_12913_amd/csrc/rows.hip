@@ -1176,7 +1176,7 @@ __device__ __forceinline__ void verify_sequence(const Plan &P, const Inputs &in,
 
 // ---------------------------------------------------------------------------
 // Untruncated target, sampled verification: each sequence's walk spread over a
-// group of G workgroups (one cooperative launch, every workgroup resident).
+// group of G workgroups (one launch of at most one workgroup per CU).
 //
 // With plaus_thresh = 0 every token is in the support, so a rejection needs the
 // normaliser Z of the residual max(0, p - pi_e) over the whole vocabulary, and the
@@ -1225,7 +1225,8 @@ __device__ __forceinline__ double block_inclusive_scan(double x, int tid, double
 // Arrival at the group's barrier number k (1, 2, ...): the workgroup's writes are
 // released at agent scope, then it waits (acquire) until all G workgroups arrived.
 // The wait is bounded; a workgroup that gives up sets the group's failure flag and
-// goes on, so every workgroup ends.
+// goes on, and a workgroup that sees the flag stops waiting at once, so every
+// workgroup ends, after at most one bounded wait, even if the group never met.
 // Every wave first waits for its own stores to complete (vmcnt(0)); thread 0 then
 // releases the workgroup's writes at agent scope with its arrival and, once all
 // have arrived, acquires at agent scope for the workgroup (the caches it
@@ -1239,8 +1240,12 @@ __device__ __forceinline__ void group_barrier(int *bar, int G, int k, WalkShared
         __hip_atomic_fetch_add(bar, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
         // relaxed polling (an acquire per poll would invalidate the caches every
         // time), one acquire fence once the count is reached
+        // (the count and the failure flag are read together, as one 8-byte word)
+        const unsigned long long *word = reinterpret_cast<const unsigned long long *>(bar);
         int tries = 0;
-        while (__hip_atomic_load(bar, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < G * k) {
+        for (;;) {
+            const unsigned long long v = __hip_atomic_load(word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if ((int)(uint32_t)v >= G * k || (v >> 32) != 0) break;
             if (++tries >= (1 << 22)) {
                 __hip_atomic_store(bar + 1, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 break;
@@ -1831,15 +1836,16 @@ int walk_group_size(const Plan &p, hipStream_t st) {
     const int t = p.dtype == kBF16 ? 1 : 0;
     int fits = fits_of[dev][t].load(std::memory_order_relaxed);
     if (fits == 0) {
-        // the cooperative launch needs every workgroup resident; one per CU is asked
-        // for, so a single workgroup with the most LDS the walk uses must fit
+        // the group barrier needs every workgroup of a group resident; the launch
+        // has at most one per CU, so a single workgroup with the most LDS the walk
+        // uses must fit on a CU
         int per_cu = 0, cur = -1;
         const void *fn = t ? (const void *)walk_kernel<kBF16> : (const void *)walk_kernel<kF32>;
         if (hipGetDevice(&cur) != hipSuccess) return 0;
         if (cur != dev && hipSetDevice(dev) != hipSuccess) return 0;
         const hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, NT,
                                                                           walk_lds_bytes(kMaxNodes));
-        if (cur != dev) hipSetDevice(cur);
+        if (cur != dev) (void)hipSetDevice(cur);
         if (e != hipSuccess) return 0;
         fits = per_cu >= 1 ? 1 : 2;
         fits_of[dev][t].store(fits, std::memory_order_relaxed);
@@ -1849,14 +1855,14 @@ int walk_group_size(const Plan &p, hipStream_t st) {
 
 hipError_t launch_walk(const Plan &p, const Inputs &in, const Outputs &out, const SampleInputs &smp,
                        hipStream_t st) {
-    Plan pc = p;
-    Inputs ic = in;
-    Outputs oc = out;
-    SampleInputs sc = smp;
-    void *args[] = {&pc, &ic, &oc, &sc};
-    const void *fn = p.dtype == kBF16 ? (const void *)walk_kernel<kBF16> : (const void *)walk_kernel<kF32>;
-    return hipLaunchCooperativeKernel(fn, dim3(p.B * p.walk_group), dim3(NT), args,
-                                      (unsigned)walk_lds_bytes(p.N), st);
+    // B * G <= CUs workgroups, each of which fits on a CU (walk_group_size): on a
+    // device with nothing else running they are all resident together
+    const unsigned lds = (unsigned)walk_lds_bytes(p.N);
+    if (p.dtype == kBF16)
+        hipLaunchKernelGGL(walk_kernel<kBF16>, dim3(p.B * p.walk_group), dim3(NT), lds, st, p, in, out, smp);
+    else
+        hipLaunchKernelGGL(walk_kernel<kF32>, dim3(p.B * p.walk_group), dim3(NT), lds, st, p, in, out, smp);
+    return hipGetLastError();
 }
 
 size_t seq_lds_bytes(int N, bool sampled, bool masked) {
