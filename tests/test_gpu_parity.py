@@ -512,6 +512,39 @@ def test_sampled_tree_at_the_node_limit():
     _check_sample(case, probs, tokens, "sampled tree of 4096 nodes")
 
 
+
+def test_sampled_settled_and_walked_sequences_together():
+    """theta > 0: each row settles its children's accept ratios and its terminal draw
+    unless a node has more than 64 children, its children's proposals at its mask
+    members exceed 4096 values, or it has more than 1024 mask members; such a sequence
+    is walked in the sequence phase instead.  One call holds one sequence of each:
+    0, a star of 80 children; 1, a tree that settles; 2, a star of 40 children under a
+    root with more than 4096 / 40 mask members; 3, a chain with a row of more than 1024
+    mask members (its hidden state scaled down, flattening the expert)."""
+    N = 81
+    case = synth.make_case("s8_chain16x8", 60, B=4, N=N, tree="tree", depth=4, max_children=5,
+                           V=3000, dp=64, dq=32, theta=0.0005, dtype="f32")
+    star = np.arange(N) - 1
+    star[1:81] = 0
+    case.parents[0] = star
+    star40 = np.arange(N) - 1
+    star40[1:41] = 0
+    star40[41] = 40
+    case.parents[2] = star40
+    case.parents[3] = synth.chain_parents(N)
+    case.hp[3 * N + 3] *= np.float32(0.02)
+    rows = oracle.eval_rows(case.hp, case.hq, case.wp, case.wq, case.bias, case.bias,
+                            theta=case.theta, s=case.s, want_lpcd=True)
+    members = np.isfinite(rows["lpcd"]).sum(1).reshape(case.B, N)
+    kids = np.stack([np.bincount(case.parents[b][1:], minlength=N) for b in range(case.B)])
+    assert kids[0, 0] == 80 > 64
+    assert kids[1].max() <= 64 and members[1].max() <= 1024 and (kids[1] * members[1]).max() <= 4096
+    assert kids[2].max() <= 64 and members[2].max() <= 1024 and kids[2, 0] * members[2, 0] > 4096
+    assert members[3].max() > 1024
+    probs, tokens = _sampled_tree_setup(case)
+    g, _ = _check_sample(case, probs, tokens, "settled and walked sequences")
+    assert np.all(g["status"] == 0)
+
 # ------------------------------------------------------------------ full-size workloads
 def _spine_tokens(case, **kw):
     """Draft tokens with one full-depth path that copies the target argmax."""
