@@ -44,17 +44,21 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 // Row shape of this translation unit (lmhead128.hip includes this file with 128):
 //   64 rows:  4 waves of 64 tokens x 64 rows, 128-byte chunks (32 KB of weights in
 //             flight per workgroup), two workgroups per CU;
-//   128 rows: 8 waves of 32 tokens x 128 rows (the same 64 accumulators per wave),
-//             256-byte chunks (64 KB in flight), one workgroup per CU (its LDS).
-// Either way about 64 KB of weights is in flight per CU, and each weight byte
-// serves ROWS rows.
+//   128 rows: 4 waves of 64 tokens x 128 rows (128 accumulators per wave), 128-byte
+//             chunks, two workgroups per CU, so that one workgroup's epilogues
+//             overlap the other's stream.  Its registers are tight: the weight
+//             fragments stay put while the hidden-state fragments stream past
+//             them, and the expert pass's row statistics wait in LDS during the
+//             amateur pass.
+// Either way 64 KB of weights is in flight per CU, and each weight byte serves ROWS
+// rows.
 #ifndef DCD_STREAM_ROWS
 #define DCD_STREAM_ROWS 64
 #endif
 #if DCD_STREAM_ROWS == 64
 constexpr int NW = 4, VB = 4, CB = 128, kMinBlocks = 2;
 #elif DCD_STREAM_ROWS == 128
-constexpr int NW = 8, VB = 2, CB = 256, kMinBlocks = 1;
+constexpr int NW = 4, VB = 4, CB = 128, kMinBlocks = 2;
 #else
 #error "DCD_STREAM_ROWS must be 64 or 128"
 #endif
@@ -71,6 +75,7 @@ constexpr int HLOADS = ROWS * CB / (NT * 16);  // 16-byte hidden-state loads per
 constexpr int WTILE = VB * 16 * CB;       // bytes of one wave's weight chunk
 constexpr int HTILE = ROWS * CB;          // bytes of one hidden-state chunk
 constexpr int QX = LPR / RPI > 0 ? LPR / RPI : 1;  // distinct weight-row swizzles per lane
+constexpr bool kParkStats = ROWS > 64;    // expert row statistics kept in LDS across the amateur pass
 static_assert(HLOADS >= 1 && ROWS * CB == HLOADS * NT * 16, "hidden-state staging must tile");
 static_assert(CB % 64 == 0 && WLOADS * RPI == 16 * VB && LPR % RPI == 0 || RPI % LPR == 0,
               "weight chunk must tile");
@@ -231,14 +236,28 @@ __device__ __forceinline__ void compute(const char *hb, const char *wbuf, const 
         // one k-step at a time: hoisting every fragment read of the chunk would
         // cost KS times the fragment registers
         __builtin_amdgcn_sched_barrier(0);
-        u32x4 bfr[RB];
+        if constexpr (RB > VB) {
+            // more row blocks than token blocks: the VB weight fragments are held and
+            // each hidden-state fragment is used as it arrives
+            u32x4 wfr[VB];
 #pragma unroll
-        for (int rb = 0; rb < RB; ++rb) bfr[rb] = ld_lds(hb + a.frag[s] + 16 * rb * CB);
+            for (int vb = 0; vb < VB; ++vb) wfr[vb] = ld_lds(wbuf + a.frag[s] + 16 * vb * CB);
 #pragma unroll
-        for (int vb = 0; vb < VB; ++vb) {
-            const u32x4 x = ld_lds(wbuf + a.frag[s] + 16 * vb * CB);
+            for (int rb = 0; rb < RB; ++rb) {
+                const u32x4 y = ld_lds(hb + a.frag[s] + 16 * rb * CB);
 #pragma unroll
-            for (int rb = 0; rb < RB; ++rb) acc[vb][rb] = mma<DT>(x, bfr[rb], acc[vb][rb]);
+                for (int vb = 0; vb < VB; ++vb) acc[vb][rb] = mma<DT>(wfr[vb], y, acc[vb][rb]);
+            }
+        } else {
+            u32x4 bfr[RB];
+#pragma unroll
+            for (int rb = 0; rb < RB; ++rb) bfr[rb] = ld_lds(hb + a.frag[s] + 16 * rb * CB);
+#pragma unroll
+            for (int vb = 0; vb < VB; ++vb) {
+                const u32x4 x = ld_lds(wbuf + a.frag[s] + 16 * vb * CB);
+#pragma unroll
+                for (int rb = 0; rb < RB; ++rb) acc[vb][rb] = mma<DT>(x, bfr[rb], acc[vb][rb]);
+            }
         }
     }
 }
@@ -294,11 +313,12 @@ __device__ __forceinline__ float wave_sum16_32(float x) {
 //   bias_lds        the tile's bias already divided by T (0 without a bias)
 //   z[vb][rb][j]    logit (divided by T); -inf for tokens >= V (ragged tile only)
 //   tmax[rb], tsum[rb]   of row 16rb + lane%16
+//   keep            if given, (tmax, tsum) of row r are also left in keep[r]
 template <bool RAGGED>
 __device__ __forceinline__ void tile_softmax(const f32x4 (&acc)[VB][RB], const float *bias_lds,
                                              int V, int tok0, int wtok0, float inv_T, float2 *pairs,
                                              float (&z)[VB][RB][4], float (&tmax)[RB],
-                                             float (&tsum)[RB]) {
+                                             float (&tsum)[RB], float2 *keep = nullptr) {
     constexpr float kLog2e = 1.4426950408889634f;
     const int lane = threadIdx.x % kWaveSize, wave = threadIdx.x / kWaveSize;
     const int n = lane % 16, g = lane / 16;
@@ -349,6 +369,7 @@ __device__ __forceinline__ void tile_softmax(const f32x4 (&acc)[VB][RB], const f
             }
         }
         pairs[r] = float2{m, s};
+        if (keep) keep[r] = float2{m, s};
     }
     __syncthreads();
 #pragma unroll
@@ -375,8 +396,9 @@ static_assert(NW * ROWS * sizeof(YStat) <= (size_t)kHTiles * HTILE, "y statistic
 // expert logit of a lane's first tile-local candidate of each row block, parked
 // until the amateur epilogue decides whether the tile survives ([rb][lane] per wave)
 constexpr int kStash = RB;
+constexpr size_t kParkBytes = kParkStats ? ROWS * sizeof(float2) : 0;  // [ROWS] (pmax, psum)
 constexpr size_t kLdsBytes = kHTiles * HTILE + NW * WTILE + 2 * TS * sizeof(float) +
-                             NW * kStash * kWaveSize * sizeof(float);
+                             NW * kStash * kWaveSize * sizeof(float) + kParkBytes;
 
 template <int DT, bool RAGGED, bool FULL, bool STREAM>
 __device__ __forceinline__ void tile_body(const Plan &P, const Inputs &in, int tile, int row0,
@@ -393,6 +415,7 @@ __device__ __forceinline__ void tile_body(const Plan &P, const Inputs &in, int t
     float *bias_p = reinterpret_cast<float *>(lds + kHTiles * HTILE + NW * WTILE);  // [TS]
     float *bias_q = bias_p + TS;                                                     // [TS]
     float *stash = bias_q + TS + wave * kStash * kWaveSize;                          // [RB][64]
+    float2 *park = reinterpret_cast<float2 *>(bias_q + TS + NW * kStash * kWaveSize);  // [ROWS]
     // epilogue scratch, aliasing the hidden-state tiles (used only between passes)
     float2 *pairs = reinterpret_cast<float2 *>(lds);                       // [NW][64]
     uint32_t *twords = reinterpret_cast<uint32_t *>(pairs + NW * ROWS);   // [64][words]
@@ -422,7 +445,8 @@ __device__ __forceinline__ void tile_body(const Plan &P, const Inputs &in, int t
     // ---- expert head (the amateur stream starts before its epilogue)
     sp.issue(0, b);
     run_pass<DT, RAGGED, STREAM>(sp, &sq, b, hbuf, wbuf, a, acc);
-    tile_softmax<RAGGED>(acc, bias_p, P.V, tok0, wtok0, P.inv_T, pairs, z, pmax, psum);
+    tile_softmax<RAGGED>(acc, bias_p, P.V, tok0, wtok0, P.inv_T, pairs, z, pmax, psum,
+                         kParkStats ? park : nullptr);
     if constexpr (FULL) {
         // untruncated target: the expert logits go to the dense array for the
         // amateur epilogue (16 contiguous bytes per lane and block)
@@ -485,23 +509,29 @@ __device__ __forceinline__ void tile_body(const Plan &P, const Inputs &in, int t
 
     // ---- amateur head
     run_pass<DT, RAGGED, STREAM>(sq, nullptr, b, hbuf, wbuf, a, acc);
-    if constexpr (FULL) {
-        tile_softmax<RAGGED>(acc, bias_q, P.V, tok0, wtok0, P.inv_T, pairs, z, qmax, qsum);
-        // the lane's expert logits back from the dense array
-        float zp[VB][RB][4];
+    if constexpr (kParkStats) {  // the expert statistics back from LDS (written before the pass)
 #pragma unroll
         for (int rb = 0; rb < RB; ++rb) {
+            const float2 t = park[rb * 16 + n];
+            pmax[rb] = t.x;
+            psum[rb] = t.y;
+        }
+    }
+    if constexpr (FULL) {
+        tile_softmax<RAGGED>(acc, bias_q, P.V, tok0, wtok0, P.inv_T, pairs, z, qmax, qsum);
+        // the lane's expert logits of row block rb back from the dense array
+        auto load_zp = [&](int rb, float (&d)[VB][4]) {
             const int row = min(row0 + rb * 16 + n, P.R - 1);
 #pragma unroll
             for (int vb = 0; vb < VB; ++vb) {
                 const float4 v = *reinterpret_cast<const float4 *>(
                     P.zp_full + (size_t)row * P.zstride + tok0 + 16 * vb + 4 * g);
-                zp[vb][rb][0] = v.x;
-                zp[vb][rb][1] = v.y;
-                zp[vb][rb][2] = v.z;
-                zp[vb][rb][3] = v.w;
+                d[vb][0] = v.x;
+                d[vb][1] = v.y;
+                d[vb][2] = v.z;
+                d[vb][3] = v.w;
             }
-        }
+        };
         if (P.store_q) {  // sampled verification draws from the whole vocabulary later
 #pragma unroll
             for (int rb = 0; rb < RB; ++rb) {
@@ -522,14 +552,15 @@ __device__ __forceinline__ void tile_body(const Plan &P, const Inputs &in, int t
 #pragma unroll
         for (int rb = 0; rb < RB; ++rb) {
             YStat st{-INFINITY, -1, -INFINITY, 0.f, 0.f, 0.f, 0.f, -1};
-            float y[VB][4];
+            float y[VB][4], zp[VB][4];
+            load_zp(rb, zp);
 #pragma unroll
             for (int vb = 0; vb < VB; ++vb)
 #pragma unroll
                 for (int j = 0; j < 4; ++j) {
                     const int t = tok0 + 16 * vb + 4 * g + j;
                     const bool ok = !RAGGED || t < P.V;
-                    const float p = zp[vb][rb][j], q = z[vb][rb][j];
+                    const float p = zp[vb][j], q = z[vb][rb][j];
                     y[vb][j] = ok ? s1 * p - P.s * q : -INFINITY;
                     st.a += ok ? __builtin_amdgcn_exp2f((p - pmax[rb]) * kLog2e) * (p - q) : 0.f;
                     // the expert's own top-1: the lowest token holding the tile max
