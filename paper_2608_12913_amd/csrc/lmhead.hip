@@ -237,17 +237,21 @@ __device__ __forceinline__ void compute(const char *hb, const char *wbuf, const 
         // cost KS times the fragment registers
         __builtin_amdgcn_sched_barrier(0);
         if constexpr (RB > VB) {
-            // more row blocks than token blocks: the VB weight fragments are held and
-            // each hidden-state fragment is used as it arrives
-            u32x4 wfr[VB];
+            // more row blocks than token blocks: every fragment of the k-step is read
+            // first (the MFMAs then wait only for the ones they use), weights first
+            u32x4 wfr[VB], hfr[RB];
 #pragma unroll
             for (int vb = 0; vb < VB; ++vb) wfr[vb] = ld_lds(wbuf + a.frag[s] + 16 * vb * CB);
 #pragma unroll
-            for (int rb = 0; rb < RB; ++rb) {
-                const u32x4 y = ld_lds(hb + a.frag[s] + 16 * rb * CB);
+            for (int rb = 0; rb < RB; ++rb) hfr[rb] = ld_lds(hb + a.frag[s] + 16 * rb * CB);
 #pragma unroll
-                for (int vb = 0; vb < VB; ++vb) acc[vb][rb] = mma<DT>(wfr[vb], y, acc[vb][rb]);
-            }
+            for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+                for (int vb = 0; vb < VB; ++vb) acc[vb][rb] = mma<DT>(wfr[vb], hfr[rb], acc[vb][rb]);
+            // keep that order: left free, the scheduler sinks each read next to its
+            // first MFMA and the LDS latency is exposed between every few MFMAs
+            __builtin_amdgcn_sched_group_barrier(0x100, VB + RB, 0);  // DS reads
+            __builtin_amdgcn_sched_group_barrier(0x008, VB * RB * (DT == kBF16 ? 1 : 4), 0);  // MFMAs
         } else {
             u32x4 bfr[RB];
 #pragma unroll
