@@ -1193,6 +1193,61 @@ __device__ __forceinline__ void verify_sequence(const Plan &P, const Inputs &in,
 // token.  Each slice sum is the last entry of a fixed-order scan of its threads'
 // run sums, the same scan the draw walks, so the two agree.
 
+// The walk's current target over the vocabulary of its current row: the stored
+// residual row x (scaled by xs), or, with x null, pi_CD from the dense logits.
+struct WalkTarget {
+    const double *x;
+    double xs;
+    const float *zp, *zq;
+    float lse_p, lse_q, logZ, s;
+
+    __device__ __forceinline__ double at(int t) const {
+        if (x) return x[t] * xs;
+        return (double)__expf((1.f + s) * (zp[t] - lse_p) - s * (zq[t] - lse_q) - logZ);
+    }
+    // the weights of the 8 * NC tokens from t (t a multiple of 4) and, with q, the
+    // residuals max(0, w - q) instead: every load of the NC chunks is issued before
+    // any weight is formed, so that they are in flight together (q4: q is 16-byte
+    // aligned)
+    template <int NC>
+    __device__ __forceinline__ void chunk(int t, const float *q, bool q4, double (&w)[8 * NC]) const {
+        double xv[8 * NC];
+        float pz[8 * NC], qz[8 * NC], pr[8 * NC];
+        if (x) {
+#pragma unroll
+            for (int i = 0; i < 4 * NC; ++i) {
+                const double2 a = *reinterpret_cast<const double2 *>(x + t + 2 * i);
+                xv[2 * i] = a.x;
+                xv[2 * i + 1] = a.y;
+            }
+        } else {
+#pragma unroll
+            for (int i = 0; i < 2 * NC; ++i) {
+                const float4 a = *reinterpret_cast<const float4 *>(zp + t + 4 * i);
+                const float4 c = *reinterpret_cast<const float4 *>(zq + t + 4 * i);
+                pz[4 * i] = a.x, pz[4 * i + 1] = a.y, pz[4 * i + 2] = a.z, pz[4 * i + 3] = a.w;
+                qz[4 * i] = c.x, qz[4 * i + 1] = c.y, qz[4 * i + 2] = c.z, qz[4 * i + 3] = c.w;
+            }
+        }
+        if (q4) {
+#pragma unroll
+            for (int i = 0; i < 2 * NC; ++i) {
+                const float4 a = *reinterpret_cast<const float4 *>(q + t + 4 * i);
+                pr[4 * i] = a.x, pr[4 * i + 1] = a.y, pr[4 * i + 2] = a.z, pr[4 * i + 3] = a.w;
+            }
+        } else if (q) {
+#pragma unroll
+            for (int i = 0; i < 8 * NC; ++i) pr[i] = q[t + i];
+        }
+#pragma unroll
+        for (int i = 0; i < 8 * NC; ++i) {
+            const double cur = x ? xv[i] * xs
+                                 : (double)__expf((1.f + s) * (pz[i] - lse_p) - s * (qz[i] - lse_q) - logZ);
+            w[i] = q ? fmax(0.0, cur - (double)pr[i]) : cur;
+        }
+    }
+};
+
 struct WalkShared {
     double wave_tot[NT / kWaveSize];
     double dval, dval2;
@@ -1326,6 +1381,7 @@ __global__ __launch_bounds__(NT) void walk_kernel(Plan P, Inputs in, Outputs out
     double xs = 0.0;               // its normaliser 1/Z
     int cur = 0, len = 0, nbar = 0;
     bool last_pass_applied = false;  // the slice sums of the last pass are the current weights
+    double last_rs = 0.0;            // this thread's run sum in the last pass
     const float *rj = nullptr;
     float lse_p = 0.f, lse_q = 0.f, logZ = 0.f;
     const float *zp = nullptr, *zq = nullptr;
@@ -1338,67 +1394,38 @@ __global__ __launch_bounds__(NT) void walk_kernel(Plan P, Inputs in, Outputs out
         zq = P.zq_full + (r0 + j) * P.zstride;
     };
     set_row(0);
-    // weight of token t under the walk's current target
-    auto weight = [&](int t) -> double {
-        if (xcur) return xcur[t] * xs;
-        return (double)__expf((1.f + P.s) * (zp[t] - lse_p) - P.s * (zq[t] - lse_q) - logZ);
+    auto current_target = [&]() {
+        return WalkTarget{xcur, xs, zp, zq, lse_p, lse_q, logZ, P.s};
     };
     // one pass over this thread's run: with q, the residual max(0, w - q) is stored
-    // to xout; returns the run's sum in token order.  Whole chunks of 8 tokens (the
-    // run starts at a multiple of 4) issue all their loads before any weight is
-    // formed: 16-byte loads of the dense or stored rows, and of the proposal row
-    // where it is 16-byte aligned.
+    // to xout; returns the run's sum, added in token order.  Groups of four chunks
+    // of 8 tokens (the run starts at a multiple of 4), then single chunks, then the
+    // partial last chunk.
     auto run_sum = [&](const float *q, double *xout) -> double {
+        const WalkTarget wt = current_target();
         double sum = 0.0;
         const bool q4 = q && (reinterpret_cast<uintptr_t>(q) & 15) == 0;
         int t = t0;
+        for (; t + 32 <= t1; t += 32) {
+            double w[32];
+            wt.chunk<4>(t, q, q4, w);
+#pragma unroll
+            for (int i = 0; i < 32; i += 2)
+                if (q) *reinterpret_cast<double2 *>(xout + t + i) = double2{w[i], w[i + 1]};
+#pragma unroll
+            for (int i = 0; i < 32; ++i) sum += w[i];
+        }
         for (; t + 8 <= t1; t += 8) {
-            double xv[8];
-            float pz[8], qz[8], pr[8];
-            if (xcur) {
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const double2 a = *reinterpret_cast<const double2 *>(xcur + t + 2 * i);
-                    xv[2 * i] = a.x;
-                    xv[2 * i + 1] = a.y;
-                }
-            } else {
-#pragma unroll
-                for (int i = 0; i < 2; ++i) {
-                    const float4 a = *reinterpret_cast<const float4 *>(zp + t + 4 * i);
-                    const float4 c = *reinterpret_cast<const float4 *>(zq + t + 4 * i);
-                    pz[4 * i] = a.x, pz[4 * i + 1] = a.y, pz[4 * i + 2] = a.z, pz[4 * i + 3] = a.w;
-                    qz[4 * i] = c.x, qz[4 * i + 1] = c.y, qz[4 * i + 2] = c.z, qz[4 * i + 3] = c.w;
-                }
-            }
-            if (q4) {
-#pragma unroll
-                for (int i = 0; i < 2; ++i) {
-                    const float4 a = *reinterpret_cast<const float4 *>(q + t + 4 * i);
-                    pr[4 * i] = a.x, pr[4 * i + 1] = a.y, pr[4 * i + 2] = a.z, pr[4 * i + 3] = a.w;
-                }
-            } else if (q) {
-#pragma unroll
-                for (int i = 0; i < 8; ++i) pr[i] = q[t + i];
-            }
             double w[8];
+            wt.chunk<1>(t, q, q4, w);
 #pragma unroll
-            for (int i = 0; i < 8; ++i) {
-                const double cur = xcur ? xv[i] * xs
-                                        : (double)__expf((1.f + P.s) * (pz[i] - lse_p) -
-                                                         P.s * (qz[i] - lse_q) - logZ);
-                w[i] = q ? fmax(0.0, cur - (double)pr[i]) : cur;
-            }
-            if (q) {
-#pragma unroll
-                for (int i = 0; i < 4; ++i)
-                    *reinterpret_cast<double2 *>(xout + t + 2 * i) = double2{w[2 * i], w[2 * i + 1]};
-            }
+            for (int i = 0; i < 8; i += 2)
+                if (q) *reinterpret_cast<double2 *>(xout + t + i) = double2{w[i], w[i + 1]};
 #pragma unroll
             for (int i = 0; i < 8; ++i) sum += w[i];
         }
         for (; t < t1; ++t) {  // the run's last, partial chunk
-            double w = weight(t);
+            double w = wt.at(t);
             if (q) {
                 w = fmax(0.0, w - (double)q[t]);
                 xout[t] = w;
@@ -1462,7 +1489,8 @@ __global__ __launch_bounds__(NT) void walk_kernel(Plan P, Inputs in, Outputs out
         // rejected: the residual max(0, p - pi_e^(c)), stored and summed slice by slice
         double *xout = xcur == xrow0 ? xrow1 : xrow0;
         double tot_all;
-        block_inclusive_scan(run_sum(smp.draft_probs + (r0 + c) * V, xout), tid, &tot_all, ws);
+        last_rs = run_sum(smp.draft_probs + (r0 + c) * V, xout);
+        block_inclusive_scan(last_rs, tid, &tot_all, ws);
         const double total = exchange(tot_all);
         if (total > 0.0) {  // applied; a zero residual (rounding only) leaves p as it was
             xcur = xout;
@@ -1480,7 +1508,8 @@ __global__ __launch_bounds__(NT) void walk_kernel(Plan P, Inputs in, Outputs out
         xs = 1.0;
     } else {
         double tot_all;
-        block_inclusive_scan(run_sum(nullptr, nullptr), tid, &tot_all, ws);
+        last_rs = run_sum(nullptr, nullptr);
+        block_inclusive_scan(last_rs, tid, &tot_all, ws);
         exchange(tot_all);
     }
     const double *sums = part + ((nbar - 1) % 2) * kWalkMaxGroup;
@@ -1506,9 +1535,11 @@ __global__ __launch_bounds__(NT) void walk_kernel(Plan P, Inputs in, Outputs out
     const double slice_before = ws.dval;
     __syncthreads();
     if (m == slice) {
-        // this workgroup's slice: the thread whose run crosses the target scans it
+        // this workgroup's slice: the thread whose run crosses the target scans it.
+        // The run sums are those of the last pass, which summed the current weights
+        // (as stored, when that pass was an applied rejection, which is why xs is 1)
         const double target = (double)u * total;
-        const double rs = run_sum(nullptr, nullptr);
+        const double rs = last_rs;
         double tot_all;
         const double incl = block_inclusive_scan(rs, tid, &tot_all, ws);
         const double start = slice_before + incl - rs;
@@ -1525,15 +1556,32 @@ __global__ __launch_bounds__(NT) void walk_kernel(Plan P, Inputs in, Outputs out
             who = ws.ival[1];
         }
         if (tid == who) {
+            // the run's weights in groups (loads in flight together), added in order
+            const WalkTarget wt = current_target();
             double run = start;
-            int found = -1, lastpos = -1;
-            for (int t = t0; t < t1 && found < 0; ++t) {
-                const double w = weight(t);
-                run += w;
-                if (w > 0.0) {
-                    lastpos = t;
-                    if (run > target) found = t;
+            int found = -1, lastpos = -1, t = t0;
+            auto scan = [&](const double *w, int n, int at) {
+                for (int i = 0; i < n && found < 0; ++i) {
+                    run += w[i];
+                    if (w[i] > 0.0) {
+                        lastpos = at + i;
+                        if (run > target) found = at + i;
+                    }
                 }
+            };
+            for (; t + 32 <= t1 && found < 0; t += 32) {
+                double w[32];
+                wt.chunk<4>(t, nullptr, false, w);
+                scan(w, 32, t);
+            }
+            for (; t + 8 <= t1 && found < 0; t += 8) {
+                double w[8];
+                wt.chunk<1>(t, nullptr, false, w);
+                scan(w, 8, t);
+            }
+            for (; t < t1 && found < 0; ++t) {
+                const double w = wt.at(t);
+                scan(&w, 1, t);
             }
             out.next_token[b] = found >= 0 ? found : lastpos;
         }
