@@ -201,6 +201,7 @@ struct Smem {
                         //   members in token order (token, cd score) packed (kMembers)
     int mcount;         // sampled, masked: the row's mask members (more than kMembers: not kept)
     float mlogz;        //   and its log Z
+    int nkids;          //   and its node's children (the first kMaxKids listed in LDS)
     float4 nodez;       // the row's draft token under its parent row (waves 1-3)
     int node_ok;        // nodez is to be written
     int wave_tot[NT / kWaveSize];
@@ -1602,6 +1603,38 @@ __global__ __launch_bounds__(NT) void walk_kernel(Plan P, Inputs in, Outputs out
 // ---------------------------------------------------------------------------
 // Masked target, sampled verification: the walk's decisions at a node, settled by
 // the node's own row workgroup before the sequence phase.
+
+// The children of node i (later nodes whose parent is i) in index order, with their
+// tokens (clamped into the vocabulary: a token outside it fails the sequence later)
+// and their proposal probability of their own token: kids, ktok and kq in LDS (the
+// first kMaxKids of them), their number in sm.nkids.  One wave, which runs it while
+// wave 0 takes the row phase (it needs only the inputs); lane l scans a contiguous
+// range of the later nodes, a wave scan orders them.
+__device__ __forceinline__ void gather_children(const Plan &P, const Inputs &in, const SampleInputs &smp,
+                                                int row, int lane, Smem &sm, int *dyn) {
+    const int N = P.N, V = P.V, i = row % N;
+    const size_t r0 = (size_t)row - i;
+    int *kids = dyn, *ktok = dyn + kMaxKids;
+    float *kq = reinterpret_cast<float *>(dyn + 2 * kMaxKids);
+    const int per = (N - 1 - i + kWaveSize - 1) / kWaveSize;
+    const int c0 = i + 1 + lane * per, c1 = min(N, c0 + per);
+    int mine = 0;
+    for (int c = c0; c < c1; ++c) mine += in.parents[r0 + c] == i;
+    int m;
+    int k = wave_exclusive_scan(mine, lane, &m);
+    if (mine > 0)
+        for (int c = c0; c < c1; ++c)
+            if (in.parents[r0 + c] == i) {
+                if (k < kMaxKids) {
+                    const int x = min(max(in.tokens[r0 + c], 0), V - 1);
+                    kids[k] = c;
+                    ktok[k] = x;
+                    kq[k] = smp.draft_probs[(r0 + c) * V + x];
+                }
+                ++k;
+            }
+    if (lane == 0) sm.nkids = m;
+}
 //
 // At node i the walk (Alg. 1 over a tree) tries i's children in index order; when
 // it reaches child c every earlier child of i has been rejected, so what it does at
@@ -1630,31 +1663,12 @@ __device__ __forceinline__ void settle_children(const Plan &P, const Inputs &in,
     const unsigned long long *mlist = reinterpret_cast<const unsigned long long *>(sm.wts);
     const int L = sm.mcount;
     const float logZ = sm.mlogz;
-    // the children of node i (all later nodes), in index order: each thread takes a
-    // contiguous range of the later nodes
-    const int per = (N - 1 - i + NT - 1) / NT;
-    const int c0 = i + 1 + tid * per, c1 = min(N, c0 + per);
-    int mine = 0;
-    for (int c = c0; c < c1; ++c) mine += in.parents[r0 + c] == i;
-    int m;
-    const int first = group_exclusive_scan(mine, tid, &m, sm);
+    // the children of node i in index order, listed by gather_children
+    const int m = sm.nkids;
     const bool ok = L <= kMembers && m <= kMaxKids && (size_t)m * (size_t)L <= (size_t)kKidQ;
-    if (ok) {
-        if (mine > 0) {
-            int k = first;
-            for (int c = c0; c < c1; ++c)
-                if (in.parents[r0 + c] == i) {
-                    // a token outside the vocabulary fails the sequence later; read in range
-                    const int x = min(max(in.tokens[r0 + c], 0), V - 1);
-                    kids[k] = c;
-                    ktok[k] = x;
-                    kq[k] = smp.draft_probs[(r0 + c) * V + x];
-                    ++k;
-                }
-        }
-        // the target over the support (the row phase's cd scores, in token order)
+    // the target over the support (the row phase's cd scores, in token order)
+    if (ok)
         for (int t = tid; t < L; t += NT) w[t] = (double)__expf(__uint_as_float((uint32_t)mlist[t]) - logZ);
-    }
     __syncthreads();
     if (ok)  // every child's proposal over the support, gathered in one round
         for (int e = tid; e < m * L; e += NT)
@@ -1743,6 +1757,8 @@ __global__ __launch_bounds__(NT) void finish_kernel(Plan P, Inputs in, Outputs o
     if (SAMPLE && P.walk_group && row % P.N == 0 && tid < 2) P.walkbar[(row / P.N) * 2 + tid] = 0;
     __syncthreads();
     combine_row<DT>(P, in, out, row, tid % kWaveSize, tid / kWaveSize, sm, SAMPLE && !P.full);
+    // sampled, masked: wave 1 lists the node's children while wave 0 takes the row phase
+    if (SAMPLE && !P.full && tid / kWaveSize == 1) gather_children(P, in, smp, row, tid % kWaveSize, sm, dyn);
     // count the row once all of its waves are done; thread 0 stores the node's
     // logits, and the release half of the counting atomic publishes them together
     // with wave 0's results and the settled walk decisions (the workgroup barrier
