@@ -20,8 +20,8 @@
 // one of two LDS tiles.  Both tiles are XOR-swizzled (16-byte column c of row m
 // at slot c ^ (m mod LPR)) so fragment reads of 16 lanes hit distinct bank
 // groups.  One batch of loads is in flight per wave; the amateur head's first
-// batch is issued before the expert epilogue, so the stream does not stop
-// between the two heads.
+// batch is issued before the expert epilogue (64 rows), so the stream does not
+// stop between the two heads.
 //
 // Epilogue.  Per (row, tile): the tile max and sum of exp of both models, and
 // the plausibility candidates: tokens whose expert logit is within ln(theta)
@@ -448,7 +448,9 @@ __device__ __forceinline__ void tile_body(const Plan &P, const Inputs &in, int t
 
     // ---- expert head (the amateur stream starts before its epilogue)
     sp.issue(0, b);
-    run_pass<DT, RAGGED, STREAM>(sp, &sq, b, hbuf, wbuf, a, acc);
+    // (the 128-row shape issues the amateur stream's first batch only after the expert
+    // epilogue: held across it, its registers push that epilogue into spills)
+    run_pass<DT, RAGGED, STREAM>(sp, kParkStats ? nullptr : &sq, b, hbuf, wbuf, a, acc);
     tile_softmax<RAGGED>(acc, bias_p, P.V, tok0, wtok0, P.inv_T, pairs, z, pmax, psum,
                          kParkStats ? park : nullptr);
     if constexpr (FULL) {
@@ -512,6 +514,7 @@ __device__ __forceinline__ void tile_body(const Plan &P, const Inputs &in, int t
     }
 
     // ---- amateur head
+    if constexpr (kParkStats) sq.issue(0, b);
     run_pass<DT, RAGGED, STREAM>(sq, nullptr, b, hbuf, wbuf, a, acc);
     if constexpr (kParkStats) {  // the expert statistics back from LDS (written before the pass)
 #pragma unroll
