@@ -441,6 +441,10 @@ __device__ __forceinline__ void tile_body(const Plan &P, const Inputs &in, int t
 
     f32x4 acc[VB][RB];
     float z[VB][RB][4];
+    // untruncated target, 64 rows: the expert logits stay in registers across the
+    // amateur pass (the 128-row shape has no room: it stores and reloads them)
+    constexpr bool kKeepZp = !kParkStats;
+    float zpk[kKeepZp ? VB : 1][RB][4];
     float pmax[RB], psum[RB], qmax[RB], qsum[RB];
     uint32_t flags[RB];  // bit (vb*4 + j): tile-local candidate
     bool pruning = false;  // the row bounds of this call are usable
@@ -454,16 +458,27 @@ __device__ __forceinline__ void tile_body(const Plan &P, const Inputs &in, int t
     tile_softmax<RAGGED>(acc, bias_p, P.V, tok0, wtok0, P.inv_T, pairs, z, pmax, psum,
                          kParkStats ? park : nullptr);
     if constexpr (FULL) {
-        // untruncated target: the expert logits go to the dense array for the
-        // amateur epilogue (16 contiguous bytes per lane and block)
-#pragma unroll
-        for (int rb = 0; rb < RB; ++rb) {
-            const int row = row0 + rb * 16 + n;
-            if (row >= P.R) continue;
+        // untruncated target: the expert logits go to the dense array (16 contiguous
+        // bytes per lane and block) where a later kernel reads them (sampled calls,
+        // proposals) or where the amateur epilogue does (128 rows); 64 rows keep them
+        if constexpr (kKeepZp) {
 #pragma unroll
             for (int vb = 0; vb < VB; ++vb)
-                *reinterpret_cast<float4 *>(P.zp_full + (size_t)row * P.zstride + tok0 + 16 * vb + 4 * g) =
-                    float4{z[vb][rb][0], z[vb][rb][1], z[vb][rb][2], z[vb][rb][3]};
+#pragma unroll
+                for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) zpk[vb][rb][j] = z[vb][rb][j];
+        }
+        if (!kKeepZp || P.store_q) {
+#pragma unroll
+            for (int rb = 0; rb < RB; ++rb) {
+                const int row = row0 + rb * 16 + n;
+                if (row >= P.R) continue;
+#pragma unroll
+                for (int vb = 0; vb < VB; ++vb)
+                    *reinterpret_cast<float4 *>(P.zp_full + (size_t)row * P.zstride + tok0 + 16 * vb + 4 * g) =
+                        float4{z[vb][rb][0], z[vb][rb][1], z[vb][rb][2], z[vb][rb][3]};
+            }
         }
     } else {
         // tile-local candidates: z_p within ln(theta) of the tile max (bit vb*4+j of
@@ -526,8 +541,15 @@ __device__ __forceinline__ void tile_body(const Plan &P, const Inputs &in, int t
     }
     if constexpr (FULL) {
         tile_softmax<RAGGED>(acc, bias_q, P.V, tok0, wtok0, P.inv_T, pairs, z, qmax, qsum);
-        // the lane's expert logits of row block rb back from the dense array
+        // the lane's expert logits of row block rb: kept, or back from the dense array
         auto load_zp = [&](int rb, float (&d)[VB][4]) {
+            if constexpr (kKeepZp) {
+#pragma unroll
+                for (int vb = 0; vb < VB; ++vb)
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) d[vb][j] = zpk[vb % (kKeepZp ? VB : 1)][rb][j];
+                return;
+            }
             const int row = min(row0 + rb * 16 + n, P.R - 1);
 #pragma unroll
             for (int vb = 0; vb < VB; ++vb) {

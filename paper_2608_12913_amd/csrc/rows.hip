@@ -309,14 +309,25 @@ __device__ __forceinline__ void combine_row(const Plan &P, const Inputs &in, con
         const size_t rowj = (size_t)(row - i + j);
         const size_t esz = DT == kBF16 ? 2 : 4;
         // the three parts go to the three waves, so their loads are in flight together
-        if (P.full) {  // every token is in the support; the expert logit is stored densely
+        if (P.full) {  // every token is in the support
+            if (P.store_q) {  // both models' logits are stored densely (sampled calls)
+                if (wave == 1 && lane == 0) {
+                    sm.nodez.x = sm.nodez.z = P.zp_full[rowj * P.zstride + x];
+                    sm.nodez.y = sm.nodez.w = P.zq_full[rowj * P.zstride + x];
+                    sm.node_ok = 1;
+                }
+                return;
+            }
+            // greedy: the logits are not stored (or only the expert's, by the 128-row
+            // shape); the node's are needed only for its statistics
             if (wave == 1 && lane == 0) {
-                const float zp = P.zp_full[rowj * P.zstride + x];
-                sm.nodez.x = sm.nodez.z = zp;
-                if (P.store_q) sm.nodez.y = sm.nodez.w = P.zq_full[rowj * P.zstride + x];
-                else if (!want_node_logits) sm.nodez.y = sm.nodez.w = 0.f;
+                if (!want_node_logits) sm.nodez = float4{0.f, 0.f, 0.f, 0.f};
                 sm.node_ok = 1;
-            } else if (wave == 3 && !P.store_q && want_node_logits) {
+            } else if (wave == 2 && want_node_logits) {
+                float zp = wave_dot<DT>((const char *)in.hp + rowj * P.dp * esz,
+                                        (const char *)in.wp + (size_t)x * P.dp * esz, P.dp, lane);
+                if (lane == 0) sm.nodez.x = sm.nodez.z = (zp + (in.bp ? in.bp[x] : 0.f)) * P.inv_T;
+            } else if (wave == 3 && want_node_logits) {
                 float zq = wave_dot<DT>((const char *)in.hq + rowj * P.dq * esz,
                                         (const char *)in.wq + (size_t)x * P.dq * esz, P.dq, lane);
                 if (lane == 0) sm.nodez.y = sm.nodez.w = (zq + (in.bq ? in.bq[x] : 0.f)) * P.inv_T;
