@@ -202,9 +202,9 @@ size_t workspace_layout(Plan &p, char *base) {
     // first, at the same place for every problem: the call count and ready word
     p.ctl = (uint32_t *)take(2 * sizeof(uint32_t));
     p.partials = (float4 *)take(R * p.ntiles * sizeof(float4));
-    if (p.full) {  // dense logits of both models, per-tile statistics of y
-        p.zp_full = (float *)take(R * (size_t)p.zstride * sizeof(float));
-        p.zq_full = (float *)take(R * (size_t)p.zstride * sizeof(float));
+    if (p.full) {  // dense y (and, for the 128-row shape, expert logits), per-tile statistics of y
+        p.zp_full = p.rows_blk == kStreamRowsLarge ? (float *)take(R * (size_t)p.zstride * sizeof(float)) : nullptr;
+        p.y_full = (float *)take(R * (size_t)p.zstride * sizeof(float));
         p.ypart = (float4 *)take(R * p.ntiles * 2 * sizeof(float4));
         p.resbuf = (double *)take((size_t)p.B * 2 * p.zstride * sizeof(double));
         p.walkbar = (int *)take((size_t)p.B * 2 * sizeof(int));

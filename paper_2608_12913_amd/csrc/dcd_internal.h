@@ -51,8 +51,10 @@ struct Plan {
     float2 *cand;      // [R][V]        (z_p, z_q) of candidate tokens (sparse)
     uint32_t *bits;    // [R][wstride]  candidate bitmap
     // untruncated target (full = 1)
-    float *zp_full;    // [R][zstride]  expert logits (divided by T)
-    float *zq_full;    // [R][zstride]  amateur logits (divided by T)
+    float *zp_full;    // [R][zstride]  expert logits (divided by T), where the 128-row shape keeps
+                       //   them between its two passes
+    float *y_full;     // [R][zstride]  sampled and proposal calls: y = (1+s) z_p - s z_q (logits
+                       //   divided by T), so pi_CD(t) = exp(y(t) - target_shift(row))
     double *resbuf;    // [B][2][zstride] sampled verification: the residual after the
                        //   last applied rejection of the walk's current node (two rows)
     float4 *ypart;     // [R][ntiles][2] per tile, over y = (1+s) z_p - s z_q:
@@ -169,6 +171,12 @@ __device__ __forceinline__ bool await_call_state(const uint32_t *ctl) {
 
 // The call's last kernel advances the call count (one thread of one workgroup).
 __device__ __forceinline__ void advance_call(uint32_t *ctl) { ctl[0] = ctl[0] + 1; }
+
+// Untruncated target: log pi_CD(t) = y(t) - shift, with y = (1+s) z_p - s z_q and
+// shift = (1+s) lse_p - s lse_q + log Z of the row (cd = y - (1+s) lse_p + s lse_q).
+__device__ __forceinline__ float target_shift(const float *rowinfo_row, float s) {
+    return (1.f + s) * rowinfo_row[RI_LSEP] - s * rowinfo_row[RI_LSEQ] + rowinfo_row[RI_LOGZ];
+}
 
 // Untruncated target: statistics of y = (1+s) z_p - s z_q over a set of tokens.
 // cd = y - (1+s) lse_p + s lse_q, so the argmax, margin and log-normaliser of the

@@ -458,9 +458,9 @@ __device__ __forceinline__ void tile_body(const Plan &P, const Inputs &in, int t
     tile_softmax<RAGGED>(acc, bias_p, P.V, tok0, wtok0, P.inv_T, pairs, z, pmax, psum,
                          kParkStats ? park : nullptr);
     if constexpr (FULL) {
-        // untruncated target: the expert logits go to the dense array (16 contiguous
-        // bytes per lane and block) where a later kernel reads them (sampled calls,
-        // proposals) or where the amateur epilogue does (128 rows); 64 rows keep them
+        // untruncated target: 64 rows keep the expert logits in registers; 128 rows
+        // store them to the dense array (16 contiguous bytes per lane and block) for
+        // their amateur epilogue
         if constexpr (kKeepZp) {
 #pragma unroll
             for (int vb = 0; vb < VB; ++vb)
@@ -469,7 +469,7 @@ __device__ __forceinline__ void tile_body(const Plan &P, const Inputs &in, int t
 #pragma unroll
                     for (int j = 0; j < 4; ++j) zpk[vb][rb][j] = z[vb][rb][j];
         }
-        if (!kKeepZp || P.store_q) {
+        if constexpr (!kKeepZp) {
 #pragma unroll
             for (int rb = 0; rb < RB; ++rb) {
                 const int row = row0 + rb * 16 + n;
@@ -561,17 +561,6 @@ __device__ __forceinline__ void tile_body(const Plan &P, const Inputs &in, int t
                 d[vb][3] = v.w;
             }
         };
-        if (P.store_q) {  // sampled verification draws from the whole vocabulary later
-#pragma unroll
-            for (int rb = 0; rb < RB; ++rb) {
-                const int row = row0 + rb * 16 + n;
-                if (row >= P.R) continue;
-#pragma unroll
-                for (int vb = 0; vb < VB; ++vb)
-                    *reinterpret_cast<float4 *>(P.zq_full + (size_t)row * P.zstride + tok0 + 16 * vb + 4 * g) =
-                        float4{z[vb][rb][0], z[vb][rb][1], z[vb][rb][2], z[vb][rb][3]};
-            }
-        }
         // per row: statistics of y over the lane's tokens (ascending, so a strict
         // comparison keeps the lowest id on ties), merged over the wave's lanes of
         // that row and then over the waves in order
@@ -604,6 +593,14 @@ __device__ __forceinline__ void tile_body(const Plan &P, const Inputs &in, int t
                         st.y2 = fmaxf(st.y2, y[vb][j]);
                     }
                 }
+            // sampled calls and proposals read y densely later (the walk's passes, the
+            // proposal rows): 16 contiguous bytes per lane and block
+            if (P.store_q && row0 + rb * 16 + n < P.R) {
+#pragma unroll
+                for (int vb = 0; vb < VB; ++vb)
+                    *reinterpret_cast<float4 *>(P.y_full + (size_t)(row0 + rb * 16 + n) * P.zstride + tok0 +
+                                                16 * vb + 4 * g) = float4{y[vb][0], y[vb][1], y[vb][2], y[vb][3]};
+            }
             if (st.i1 >= 0) {
                 const float ml = st.y1 * kLog2e;
 #pragma unroll

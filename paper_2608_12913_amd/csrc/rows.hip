@@ -310,24 +310,17 @@ __device__ __forceinline__ void combine_row(const Plan &P, const Inputs &in, con
         const size_t esz = DT == kBF16 ? 2 : 4;
         // the three parts go to the three waves, so their loads are in flight together
         if (P.full) {  // every token is in the support
-            if (P.store_q) {  // both models' logits are stored densely (sampled calls)
-                if (wave == 1 && lane == 0) {
-                    sm.nodez.x = sm.nodez.z = P.zp_full[rowj * P.zstride + x];
-                    sm.nodez.y = sm.nodez.w = P.zq_full[rowj * P.zstride + x];
-                    sm.node_ok = 1;
-                }
-                return;
-            }
-            // greedy: the logits are not stored (or only the expert's, by the 128-row
-            // shape); the node's are needed only for its statistics
+            // the logits are not stored densely (only y, for sampled calls): the node's,
+            // needed for the sampled walk and for its statistics, are dot products
+            const bool need = want_node_logits || P.store_q;
             if (wave == 1 && lane == 0) {
-                if (!want_node_logits) sm.nodez = float4{0.f, 0.f, 0.f, 0.f};
+                if (!need) sm.nodez = float4{0.f, 0.f, 0.f, 0.f};
                 sm.node_ok = 1;
-            } else if (wave == 2 && want_node_logits) {
+            } else if (wave == 2 && need) {
                 float zp = wave_dot<DT>((const char *)in.hp + rowj * P.dp * esz,
                                         (const char *)in.wp + (size_t)x * P.dp * esz, P.dp, lane);
                 if (lane == 0) sm.nodez.x = sm.nodez.z = (zp + (in.bp ? in.bp[x] : 0.f)) * P.inv_T;
-            } else if (wave == 3 && want_node_logits) {
+            } else if (wave == 3 && need) {
                 float zq = wave_dot<DT>((const char *)in.hq + rowj * P.dq * esz,
                                         (const char *)in.wq + (size_t)x * P.dq * esz, P.dq, lane);
                 if (lane == 0) sm.nodez.y = sm.nodez.w = (zq + (in.bq ? in.bq[x] : 0.f)) * P.inv_T;
@@ -763,9 +756,8 @@ __device__ __forceinline__ int masked_scan(const Plan &P, size_t jrow, const Res
 __device__ __forceinline__ int full_scan(const Plan &P, size_t jrow, const Residual &res, bool draw, float u,
                          double *total_out, int tid, Smem &sm, bool reuse = false) {
     constexpr int kUnroll = 8;
-    const float *rj = P.rowinfo + jrow * kRowInfo;
-    const float lse_p = rj[RI_LSEP], lse_q = rj[RI_LSEQ], logZ = rj[RI_LOGZ];
-    const float *zp = P.zp_full + jrow * P.zstride, *zq = P.zq_full + jrow * P.zstride;
+    const float shift = target_shift(P.rowinfo + jrow * kRowInfo, P.s);
+    const float *yrow = P.y_full + jrow * P.zstride;
     const int lane = tid % kWaveSize, wave = tid / kWaveSize;
     constexpr int NW = NT / kWaveSize;
     const int k = 4 * max(1, (P.V + 4 * kList * kWaveSize - 1) / (4 * kList * kWaveSize));
@@ -777,7 +769,7 @@ __device__ __forceinline__ int full_scan(const Plan &P, size_t jrow, const Resid
     // the raw inputs of tokens t .. t+3: loads clamped into the rows (the dense and
     // stored rows have zstride entries, the proposal rows V), values past the
     // vocabulary discarded by weigh4
-    // (lo, hi: z_p and z_q of the 4 tokens, or their 4 stored doubles)
+    // (lo: y of the 4 tokens; or lo, hi: their 4 stored doubles)
     struct Raw4 {
         uint4 lo, hi;
         float4 qn;
@@ -788,8 +780,8 @@ __device__ __forceinline__ int full_scan(const Plan &P, size_t jrow, const Resid
             r.lo = *reinterpret_cast<const uint4 *>(res.x + tl);
             r.hi = *reinterpret_cast<const uint4 *>(res.x + tl + 2);
         } else {
-            r.lo = *reinterpret_cast<const uint4 *>(zp + tl);
-            r.hi = *reinterpret_cast<const uint4 *>(zq + tl);
+            r.lo = *reinterpret_cast<const uint4 *>(yrow + tl);
+            r.hi = uint4{0u, 0u, 0u, 0u};
         }
         if (res.qnext) {
             if (q4) {
@@ -803,17 +795,14 @@ __device__ __forceinline__ int full_scan(const Plan &P, size_t jrow, const Resid
         }
     };
     auto weigh4 = [&](int t, const Raw4 &r, double (&w)[4]) {
-        const float zpv[4] = {__uint_as_float(r.lo.x), __uint_as_float(r.lo.y), __uint_as_float(r.lo.z),
-                              __uint_as_float(r.lo.w)};
-        const float zqv[4] = {__uint_as_float(r.hi.x), __uint_as_float(r.hi.y), __uint_as_float(r.hi.z),
-                              __uint_as_float(r.hi.w)};
+        const float yv[4] = {__uint_as_float(r.lo.x), __uint_as_float(r.lo.y), __uint_as_float(r.lo.z),
+                             __uint_as_float(r.lo.w)};
         const float qn[4] = {r.qn.x, r.qn.y, r.qn.z, r.qn.w};
         auto dbl = [](uint32_t l, uint32_t h) { return __hiloint2double((int)h, (int)l); };
         const double xv[4] = {dbl(r.lo.x, r.lo.y), dbl(r.lo.z, r.lo.w), dbl(r.hi.x, r.hi.y), dbl(r.hi.z, r.hi.w)};
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            double v = res.x ? xv[i] * res.xs
-                             : (double)__expf((1.f + P.s) * (zpv[i] - lse_p) - P.s * (zqv[i] - lse_q) - logZ);
+            double v = res.x ? xv[i] * res.xs : (double)__expf(yv[i] - shift);
             if (res.qnext) v = fmax(0.0, v - (double)qn[i]);
             w[i] = t + i < P.V ? v : 0.0;
         }
@@ -1206,16 +1195,17 @@ __device__ __forceinline__ void verify_sequence(const Plan &P, const Inputs &in,
 // run sums, the same scan the draw walks, so the two agree.
 
 // The walk's current target over the vocabulary of its current row: the stored
-// residual row x (scaled by xs), or, with x null, pi_CD from the dense logits.
+// residual row x (scaled by xs), or, with x null, pi_CD = exp(y - shift) from the
+// row's dense y.
 struct WalkTarget {
     const double *x;
     double xs;
-    const float *zp, *zq;
-    float lse_p, lse_q, logZ, s;
+    const float *y;
+    float shift;
 
     __device__ __forceinline__ double at(int t) const {
         if (x) return x[t] * xs;
-        return (double)__expf((1.f + s) * (zp[t] - lse_p) - s * (zq[t] - lse_q) - logZ);
+        return (double)__expf(y[t] - shift);
     }
     // the weights of the 8 * NC tokens from t (t a multiple of 4) and, with q, the
     // residuals max(0, w - q) instead: every load of the NC chunks is issued before
@@ -1224,7 +1214,7 @@ struct WalkTarget {
     template <int NC>
     __device__ __forceinline__ void chunk(int t, const float *q, bool q4, double (&w)[8 * NC]) const {
         double xv[8 * NC];
-        float pz[8 * NC], qz[8 * NC], pr[8 * NC];
+        float yz[8 * NC], pr[8 * NC];
         if (x) {
 #pragma unroll
             for (int i = 0; i < 4 * NC; ++i) {
@@ -1235,10 +1225,8 @@ struct WalkTarget {
         } else {
 #pragma unroll
             for (int i = 0; i < 2 * NC; ++i) {
-                const float4 a = *reinterpret_cast<const float4 *>(zp + t + 4 * i);
-                const float4 c = *reinterpret_cast<const float4 *>(zq + t + 4 * i);
-                pz[4 * i] = a.x, pz[4 * i + 1] = a.y, pz[4 * i + 2] = a.z, pz[4 * i + 3] = a.w;
-                qz[4 * i] = c.x, qz[4 * i + 1] = c.y, qz[4 * i + 2] = c.z, qz[4 * i + 3] = c.w;
+                const float4 a = *reinterpret_cast<const float4 *>(y + t + 4 * i);
+                yz[4 * i] = a.x, yz[4 * i + 1] = a.y, yz[4 * i + 2] = a.z, yz[4 * i + 3] = a.w;
             }
         }
         if (q4) {
@@ -1253,8 +1241,7 @@ struct WalkTarget {
         }
 #pragma unroll
         for (int i = 0; i < 8 * NC; ++i) {
-            const double cur = x ? xv[i] * xs
-                                 : (double)__expf((1.f + s) * (pz[i] - lse_p) - s * (qz[i] - lse_q) - logZ);
+            const double cur = x ? xv[i] * xs : (double)__expf(yz[i] - shift);
             w[i] = q ? fmax(0.0, cur - (double)pr[i]) : cur;
         }
     }
@@ -1394,20 +1381,15 @@ __global__ __launch_bounds__(NT) void walk_kernel(Plan P, Inputs in, Outputs out
     int cur = 0, len = 0, nbar = 0;
     bool last_pass_applied = false;  // the slice sums of the last pass are the current weights
     double last_rs = 0.0;            // this thread's run sum in the last pass
-    const float *rj = nullptr;
-    float lse_p = 0.f, lse_q = 0.f, logZ = 0.f;
-    const float *zp = nullptr, *zq = nullptr;
+    float shift = 0.f;
+    const float *yrow = nullptr;
     auto set_row = [&](int j) {
-        rj = P.rowinfo + (r0 + j) * kRowInfo;
-        lse_p = rj[RI_LSEP];
-        lse_q = rj[RI_LSEQ];
-        logZ = rj[RI_LOGZ];
-        zp = P.zp_full + (r0 + j) * P.zstride;
-        zq = P.zq_full + (r0 + j) * P.zstride;
+        shift = target_shift(P.rowinfo + (r0 + j) * kRowInfo, P.s);
+        yrow = P.y_full + (r0 + j) * P.zstride;
     };
     set_row(0);
     auto current_target = [&]() {
-        return WalkTarget{xcur, xs, zp, zq, lse_p, lse_q, logZ, P.s};
+        return WalkTarget{xcur, xs, yrow, shift};
     };
     // one pass over this thread's run: with q, the residual max(0, w - q) is stored
     // to xout; returns the run's sum, added in token order.  Groups of four chunks
@@ -1829,12 +1811,11 @@ __global__ __launch_bounds__(NT) void propose_probs_kernel(Plan P, float *probs,
     const float thr = rj[RI_THRESH], lse_p = rj[RI_LSEP], lse_q = rj[RI_LSEQ], logZ = rj[RI_LOGZ];
     float v[4] = {0.f, 0.f, 0.f, 0.f};
     if constexpr (FULL) {
-        // the dense logit rows are padded to whole tiles, so the loads stay inside the row
-        const float4 p = *reinterpret_cast<const float4 *>(P.zp_full + (size_t)row * P.zstride + t0);
-        const float4 q = *reinterpret_cast<const float4 *>(P.zq_full + (size_t)row * P.zstride + t0);
-        const float zp[4] = {p.x, p.y, p.z, p.w}, zq[4] = {q.x, q.y, q.z, q.w};
+        // the dense y rows are padded to whole tiles, so the load stays inside the row
+        const float4 yv = *reinterpret_cast<const float4 *>(P.y_full + (size_t)row * P.zstride + t0);
+        const float shift = target_shift(rj, P.s), y[4] = {yv.x, yv.y, yv.z, yv.w};
 #pragma unroll
-        for (int i = 0; i < 4; ++i) v[i] = __expf((1.f + P.s) * (zp[i] - lse_p) - P.s * (zq[i] - lse_q) - logZ);
+        for (int i = 0; i < 4; ++i) v[i] = __expf(y[i] - shift);
     } else {
         // bitmap words are valid only in tiles that kept candidates; the 4 tokens
         // share a tile and a word (t0 is a multiple of 4)
