@@ -171,12 +171,12 @@ typedef struct {                 /* device pointers, written by the call        
  * with final_norm = 1 it includes the normalised copies of h_* (B*N*(d_p + d_q)
  * elements).
  * The workspace holds per-tile softmax partials, the candidate logits that may
- * fall inside the plausibility mask (theta > 0) or both models' dense logits
- * (theta = 0, where every token is in the support, plus two rows of V doubles per
- * sequence for the residuals of sampled verification), and per-row results; it is
- * O(B*N*V) bytes (about 8.1 bytes per row and vocabulary entry).  The size depends
- * on the problem, so a workspace sized for one problem may be too small for
- * another.
+ * fall inside the plausibility mask (theta > 0) or, with theta = 0 (every token in
+ * the support), a dense row of y = (1+s) z_p - s z_q per row (the expert logits as
+ * well from 65 to 511 rows) and two rows of V doubles per sequence for the
+ * residuals of sampled verification, and per-row results; it is O(B*N*V) bytes
+ * (at most about 8.1 bytes per row and vocabulary entry).  The size depends on the
+ * problem, so a workspace sized for one problem may be too small for another.
  */
 size_t dcd_workspace_bytes(const dcd_problem *p);
 
