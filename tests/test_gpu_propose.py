@@ -73,6 +73,18 @@ def test_propose_drafter_heads_ragged(theta, T):
     _check(case, u, f"drafter heads theta {theta} T {T}")
 
 
+@pytest.mark.parametrize("theta", [0.0, 0.1])
+def test_propose_128_row_shape(theta):
+    """96 rows: the 128-row LM-head shape (the untruncated one keeps the dense expert
+    row for its own amateur epilogue and writes the y rows the proposals are read
+    from), with a ragged row block."""
+    rng = np.random.default_rng(64)
+    case = synth.make_case("s8_chain16x8", 64, B=12, N=8, V=3001, dp=256, dq=128, theta=theta)
+    case.wp, case.wq = _drafter_heads(case, rng)
+    u = rng.random(case.R).astype(np.float32)
+    _check(case, u, f"128-row shape theta {theta}")
+
+
 def test_propose_fp32_ragged_k():
     case = synth.make_case("tiny_chain8", 61, N=19, V=777, dp=100, dq=36, theta=0.02)
     u = np.random.default_rng(61).random(case.R).astype(np.float32)
