@@ -152,6 +152,36 @@ __device__ __forceinline__ void clear_call_state(const uint32_t *ctl, uint32_t *
 
 // Called by every thread of a workgroup (contains a barrier); true once the bounds
 // of this call are cleared, false if the wait gave up.
+// The same in two halves, so that the first reads travel while the caller works:
+// thread 0 reads the call count and the ready word (start_call_state), and later
+// checks them, polls on if the word is not there yet, and shares the outcome with
+// the workgroup (finish_call_state, which every thread calls).
+struct CallState {
+    uint32_t want, seen;
+};
+__device__ __forceinline__ CallState start_call_state(const uint32_t *ctl) {
+    CallState c{0u, 0u};
+    if (threadIdx.x == 0) {
+        c.want = ctl[0] + 1;
+        c.seen = __hip_atomic_load(ctl + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    return c;
+}
+__device__ __forceinline__ bool finish_call_state(const uint32_t *ctl, CallState c) {
+    __shared__ int ok;
+    if (threadIdx.x == 0) {
+        int tries = 0;
+        while (c.seen != c.want && ++tries < (1 << 16)) {
+            __builtin_amdgcn_s_sleep(8);
+            c.seen = __hip_atomic_load(ctl + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+        ok = tries < (1 << 16);
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    }
+    __syncthreads();
+    return ok != 0;
+}
+
 __device__ __forceinline__ bool await_call_state(const uint32_t *ctl) {
     __shared__ int ok;
     if (threadIdx.x == 0) {

@@ -455,6 +455,11 @@ __device__ __forceinline__ void tile_body(const Plan &P, const Inputs &in, int t
     // (the 128-row shape issues the amateur stream's first batch only after the expert
     // epilogue: held across it, its registers push that epilogue into spills)
     run_pass<DT, RAGGED, STREAM>(sp, kParkStats ? nullptr : &sq, b, hbuf, wbuf, a, acc);
+    // (masked) this call's row bounds are cleared by workgroup 0, long done by now:
+    // the reads that confirm it travel during the softmax
+    CallState cs{};
+    if constexpr (!FULL) cs = start_call_state(P.ctl);
+    __builtin_amdgcn_sched_barrier(0);
     tile_softmax<RAGGED>(acc, bias_p, P.V, tok0, wtok0, P.inv_T, pairs, z, pmax, psum,
                          kParkStats ? park : nullptr);
     if constexpr (FULL) {
@@ -486,8 +491,7 @@ __device__ __forceinline__ void tile_body(const Plan &P, const Inputs &in, int t
         // block waits in its LDS slot; most tiles are pruned at the end, and global
         // stores issued here would delay the amateur stream's first loads behind
         // them.  Further candidates of a row block (rare) are stored at once.
-        // The row bounds of this call are cleared by workgroup 0 (long done by now).
-        pruning = await_call_state(P.ctl);
+        pruning = finish_call_state(P.ctl, cs);
         bool over = false;
 #pragma unroll
         for (int rb = 0; rb < RB; ++rb) {
