@@ -51,7 +51,7 @@ int make_plan(const dcd_problem *p, bool sample, Plan &P) {
     // ln(theta) in double, rounded once; theta = 0 switches the mask off
     P.log_theta = p->plaus_thresh > 0.f ? (float)log((double)p->plaus_thresh) : -INFINITY;
     P.full = p->plaus_thresh == 0.f;
-    P.store_q = P.full && sample;
+    P.store_y = P.full && sample;
     P.zstride = P.ntiles * kTileTokens;
     P.s = p->cd_strength;
     P.inv_T = sample ? (float)(1.0 / (double)p->temperature) : 1.f;

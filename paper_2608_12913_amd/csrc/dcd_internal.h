@@ -42,7 +42,7 @@ struct Plan {
     int full;          // plaus_thresh = 0: the untruncated target (every token in the support);
                        // no candidates, dense logits instead
     int zstride;       // ntiles * kTileTokens: row stride of the dense logit arrays
-    int store_q;       // full and sampled: the amateur logits are kept for the draw
+    int store_y;       // full, and sampled or proposing: the dense y rows are written (y_full)
     int final_norm;    // the rows of h_* are normalised first (into hn_p, hn_q)
     float norm_eps;
     // workspace carve-up

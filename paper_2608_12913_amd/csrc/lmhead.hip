@@ -599,7 +599,7 @@ __device__ __forceinline__ void tile_body(const Plan &P, const Inputs &in, int t
                 }
             // sampled calls and proposals read y densely later (the walk's passes, the
             // proposal rows): 16 contiguous bytes per lane and block
-            if (P.store_q && row0 + rb * 16 + n < P.R) {
+            if (P.store_y && row0 + rb * 16 + n < P.R) {
 #pragma unroll
                 for (int vb = 0; vb < VB; ++vb)
                     *reinterpret_cast<float4 *>(P.y_full + (size_t)(row0 + rb * 16 + n) * P.zstride + tok0 +

@@ -312,7 +312,7 @@ __device__ __forceinline__ void combine_row(const Plan &P, const Inputs &in, con
         if (P.full) {  // every token is in the support
             // the logits are not stored densely (only y, for sampled calls): the node's,
             // needed for the sampled walk and for its statistics, are dot products
-            const bool need = want_node_logits || P.store_q;
+            const bool need = want_node_logits || P.store_y;
             if (wave == 1 && lane == 0) {
                 if (!need) sm.nodez = float4{0.f, 0.f, 0.f, 0.f};
                 sm.node_ok = 1;
