@@ -81,7 +81,11 @@ __device__ __forceinline__ void lds_barrier() {
     asm volatile("" ::: "memory");
 }
 
-__device__ __forceinline__ u32x4 ld16(const char *p) { return *reinterpret_cast<const u32x4 *>(p); }
+// The wave's index, known to the compiler as uniform: the row bases computed from it
+// then sit in scalar registers and every load takes the scalar-base form (a 32-bit
+// lane offset), instead of a 64-bit address per lane and load instruction.
+__device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane(threadIdx.x / kWaveSize); }
+
 __device__ __forceinline__ void st_lds(char *p, u32x4 v) { *reinterpret_cast<u32x4 *>(p) = v; }
 __device__ __forceinline__ u32x4 ld_lds(const char *p) { return *reinterpret_cast<const u32x4 *>(p); }
 
@@ -114,7 +118,7 @@ struct Stream {
 
     __device__ __forceinline__ void init(const void *h, const void *w, int d, int R, int V, int row0,
                                          int tile0) {
-        const int lane = threadIdx.x % kWaveSize, wave = threadIdx.x / kWaveSize;
+        const int lane = threadIdx.x % kWaveSize, wave = wave_id();
         r = lane / LPR;
         col16 = (lane % LPR) ^ (r % LPR);  // the slot's column (slab rows start at multiples of LPR)
         rowbytes = (uint32_t)d * 2;
@@ -133,7 +137,7 @@ struct Stream {
     // re-reads the row's last 16 bytes (finite values); the hidden-state slots there
     // are zeroed after arrival (zero_tail).
     __device__ __forceinline__ void dma(int c, char *st) const {
-        const int wave = threadIdx.x / kWaveSize;
+        const int wave = wave_id();
         const uint32_t col = (uint32_t)c * CB + col16 * 16;
         const uint32_t kcol = col < rowbytes ? col : rowbytes - 16;
         char *wdst = st + SLAB * wave * CB, *hdst = st + OPB + SLAB * wave * CB;
@@ -156,7 +160,7 @@ struct Stream {
     // 512 bytes of `sink`, which nothing reads.  Past the last chunk it re-reads the
     // last one.
     __device__ __forceinline__ void prefetch(int c, char *sink) const {
-        const int lane = threadIdx.x % kWaveSize, wave = threadIdx.x / kWaveSize;
+        const int lane = threadIdx.x % kWaveSize, wave = wave_id();
         const uint32_t col = min((uint32_t)c * CB, rowbytes - 16);
         const char *ws = RAGGED ? wbase + (uint32_t)(min(wskip + lane, wlast) * rowbytes + col)
                                 : wbase + (uint32_t)(lane * rowbytes + col);
@@ -172,16 +176,13 @@ struct Stream {
     // weights there multiply zeros.
     __device__ __forceinline__ void zero_tail(int c, char *st) const {
         if ((uint32_t)(c + 1) * CB <= rowbytes) return;  // workgroup-uniform
-        const int lane = threadIdx.x % kWaveSize, wave = threadIdx.x / kWaveSize;
+        const int lane = threadIdx.x % kWaveSize, wave = wave_id();
         if ((uint32_t)c * CB + col16 * 16 < rowbytes) return;
         char *hdst = st + OPB + SLAB * wave * CB + lane * 16;
 #pragma unroll
         for (int q = 0; q < LOADS; ++q) st_lds(hdst + q * RPI * CB, u32x4{0u, 0u, 0u, 0u});
     }
 };
-
-// 16-byte column c of row m of a swizzled [256][CB] operand tile
-__device__ __forceinline__ int swz(int m, int c) { return m * CB + ((c ^ (m % LPR)) << 4); }
 
 // The wave's 128 x 128 block over one staged chunk.  A = weights (tokens as M),
 // B = hidden states (rows as N); lane l supplies row l%16 of a block and K columns
@@ -314,7 +315,7 @@ template <bool RAGGED>
 __device__ __forceinline__ void wide_tile(const Plan &P, const Inputs &in, int tile, int row0, char *s0,
                                           char *s1, float *misc, char *sink) {
     const int tid = threadIdx.x, lane = tid % kWaveSize;
-    const int wave = __builtin_amdgcn_readfirstlane(tid / kWaveSize);
+    const int wave = wave_id();
     const int wt = wave & 1, wr = wave >> 1;
     const int n = lane % 16, g = lane / 16;
     const int tile0 = tile * TT;
