@@ -102,6 +102,14 @@ def test_mask_and_strength_settings(theta, s):
     _check_greedy(case, tokens, f"theta={theta} s={s}", theta=theta, s=s)
 
 
+@pytest.mark.parametrize("theta,s", [(1.0, 0.5), (0.1, 0.0), (0.3, 2.0), (0.001, 1.0)])
+def test_mask_and_strength_settings_many_rows(theta, s):
+    # 576 rows: the many-row LM-head kernel under every mask width and strength
+    case = synth.make_case("b8_batch32x64", 12, B=9, V=2000, dp=256, dq=128)
+    tokens = _greedy_tokens(case, theta=theta, s=s)
+    _check_greedy(case, tokens, f"many rows theta={theta} s={s}", theta=theta, s=s)
+
+
 @pytest.mark.parametrize("seed", range(2))
 def test_untruncated_target_ragged(seed):
     # theta = 0: every token is in the support (dense-logit path); 16 full tiles + 3
@@ -163,6 +171,34 @@ def test_exact_integer_logits_theta_one():
     assert np.array_equal(g["row_argmax_expert"], o["row_diag"][:, oracle.RD_ARGMAX_P])
 
 
+def test_exact_integer_logits_many_rows():
+    """The same exactness through the many-row LM-head kernel: 9 sequences of 64 nodes
+    (576 rows, the last 256-row tile ragged), a ragged vocabulary, two K chunks of the
+    expert rows and one of the amateur rows.  The theta = 1 mask (the tokens tied at the
+    expert max), the argmax, the expert max and the walk must match exactly."""
+    rng = np.random.default_rng(15)
+    V = 3001
+    case = synth.make_case("b8_batch32x64", 15, B=9, V=V, dp=128, dq=64)
+    assert case.R == 576
+    for name, d in (("hp", 128), ("hq", 64)):
+        setattr(case, name, synth.bf16_bits(rng.integers(-2, 3, (case.R, d)).astype(np.float32)))
+    case.wp = synth.bf16_bits(rng.integers(-1, 2, (V, 128)).astype(np.float32))
+    case.wq = synth.bf16_bits(rng.integers(-1, 2, (V, 64)).astype(np.float32))
+    case.bias[:] = 0
+    tokens = _greedy_tokens(case, theta=1.0)
+    _say("exact integer logits, many rows")
+    o = _oracle_greedy(case, tokens, theta=1.0)
+    g = _runner().from_case(case, tokens, theta=1.0).run("greedy")
+    assert np.array_equal(g["row_argmax"], o["row_argmax"])
+    assert np.array_equal(g["row_stats"][:, oracle.RS_COUNT], o["row_stats"][:, oracle.RS_COUNT])
+    assert np.array_equal(g["accept_len"], o["accept_len"])
+    assert np.array_equal(g["accept_path"], o["accept_path"])
+    np.testing.assert_allclose(g["row_stats"][:, oracle.RS_MAXP], o["row_stats"][:, oracle.RS_MAXP],
+                               rtol=0, atol=0)
+    assert np.array_equal(g["row_argmax_expert"], o["row_diag"][:, oracle.RD_ARGMAX_P])
+    assert (o["accept_len"] > 0).sum() >= 6, "most sequences must accept along their spine"
+
+
 def test_exact_integer_logits_untruncated_expert_top1():
     """theta = 0 with exact integer logits: many tokens tie at the expert max across
     vocabulary tiles; the expert's top-1 is the lowest of them, merged over tiles."""
@@ -208,11 +244,16 @@ def test_sequence_status_codes():
     _check_greedy(case, tokens, "status codes")
 
 
-@pytest.mark.parametrize("which", ["separate", "none"])
-def test_bias_variants(which):
+@pytest.mark.parametrize("which,rows", [("separate", "few"), ("none", "few"), ("separate", "many"),
+                                        ("none", "many")])
+def test_bias_variants(which, rows):
     # one bias per model (the amateur's differs from the expert's), or none at all
-    # (null pointers: both models' logits unbiased)
-    case = synth.make_case("b8_tree64", 70, N=20, depth=4, max_children=4, V=1500, dp=128, dq=64)
+    # (null pointers: both models' logits unbiased); "many": 576 rows, through the
+    # many-row LM-head kernel
+    if rows == "few":
+        case = synth.make_case("b8_tree64", 70, N=20, depth=4, max_children=4, V=1500, dp=128, dq=64)
+    else:
+        case = synth.make_case("b8_batch32x64", 71, B=9, V=1500, dp=128, dq=64)
     zero = np.zeros(case.V, np.float32)
     if which == "separate":
         bp, bq = case.bias, (0.5 * case.bias - 0.25).astype(np.float32)
@@ -222,7 +263,7 @@ def test_bias_variants(which):
     oq = bq if bq is not None else zero
     rows = oracle.eval_rows(case.hp, case.hq, case.wp, case.wq, op, oq, theta=case.theta, s=case.s)
     tokens = synth.greedy_tokens(case, rows["argmax"])
-    _say(f"bias {which}: B={case.B} N={case.N} V={case.V}")
+    _say(f"bias {which}: B={case.B} N={case.N} V={case.V} R={case.R}")
     o = oracle.verify("greedy", case.B, case.N, case.hp, case.hq, case.wp, case.wq, op, oq,
                       case.parents, tokens, theta=case.theta, s=case.s)
     g = _runner().from_case(case, tokens, bias_p=bp, bias_q=bq).run("greedy")
@@ -678,16 +719,19 @@ def test_full_b8_batch32x64(theta):
 
 @pytest.mark.slow
 @pytest.mark.parametrize("workload,mode,theta", [("b8_tree64", "greedy", 0.1), ("s8_chain16x8", "sample", 0.1),
-                                                 ("b8_tree64", "sample", 0.1), ("b8_tree64", "sample", 0.0)])
+                                                 ("b8_tree64", "sample", 0.1), ("b8_tree64", "sample", 0.0),
+                                                 ("b8_batch32x64", "greedy", 0.1)])
 def test_full_size_repeated_calls_are_bit_identical(workload, mode, theta):
     """Which vocabulary tiles keep their candidates depends on when each reads the
     running bound; the outputs must not.  Full-size calls (64 rows: one row block per
-    tile; 128 rows: the 128-row shape, 501 tiles on 256 CUs in two rounds) repeated
-    with another call of a different problem in between, every output compared bit
-    for bit."""
+    tile; 128 rows: the 128-row shape, 501 tiles on 256 CUs in two rounds; 2048 rows:
+    the many-row kernel) repeated with another call of a different problem in between,
+    every output compared bit for bit."""
     case = synth.make_case(workload, 0, mode=mode, theta=theta)
     if mode == "sample":
         probs, tokens = _full_sampled_setup(case)
+    elif case.R > 512:  # the coin rule with every token uniform: no oracle rows needed
+        probs, tokens = None, synth.greedy_tokens(case, np.full(case.R, -1, np.int32))
     else:
         probs, tokens = None, _spine_tokens(case)
     _say(f"{workload} {mode}: repeated calls")
