@@ -482,6 +482,18 @@ def test_sampled_trees_small(seed, theta, s):
          f"accept lengths {g['accept_len'].tolist()}")
 
 
+@pytest.mark.parametrize("seed,theta,s", [(3, 0.1, 0.5), (4, 0.3, 1.0)])
+def test_sampled_trees_many_rows(seed, theta, s):
+    """Sampled verification of 9 trees of 64 nodes (576 rows): the many-row LM-head
+    kernel feeding the walk decisions settled per row."""
+    case = synth.make_case("s8_chain16x8", 40 + seed, B=9, N=64, tree="tree", depth=6,
+                           max_children=4, V=2500, dp=256, dq=128, theta=theta, s=s)
+    assert case.R == 576 and case.dtype == "bf16"
+    probs, tokens = _sampled_tree_setup(case)
+    g, o = _check_sample(case, probs, tokens, f"sampled trees, many rows, seed {seed}")
+    _say(f"sampled trees, many rows, seed {seed}: accept lengths {g['accept_len'].tolist()}")
+
+
 @pytest.mark.parametrize("theta", [0.1, 0.0])
 def test_sampled_trees_odd_node_count(theta):
     # 23 nodes per sequence: the walk's per-node LDS state at an odd count
