@@ -90,6 +90,14 @@ def test_many_rows_ragged(seed):
     _check_greedy(case, _greedy_tokens(case), f"many rows seed {seed}")
 
 
+def test_many_rows_tiny_hidden_and_vocabulary():
+    # the many-row kernel's extreme tails: 8- and 24-element rows (one K chunk, most of
+    # it past the row end) and a vocabulary of one full tile plus one token
+    case = synth.make_case("b8_batch32x64", 33, B=9, V=257, dp=8, dq=24)
+    assert case.R == 576
+    _check_greedy(case, _greedy_tokens(case), "many rows, tiny rows and vocabulary")
+
+
 def test_ragged_fp32():
     case = synth.make_case("tiny_chain8", 8, N=19, V=777, dp=100, dq=36)
     _check_greedy(case, _greedy_tokens(case), "ragged fp32")

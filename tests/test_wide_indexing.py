@@ -53,6 +53,6 @@ def _check(R, V, d):
 
 
 @pytest.mark.parametrize("R,V,d", [(576, 4099, 512), (576, 4099, 200), (640, 4099, 200),
-                                   (512, 300, 64), (513, 257, 8), (2049, 128256, 256)])
+                                   (512, 300, 64), (513, 257, 8), (576, 257, 24), (2049, 128256, 256)])
 def test_ragged_load_addresses_stay_in_bounds(R, V, d):
     assert _check(R, V, d) > 0
