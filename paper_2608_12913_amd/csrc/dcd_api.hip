@@ -57,8 +57,8 @@ int make_plan(const dcd_problem *p, bool sample, Plan &P) {
     P.inv_T = sample ? (float)(1.0 / (double)p->temperature) : 1.f;
     // from 65 to 511 rows the streaming kernel takes 128 rows per workgroup, so a
     // weight byte is streamed once for each 128 rows (10% faster at 128 rows); from
-    // 512 rows the many-row kernel takes a masked bf16 problem, and the others keep
-    // 64-row workgroups, two per CU (7% faster than 128 rows at 2048 untruncated rows)
+    // 512 rows the many-row kernel takes a bf16 problem, and fp32 ones keep 64-row
+    // workgroups, two per CU
     P.rows_blk = P.R > kStreamRowsSmall && P.R < kWideMinRows ? kStreamRowsLarge : kStreamRowsSmall;
     P.nrb = (P.R + P.rows_blk - 1) / P.rows_blk;
     const long long groups = (long long)((P.ntiles + 7) / 8) * 8 * P.nrb;

@@ -242,7 +242,7 @@ hipError_t launch_rmsnorm(const Plan &p, const Inputs &in, hipStream_t st);
 hipError_t launch_lmhead(const Plan &p, const Inputs &in, hipStream_t st);
 // advances the workspace's call count (after an LM-head launch no other kernel follows)
 hipError_t launch_advance_call(const Plan &p, hipStream_t st);
-// the many-row variant (bf16, masked target, R >= kWideMinRows): same outputs
+// the many-row variant (bf16, R >= kWideMinRows): same outputs
 bool use_wide_lmhead(const Plan &p);
 hipError_t launch_lmhead_wide(const Plan &p, const Inputs &in, hipStream_t st);
 // the streaming LM-head kernel in its two row shapes (p.rows_blk selects)

@@ -453,6 +453,145 @@ __device__ __forceinline__ void wide_tile(const Plan &P, const Inputs &in, int t
     }
 }
 
+// Untruncated target (no mask): the same two passes.  The expert epilogue leaves the
+// lane's expert logits in the dense y rows (16 contiguous bytes per lane and token
+// block); the amateur epilogue reads them back, forms y = (1+s) z_p - s z_q, keeps per
+// (row, tile) the statistics of y (best and second-best y, its token, the sum of
+// exp(y - best), z_p and z_q at the best token), the expert's own top-1 and the weight
+// sum(exp(z_p - tile max) (z_p - z_q)) of D_KL(pi_p || pi_q), and overwrites the dense
+// rows with y when they are wanted (sampled verification, proposals).  The two token
+// halves of a row are merged in token order through LDS.
+__device__ __forceinline__ YStat ystat_shfl_xor(const YStat &x, int m) {
+    return YStat{__shfl_xor(x.y1, m), __shfl_xor(x.i1, m), __shfl_xor(x.y2, m), __shfl_xor(x.ys, m),
+                 __shfl_xor(x.zp1, m), __shfl_xor(x.zq1, m), __shfl_xor(x.a, m), __shfl_xor(x.ip, m)};
+}
+
+template <bool RAGGED>
+__device__ __forceinline__ void wide_tile_full(const Plan &P, const Inputs &in, int tile, int row0, char *s0,
+                                               char *s1, float *misc, char *sink) {
+    constexpr float kLog2e = 1.4426950408889634f;
+    const int tid = threadIdx.x, lane = tid % kWaveSize;
+    const int wave = wave_id();
+    const int wt = wave & 1, wr = wave >> 1;
+    const int n = lane % 16, g = lane / 16;
+    const int tile0 = tile * TT;
+    const int tok0 = tile0 + wt * WT;  // first token of the wave's half
+
+    float *bias_p = misc;                                          // [TT]
+    float *bias_q = bias_p + TT;                                   // [TT]
+    float2 *pairs = reinterpret_cast<float2 *>(s0);                // [2][TR]
+    YStat *ys = reinterpret_cast<YStat *>(s0 + kPairsBytes);       // [2][TR]: the two token halves
+    static_assert(kPairsBytes + 2 * TR * sizeof(YStat) <= kStageBytes, "y statistics must fit stage 0");
+
+    if (tid < TT) {
+        const int t = tile0 + tid;
+        bias_p[tid] = (t < P.V && in.bp) ? in.bp[t] * P.inv_T : 0.f;
+        bias_q[tid] = (t < P.V && in.bq) ? in.bq[t] * P.inv_T : 0.f;
+    }
+
+    Stream<RAGGED> sp, sq;
+    sp.init(in.hp, in.wp, P.dp, P.R, P.V, row0, tile0);
+    sq.init(in.hq, in.wq, P.dq, P.R, P.V, row0, tile0);
+    f32x4 acc[BV][BR];
+    float pmax[BR], psum[BR], qmax[BR], qsum[BR];
+
+    // ---- expert head
+    sp.dma(0, s0);
+    sp.prefetch(1, sink);
+    run_pass<RAGGED>(sp, s0, s1, sink, wt, wr, acc);
+    sq.dma(0, s1);
+    sq.prefetch(1, sink);
+    const float *bias = bias_p + wt * WT;
+    tile_softmax<RAGGED>(acc, bias, P.inv_T, tok0, P.V, wt, wr, pairs, pmax, psum);
+#pragma unroll
+    for (int rb = 0; rb < BR; ++rb) {
+        const int row = row0 + wr * WR + rb * 16 + n;
+        if (row >= P.R) continue;
+        float z[BV][4];
+        block_logits<RAGGED>(acc, rb, bias, P.inv_T, tok0, P.V, z);
+        float *dst = P.y_full + (size_t)row * P.zstride + tok0 + 4 * g;
+#pragma unroll
+        for (int vb = 0; vb < BV; ++vb)
+            *reinterpret_cast<float4 *>(dst + 16 * vb) = float4{z[vb][0], z[vb][1], z[vb][2], z[vb][3]};
+    }
+
+    // ---- amateur head
+    run_pass<RAGGED>(sq, s1, s0, sink, wt, wr, acc);
+    bias = bias_q + wt * WT;
+    tile_softmax<RAGGED>(acc, bias, P.inv_T, tok0, P.V, wt, wr, pairs, qmax, qsum);
+    const float s1f = 1.f + P.s;
+#pragma unroll
+    for (int rb = 0; rb < BR; ++rb) {
+        const int rloc = wr * WR + rb * 16 + n, row = row0 + rloc;
+        float *yrow = P.y_full + (size_t)min(row, P.R - 1) * P.zstride + tok0 + 4 * g;
+        float zq[BV][4], zp[BV][4];
+        block_logits<RAGGED>(acc, rb, bias, P.inv_T, tok0, P.V, zq);
+#pragma unroll
+        for (int vb = 0; vb < BV; ++vb) {
+            const float4 v = *reinterpret_cast<const float4 *>(yrow + 16 * vb);
+            zp[vb][0] = v.x;
+            zp[vb][1] = v.y;
+            zp[vb][2] = v.z;
+            zp[vb][3] = v.w;
+        }
+        // the lane's tokens in ascending order, so a strict comparison keeps the
+        // lowest id on ties
+        YStat st{-INFINITY, -1, -INFINITY, 0.f, 0.f, 0.f, 0.f, -1};
+        float y[BV][4];
+#pragma unroll
+        for (int vb = 0; vb < BV; ++vb)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int t = tok0 + 16 * vb + 4 * g + j;
+                const bool ok = !RAGGED || t < P.V;
+                const float p = zp[vb][j], q = zq[vb][j];
+                y[vb][j] = ok ? s1f * p - P.s * q : -INFINITY;
+                st.a += ok ? __builtin_amdgcn_exp2f((p - pmax[rb]) * kLog2e) * (p - q) : 0.f;
+                st.ip = (ok && st.ip < 0 && p == pmax[rb]) ? t : st.ip;
+                if (ok && y[vb][j] > st.y1) {
+                    st.y2 = st.y1;
+                    st.y1 = y[vb][j];
+                    st.i1 = t;
+                    st.zp1 = p;
+                    st.zq1 = q;
+                } else if (ok) {
+                    st.y2 = fmaxf(st.y2, y[vb][j]);
+                }
+            }
+        if (P.store_y && row < P.R) {
+#pragma unroll
+            for (int vb = 0; vb < BV; ++vb)
+                *reinterpret_cast<float4 *>(yrow + 16 * vb) = float4{y[vb][0], y[vb][1], y[vb][2], y[vb][3]};
+        }
+        if (st.i1 >= 0) {
+            const float ml = st.y1 * kLog2e;
+#pragma unroll
+            for (int vb = 0; vb < BV; ++vb)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) st.ys += __builtin_amdgcn_exp2f(fmaf(y[vb][j], kLog2e, -ml));
+        }
+        st = ystat_merge(st, ystat_shfl_xor(st, 16));
+        st = ystat_merge(st, ystat_shfl_xor(st, 32));
+        if (g == 0) ys[wt * TR + rloc] = st;
+    }
+    __syncthreads();
+    // per (row, tile): the y statistics of the two halves merged in token order, and
+    // the softmax partials of both models
+    if (wt == 0 && g == 0) {
+#pragma unroll
+        for (int rb = 0; rb < BR; ++rb) {
+            const int rloc = wr * WR + rb * 16 + n, row = row0 + rloc;
+            if (row >= P.R) continue;
+            const YStat st = ystat_merge(ys[rloc], ys[TR + rloc]);
+            float4 *dst = P.ypart + ((size_t)row * P.ntiles + tile) * 2;
+            dst[0] = float4{st.y1, st.ys, st.y2, st.a};
+            dst[1] = float4{__int_as_float(st.i1), st.zp1, st.zq1, __int_as_float(st.ip)};
+            P.partials[(size_t)row * P.ntiles + tile] = float4{pmax[rb], psum[rb], qmax[rb], qsum[rb]};
+        }
+    }
+}
+
+template <bool FULL>
 __global__ __launch_bounds__(NT, 1) void lmhead_wide_kernel(Plan P, Inputs in) {
     __shared__ __align__(16) char stage0[kStageBytes];
     __shared__ __align__(16) char stage1[kStageBytes];
@@ -468,20 +607,31 @@ __global__ __launch_bounds__(NT, 1) void lmhead_wide_kernel(Plan P, Inputs in) {
     const int tile = (local / nrt) * 8 + xcd;
     if (tile >= P.ntiles) return;
     const int row0 = (local % nrt) * TR;
-    if ((tile + 1) * TT > P.V || row0 + TR > P.R)  // workgroup-uniform
-        wide_tile<true>(P, in, tile, row0, stage0, stage1, misc, sink);
-    else
-        wide_tile<false>(P, in, tile, row0, stage0, stage1, misc, sink);
+    const bool ragged = (tile + 1) * TT > P.V || row0 + TR > P.R;  // workgroup-uniform
+    if constexpr (FULL) {
+        if (ragged)
+            wide_tile_full<true>(P, in, tile, row0, stage0, stage1, misc, sink);
+        else
+            wide_tile_full<false>(P, in, tile, row0, stage0, stage1, misc, sink);
+    } else {
+        if (ragged)
+            wide_tile<true>(P, in, tile, row0, stage0, stage1, misc, sink);
+        else
+            wide_tile<false>(P, in, tile, row0, stage0, stage1, misc, sink);
+    }
 }
 
 }  // namespace
 
-bool use_wide_lmhead(const Plan &p) { return p.dtype == kBF16 && !p.full && p.R >= kWideMinRows; }
+bool use_wide_lmhead(const Plan &p) { return p.dtype == kBF16 && p.R >= kWideMinRows; }
 
 hipError_t launch_lmhead_wide(const Plan &p, const Inputs &in, hipStream_t st) {
     const int nrt = (p.R + TR - 1) / TR;
     const int groups = ((p.ntiles + 7) / 8) * 8 * nrt;
-    hipLaunchKernelGGL(lmhead_wide_kernel, dim3(groups), dim3(NT), 0, st, p, in);
+    if (p.full)
+        hipLaunchKernelGGL(lmhead_wide_kernel<true>, dim3(groups), dim3(NT), 0, st, p, in);
+    else
+        hipLaunchKernelGGL(lmhead_wide_kernel<false>, dim3(groups), dim3(NT), 0, st, p, in);
     return hipGetLastError();
 }
 

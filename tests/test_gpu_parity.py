@@ -90,12 +90,13 @@ def test_many_rows_ragged(seed):
     _check_greedy(case, _greedy_tokens(case), f"many rows seed {seed}")
 
 
-def test_many_rows_tiny_hidden_and_vocabulary():
+@pytest.mark.parametrize("theta", [0.1, 0.0])
+def test_many_rows_tiny_hidden_and_vocabulary(theta):
     # the many-row kernel's extreme tails: 8- and 24-element rows (one K chunk, most of
     # it past the row end) and a vocabulary of one full tile plus one token
-    case = synth.make_case("b8_batch32x64", 33, B=9, V=257, dp=8, dq=24)
+    case = synth.make_case("b8_batch32x64", 33, B=9, V=257, dp=8, dq=24, theta=theta)
     assert case.R == 576
-    _check_greedy(case, _greedy_tokens(case), "many rows, tiny rows and vocabulary")
+    _check_greedy(case, _greedy_tokens(case), f"many rows, tiny rows and vocabulary, theta {theta}")
 
 
 def test_ragged_fp32():
@@ -110,9 +111,10 @@ def test_mask_and_strength_settings(theta, s):
     _check_greedy(case, tokens, f"theta={theta} s={s}", theta=theta, s=s)
 
 
-@pytest.mark.parametrize("theta,s", [(1.0, 0.5), (0.1, 0.0), (0.3, 2.0), (0.001, 1.0)])
+@pytest.mark.parametrize("theta,s", [(1.0, 0.5), (0.1, 0.0), (0.3, 2.0), (0.001, 1.0), (0.0, 0.5), (0.0, 2.0)])
 def test_mask_and_strength_settings_many_rows(theta, s):
-    # 576 rows: the many-row LM-head kernel under every mask width and strength
+    # 576 rows: the many-row LM-head kernel under every mask width and strength, and
+    # without the mask (its untruncated epilogue)
     case = synth.make_case("b8_batch32x64", 12, B=9, V=2000, dp=256, dq=128)
     tokens = _greedy_tokens(case, theta=theta, s=s)
     _check_greedy(case, tokens, f"many rows theta={theta} s={s}", theta=theta, s=s)
@@ -231,6 +233,35 @@ def test_exact_integer_logits_untruncated_expert_top1():
     np.testing.assert_allclose(g["row_kl"][:, 0], o["row_diag"][:, oracle.RD_KL_PQ], atol=parity.ATOL)
     np.testing.assert_allclose(g["row_kl"][:, 1], o["row_diag"][:, oracle.RD_KL_PCD],
                                atol=(1 + case.s) * parity.ATOL)
+
+
+def test_exact_integer_logits_untruncated_many_rows():
+    """theta = 0 through the many-row kernel with exact integer logits: the expert max
+    ties across vocabulary tiles and across the two token halves of a tile, so the
+    expert's top-1 (the lowest tied token) and the argmax are compared exactly."""
+    rng = np.random.default_rng(16)
+    V = 3001
+    case = synth.make_case("b8_batch32x64", 16, B=9, V=V, dp=128, dq=64, theta=0.0)
+    assert case.R == 576
+    for name, d in (("hp", 128), ("hq", 64)):
+        setattr(case, name, synth.bf16_bits(rng.integers(-1, 2, (case.R, d)).astype(np.float32)))
+    case.wp = synth.bf16_bits(rng.integers(-1, 2, (V, 128)).astype(np.float32))
+    case.wq = synth.bf16_bits(rng.integers(-1, 2, (V, 64)).astype(np.float32))
+    case.bias[:] = 0
+    tokens = _greedy_tokens(case)
+    _say("exact integer logits, theta 0, many rows")
+    o = _oracle_greedy(case, tokens)
+    g = _runner().from_case(case, tokens).run("greedy")
+    zp = oracle.eval_rows(case.hp, case.hq, case.wp, case.wq, case.bias, case.bias, theta=0.0,
+                          s=case.s, want_logits=True)["zp"]
+    cross = sum(len(set(np.flatnonzero(z == z.max()) // 128)) > 1 for z in zp)
+    assert cross >= 20, "the case must tie the expert max across token halves"
+    assert np.array_equal(g["row_argmax_expert"], o["row_diag"][:, oracle.RD_ARGMAX_P])
+    assert np.array_equal(g["row_argmax"], o["row_argmax"])
+    assert np.array_equal(g["accept_len"], o["accept_len"])
+    np.testing.assert_allclose(g["row_stats"][:, oracle.RS_MAXP], o["row_stats"][:, oracle.RS_MAXP],
+                               rtol=0, atol=0)
+    np.testing.assert_allclose(g["row_kl"][:, 0], o["row_diag"][:, oracle.RD_KL_PQ], atol=parity.ATOL)
 
 
 def test_duplicate_sibling_tokens():
@@ -490,7 +521,7 @@ def test_sampled_trees_small(seed, theta, s):
          f"accept lengths {g['accept_len'].tolist()}")
 
 
-@pytest.mark.parametrize("seed,theta,s", [(3, 0.1, 0.5), (4, 0.3, 1.0)])
+@pytest.mark.parametrize("seed,theta,s", [(3, 0.1, 0.5), (4, 0.3, 1.0), (5, 0.0, 0.5)])
 def test_sampled_trees_many_rows(seed, theta, s):
     """Sampled verification of 9 trees of 64 nodes (576 rows): the many-row LM-head
     kernel feeding the walk decisions settled per row."""

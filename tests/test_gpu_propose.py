@@ -85,6 +85,18 @@ def test_propose_128_row_shape(theta):
     _check(case, u, f"128-row shape theta {theta}")
 
 
+@pytest.mark.parametrize("theta", [0.0, 0.1])
+def test_propose_many_rows(theta):
+    """520 rows: the many-row LM-head kernel (untruncated: the dense y rows the
+    proposals are read from, written over the expert logits), a ragged row tile."""
+    rng = np.random.default_rng(65)
+    case = synth.make_case("s8_chain16x8", 65, B=65, N=8, V=3001, dp=256, dq=128, theta=theta)
+    assert case.R == 520
+    case.wp, case.wq = _drafter_heads(case, rng)
+    u = rng.random(case.R).astype(np.float32)
+    _check(case, u, f"many rows theta {theta}")
+
+
 def test_propose_fp32_ragged_k():
     case = synth.make_case("tiny_chain8", 61, N=19, V=777, dp=100, dq=36, theta=0.02)
     u = np.random.default_rng(61).random(case.R).astype(np.float32)
