@@ -218,9 +218,8 @@ def main():
     nodes_per_s = R / (ms_step * 1e-3)
     kbytes = lmhead_bytes(case)
     flops = 2 * R * (case.dp + case.dq) * case.V
-    # many rows (bf16, masked target) go to the compute-shaped LM-head kernel
-    kernel = ("lmhead_wide_kernel" if case.dtype == "bf16" and case.theta > 0 and R >= 512
-              else "lmhead_kernel")
+    # many rows (bf16, with or without the mask) go to the compute-shaped LM-head kernel
+    kernel = "lmhead_wide_kernel" if case.dtype == "bf16" and R >= 512 else "lmhead_kernel"
     ridge = MFMA_BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9)
     # committed counters: per kernel and workload, and per mode and theta where they
     # differ from the workload's own
