@@ -1,7 +1,7 @@
 // LM-head projection for many rows (the compute-bound regime), with the same
-// softmax-partials and candidate epilogue as the streaming kernel (Alg. 1 "parallel
-// model evaluation", the per-tile pieces of Eq. (1) and the plausibility mask of
-// Sec. 2.1).
+// epilogues as the streaming kernel (Alg. 1 "parallel model evaluation", the
+// per-tile pieces of Eq. (1); with the plausibility mask of Sec. 2.1 or, at
+// theta = 0, the untruncated target).
 //
 // With thousands of rows (many sequences verified together) the projection is a
 // dense GEMM far above the MFMA ridge, so the tile is shaped for reuse rather
@@ -18,7 +18,9 @@
 // both models, tile-local candidates (z_p within ln(theta) of the tile max)
 // pruned against the running row bound.  It works one 16-row block at a time and
 // recomputes logits from the accumulators; the block's logits also go to an LDS
-// buffer so that a lane can fetch the one of a given token.
+// buffer so that a lane can fetch the one of a given token.  Untruncated target:
+// per (row, tile) the statistics of y = (1+s) z_p - s z_q instead of candidates
+// (wide_tile_full).
 #include "dcd_internal.h"
 
 namespace dcd {
