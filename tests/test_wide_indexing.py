@@ -1,4 +1,4 @@
-"""CPU model of the global-load addresses of the many-row LM-head kernel
+"""CPU model of the global addresses of the many-row LM-head kernel
 (paper_2608_12913_amd/csrc/lmhead_wide.hip: workgroup -> tile mapping, Stream::init,
 Stream::issue), checked for every lane, load and K-chunk of the ragged workgroups:
 every address stays inside its operand and every 32-bit lane offset is non-negative
@@ -56,3 +56,38 @@ def _check(R, V, d):
                                    (512, 300, 64), (513, 257, 8), (576, 257, 24), (2049, 128256, 256)])
 def test_ragged_load_addresses_stay_in_bounds(R, V, d):
     assert _check(R, V, d) > 0
+
+
+def _check_dense_rows(R, V):
+    """The untruncated epilogue's float4 accesses to the dense rows [R][tiles*256]:
+    row = row0 + 128 wr + 16 rb + lane%16 (clamped to R-1 for loads, skipped past R for
+    stores), column = tile*256 + 128 wt + 4 (lane/16) + 16 vb .. +3, for every workgroup
+    the kernel launches."""
+    ntiles, nrt = (V + TT - 1) // TT, (R + 256 - 1) // 256
+    zstride = ntiles * TT
+    lane = np.arange(64)
+    rb, vb, ln = np.meshgrid(np.arange(8), np.arange(8), lane, indexing="ij")
+    n, g = ln % 16, ln // 16
+    checked = 0
+    for gid in range((ntiles + 7) // 8 * 8 * nrt):
+        xcd, local = gid % 8, gid // 8
+        tile = (local // nrt) * 8 + xcd
+        if tile >= ntiles:
+            continue
+        row0 = (local % nrt) * 256
+        for wave in range(4):
+            wt, wr = wave & 1, wave >> 1
+            row = row0 + 128 * wr + 16 * rb + n
+            col = tile * TT + 128 * wt + 4 * g + 16 * vb
+            assert np.all(col % 4 == 0) and np.all(col + 4 <= zstride)
+            load = np.minimum(row, R - 1) * zstride + col
+            assert np.all(load >= 0) and np.all(load + 4 <= R * zstride)
+            store = (row * zstride + col)[row < R]
+            assert np.all(store + 4 <= R * zstride)
+            checked += row.size
+    return checked
+
+
+@pytest.mark.parametrize("R,V", [(512, 300), (520, 3001), (576, 257), (2048, 128256)])
+def test_untruncated_dense_row_accesses_stay_in_bounds(R, V):
+    assert _check_dense_rows(R, V) > 0
