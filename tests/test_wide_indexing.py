@@ -1,6 +1,7 @@
 """CPU model of the global addresses of the many-row LM-head kernel
 (paper_2608_12913_amd/csrc/lmhead_wide.hip: workgroup -> tile mapping, Stream::init,
-Stream::issue), checked for every lane, load and K-chunk of the ragged workgroups:
+Stream::dma, Stream::prefetch), checked for every lane, load and K-chunk of the ragged
+workgroups:
 every address stays inside its operand and every 32-bit lane offset is non-negative
 and below 2^32.  The kernel's ragged path once formed a negative offset from a slab
 that starts past the last row (a GPU memory fault); this guards the fix."""
@@ -40,15 +41,21 @@ def _check(R, V, d):
                 base = min(first, count - 1)          # the slab's base row, clamped
                 skip, last = first - base, count - 1 - base
                 assert skip >= 0 and last >= 0
-                for c in range(nch):
-                    col = c * CB + col16 * 16
-                    col = np.where(col < rowbytes, col, rowbytes - 16)  # weights; hidden: 0
-                    rel = np.minimum(skip + RPI * q + r, last)
-                    off = rel * rowbytes + col
-                    assert np.all(off >= 0) and np.all(off < 2 ** 32)
-                    byte = base * rowbytes + off
-                    assert np.all(byte >= 0) and np.all(byte + 16 <= count * rowbytes)
-                    checked += off.size
+                for c in range(nch + 2):  # the L2 prefetch runs two chunks ahead
+                    if c < nch:
+                        col = c * CB + col16 * 16
+                        col = np.where(col < rowbytes, col, rowbytes - 16)  # weights; hidden: 0
+                        rel = np.minimum(skip + RPI * q + r, last)
+                        off = rel * rowbytes + col
+                        assert np.all(off >= 0) and np.all(off < 2 ** 32)
+                        byte = base * rowbytes + off
+                        assert np.all(byte >= 0) and np.all(byte + 16 <= count * rowbytes)
+                        checked += off.size
+                    # the prefetch: 4 bytes of slab row `lane` at the chunk's start
+                    # (clamped to the row's last 16 bytes)
+                    poff = np.minimum(skip + lane, last) * rowbytes + min(c * CB, rowbytes - 16)
+                    assert np.all(poff >= 0) and np.all(poff < 2 ** 32)
+                    assert np.all(base * rowbytes + poff + 4 <= count * rowbytes)
     return checked
 
 
